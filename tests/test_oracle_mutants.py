@@ -1,0 +1,103 @@
+"""Strength of the oracle pins: plausible mistakes planted in a copy of the
+oracle (on the CPU, never on a device) must each be caught by the pin battery
+(hand-worked closed-form examples plus finite differences)."""
+
+import importlib.util
+import json
+import math
+import os
+import types
+
+import numpy as np
+import pytest
+
+import oracle.noble_oracle as good
+from paper_2603_06492_amd import inputs as inp
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+MUTATIONS = {
+    "forward_mixing_transposed": ("H2 = C1 @ _f64(M)", "H2 = C1 @ _f64(M).T"),
+    "phase2_dropped": ("A2 = H2 * _f64(omega2) + _f64(phi2)", "A2 = H2 * _f64(omega2)"),
+    "bias_dropped": ("Y = Y + _f64(b)", "Y = Y"),
+    "sin_sign_outer": ("dA2 = -np.sin(f[\"A2\"]) * dC2", "dA2 = np.sin(f[\"A2\"]) * dC2"),
+    "sin_sign_inner": ("dA1 = -np.sin(f[\"A1\"]) * dC1", "dA1 = np.sin(f[\"A1\"]) * dC1"),
+    "dC1_not_transposed": ("dC1 = dH2 @ _f64(M).T", "dC1 = dH2 @ _f64(M)"),
+    "dM_transposed": ("dM = f[\"C1\"].T @ dH2", "dM = dH2.T @ f[\"C1\"]"),
+    "domega1_dropped_H": ("domega1 = np.sum(dA1 * H, axis=0)", "domega1 = np.sum(dA1, axis=0)"),
+    "domega2_wrong_factor": ("domega2 = np.sum(dA2 * f[\"H2\"], axis=0)",
+                             "domega2 = np.sum(dA2 * f[\"C1\"], axis=0)"),
+    "dH_missing_omega1": ("dH = dA1 * w1", "dH = dA1"),
+    "dH2_missing_omega2": ("dH2 = dA2 * w2", "dH2 = dA2"),
+    "dx_missing_branch": ("out[\"dx\"] = dy @ W.T + dH @ D.T", "out[\"dx\"] = dy @ W.T"),
+    "dW_up_uses_cos_argument": ("\"dW_up\": cb[\"C2\"].T @ dy", "\"dW_up\": np.cos(cb[\"C2\"]).T @ dy"),
+}
+
+
+def _mutant(name):
+    old, new = MUTATIONS[name]
+    src = open(good.__file__).read()
+    assert src.count(old) == 1, name
+    mod = types.ModuleType(f"oracle_mutant_{name}")
+    exec(compile(src.replace(old, new), f"<mutant {name}>", "exec"), mod.__dict__)
+    return mod
+
+
+def _eval(v):
+    if isinstance(v, list):
+        return np.array([_eval(e) for e in v], dtype=np.float64)
+    if isinstance(v, str):
+        return float(eval(v, {"__builtins__": {}}, {"pi": math.pi, "sqrt": math.sqrt}))
+    return float(v)
+
+
+def _battery_passes(mod):
+    """True when every pin in the battery holds for oracle module ``mod``."""
+    def fwd(p):
+        return mod.forward(p["x"], p["W"], p["b"], p["W_down"], p["omega1"], p["phi1"],
+                           p["M"], p["omega2"], p["phi2"], p["W_up"])
+
+    def bwd(p):
+        return mod.backward(p["dy"], p["x"], p["W"], p["W_down"], p["omega1"], p["phi1"],
+                            p["M"], p["omega2"], p["phi2"], p["W_up"])
+
+    with open(os.path.join(GOLDEN, "hand_examples.json")) as f:
+        for ex in json.load(f)["examples"]:
+            p = {k: _eval(v) for k, v in ex["inputs"].items()}
+            e = {k: _eval(v) for k, v in ex["expected"].items()}
+            Y, _ = fwd(p)
+            if not np.allclose(Y, e["y"], rtol=0, atol=1e-12):
+                return False
+            g = bwd(p)
+            for k in e:
+                if k in g and not np.allclose(g[k], e[k], rtol=0, atol=1e-11):
+                    return False
+    p = {k: v.astype(np.float64) for k, v in
+         inp.draw_projection("t", 4, 5, 6, 3, "f32", 21, bias_std=0.5).arrays.items()}
+    g = bwd(p)
+
+    def loss(q):
+        return float(np.sum(q["dy"] * fwd(q)[0]))
+
+    pairs = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "M": "dM", "W_up": "dW_up",
+             "omega1": "domega1", "phi1": "dphi1", "omega2": "domega2", "phi2": "dphi2"}
+    for pn, gn in pairs.items():
+        for idx in np.ndindex(p[pn].shape):
+            qp, qm = dict(p), dict(p)
+            qp[pn] = p[pn].copy()
+            qm[pn] = p[pn].copy()
+            qp[pn][idx] += 1e-6
+            qm[pn][idx] -= 1e-6
+            fd = (loss(qp) - loss(qm)) / 2e-6
+            if abs(fd - g[gn][idx]) > 1e-6 * max(1.0, abs(g[gn][idx])):
+                return False
+    return True
+
+
+def test_battery_accepts_the_oracle():
+    assert _battery_passes(good)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_battery_rejects_mutant(name):
+    assert not _battery_passes(_mutant(name))

@@ -1,0 +1,303 @@
+"""Pins of the fp64 oracle against things fixed outside it (CPU only).
+
+* hand-worked closed-form examples of Eq. (1)-(2) (tests/golden/hand_examples.json)
+* Table 1 "Params+" from the branch's parameter shapes
+* central finite differences of L = sum(dy * y) for every gradient
+* an independently written torch forward differentiated by autograd (fp64)
+* special cases with closed forms (W_up = 0, omega2 = 0, omega1 = 0, M = 0)
+* invariants: evenness of cos, 2 pi periodicity, rescaling of W_down, row
+  permutation, and the |C2| <= 1 bound on the branch
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2603_06492_amd import inputs as inp
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+GRADS = ("dx", "dW", "db", "dW_down", "dM", "dW_up", "domega1", "dphi1", "domega2", "dphi2")
+
+
+def _eval(v):
+    if isinstance(v, str):
+        return float(eval(v, {"__builtins__": {}}, {"pi": math.pi, "sqrt": math.sqrt}))
+    return float(v)
+
+
+def _arr(v):
+    if isinstance(v, list):
+        return np.array([_arr(e) for e in v], dtype=np.float64)
+    return _eval(v)
+
+
+def _fwd(p):
+    return oracle.forward(p["x"], p["W"], p["b"], p["W_down"], p["omega1"], p["phi1"],
+                          p["M"], p["omega2"], p["phi2"], p["W_up"])
+
+
+def _bwd(p, **kw):
+    return oracle.backward(p["dy"], p["x"], p["W"], p["W_down"], p["omega1"], p["phi1"],
+                           p["M"], p["omega2"], p["phi2"], p["W_up"], **kw)
+
+
+def _tiny(seed=3, T=5, d_in=7, d_out=6, r=3):
+    p = inp.draw_projection("tiny", T, d_in, d_out, r, "f32", seed, bias_std=0.5)
+    return {k: v.astype(np.float64) for k, v in p.arrays.items()}
+
+
+# ---------------------------------------------------------------- golden -----
+
+def _hand_examples():
+    with open(os.path.join(GOLDEN, "hand_examples.json")) as f:
+        return json.load(f)["examples"]
+
+
+@pytest.mark.parametrize("ex", _hand_examples(), ids=lambda e: e["name"])
+def test_hand_worked_examples(ex):
+    p = {k: _arr(v) for k, v in ex["inputs"].items()}
+    exp = {k: _arr(v) for k, v in ex["expected"].items()}
+    Y, H = _fwd(p)
+    np.testing.assert_allclose(Y, exp["y"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(H, exp["H"], rtol=0, atol=1e-12)
+    g = _bwd(p)
+    for k in GRADS:
+        np.testing.assert_allclose(g[k], exp[k], rtol=0, atol=1e-11, err_msg=k)
+
+
+def test_mixing_orientation_is_distinguished():
+    """The r = 2 example gives a different y under the transposed mixing."""
+    ex = [e for e in _hand_examples() if e["name"] == "mixing_orientation_r2"][0]
+    p = {k: _arr(v) for k, v in ex["inputs"].items()}
+    p_t = dict(p, M=p["M"].T.copy())
+    Y, _ = _fwd(p)
+    Yt, _ = _fwd(p_t)
+    assert abs(Y[0, 0] - Yt[0, 0]) > 1.0
+
+
+def test_table1_params_plus():
+    with open(os.path.join(GOLDEN, "table1_params_plus.json")) as f:
+        t1 = json.load(f)
+    V = t1["vocab"]
+    for row in t1["rows"]:
+        L, d, r = row["layers"], row["width"], row["rank"]
+        h = math.ceil(8 * d / 3 / 64) * 64
+        # untied input embedding and LM head, Q K V O, fused GeGLU up (d -> 2h),
+        # down (h -> d), two RMSNorm gains per block and a final one
+        base = 2 * V * d + L * (4 * d * d + 2 * h * d + h * d + 2 * d) + d
+
+        def branch(di, do):
+            return sum(int(np.prod(s)) for s in oracle.branch_param_shapes(di, do, r).values())
+
+        extra = L * (4 * branch(d, d) + branch(d, 2 * h) + branch(h, d))
+        pct = 100.0 * extra / base
+        assert abs(pct - row["params_plus_pct"]) < 0.1, (row, pct)
+
+
+# ------------------------------------------------------- finite differences --
+
+def test_gradients_match_central_differences():
+    p = _tiny()
+    g = _bwd(p)
+
+    def loss(q):
+        Y, _ = _fwd(q)
+        return float(np.sum(q["dy"] * Y))
+
+    names = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "M": "dM", "W_up": "dW_up",
+             "omega1": "domega1", "phi1": "dphi1", "omega2": "domega2", "phi2": "dphi2"}
+    for pname, gname in names.items():
+        base = p[pname]
+        fd = np.zeros_like(base)
+        for idx in np.ndindex(base.shape):
+            h = 1e-6 * max(1.0, abs(base[idx]))
+            qp = dict(p)
+            qp[pname] = base.copy()
+            qp[pname][idx] += h
+            qm = dict(p)
+            qm[pname] = base.copy()
+            qm[pname][idx] -= h
+            fd[idx] = (loss(qp) - loss(qm)) / (2 * h)
+        scale = max(1.0, float(np.max(np.abs(g[gname]))))
+        assert np.max(np.abs(fd - g[gname])) <= 1e-6 * scale, gname
+
+
+def test_gradients_match_torch_autograd():
+    torch = pytest.importorskip("torch")
+    p = _tiny(seed=11, T=9, d_in=16, d_out=24, r=8)
+    t = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True) for k, v in p.items()}
+    # independent formulation: column-vector CosNet with the mixing written as
+    # an explicit sum over the input rank, per token
+    h = t["x"] @ t["W_down"]
+    c1 = torch.cos(t["omega1"] * h + t["phi1"])
+    h2 = (c1[:, :, None] * t["M"][None, :, :]).sum(dim=1)
+    branch = torch.cos(t["omega2"] * h2 + t["phi2"]) @ t["W_up"]
+    y = t["x"] @ t["W"] + t["b"] + branch
+    (y * t["dy"]).sum().backward()
+    g = _bwd(p)
+    Y, _ = _fwd(p)
+    np.testing.assert_allclose(Y, y.detach().numpy(), rtol=0, atol=1e-12)
+    names = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "M": "dM", "W_up": "dW_up",
+             "omega1": "domega1", "phi1": "dphi1", "omega2": "domega2", "phi2": "dphi2"}
+    for pname, gname in names.items():
+        np.testing.assert_allclose(g[gname], t[pname].grad.numpy(), rtol=1e-10, atol=1e-10,
+                                   err_msg=gname)
+
+
+# ------------------------------------------------------------- closed forms --
+
+def test_zero_up_projection_collapses_to_linear():
+    p = _tiny(seed=5)
+    p["W_up"] = np.zeros_like(p["W_up"])
+    Y, _ = _fwd(p)
+    np.testing.assert_array_equal(Y, p["x"] @ p["W"] + p["b"])
+    g = _bwd(p)
+    for k in ("dW_down", "dM", "domega1", "dphi1", "domega2", "dphi2"):
+        np.testing.assert_array_equal(g[k], 0.0, err_msg=k)
+    np.testing.assert_array_equal(g["dx"], p["dy"] @ p["W"].T)
+    np.testing.assert_array_equal(g["dW"], p["x"].T @ p["dy"])
+    np.testing.assert_allclose(g["db"], p["dy"].sum(axis=0), rtol=0, atol=1e-14)
+
+
+def test_zero_second_frequency_gives_constant_branch():
+    p = _tiny(seed=6)
+    p["omega2"] = np.zeros_like(p["omega2"])
+    Y, _ = _fwd(p)
+    c = np.cos(p["phi2"])
+    np.testing.assert_allclose(Y, p["x"] @ p["W"] + p["b"] + c @ p["W_up"], rtol=0, atol=1e-13)
+    g = _bwd(p)
+    sg = p["dy"].sum(axis=0)
+    np.testing.assert_allclose(g["dW_up"], np.outer(c, sg), rtol=0, atol=1e-13)
+    np.testing.assert_allclose(g["dphi2"], -np.sin(p["phi2"]) * (p["W_up"] @ sg), rtol=0, atol=1e-13)
+    for k in ("dM", "domega1", "dphi1", "dW_down"):
+        np.testing.assert_array_equal(g[k], 0.0, err_msg=k)
+    np.testing.assert_allclose(g["dx"], p["dy"] @ p["W"].T, rtol=0, atol=1e-14)
+
+
+def test_zero_first_frequency_gives_constant_branch():
+    p = _tiny(seed=7)
+    p["omega1"] = np.zeros_like(p["omega1"])
+    Y, _ = _fwd(p)
+    row = np.cos((np.cos(p["phi1"]) @ p["M"]) * p["omega2"] + p["phi2"]) @ p["W_up"]
+    np.testing.assert_allclose(Y, p["x"] @ p["W"] + p["b"] + row, rtol=0, atol=1e-13)
+    g = _bwd(p)
+    np.testing.assert_array_equal(g["dW_down"], 0.0)
+    np.testing.assert_allclose(g["dx"], p["dy"] @ p["W"].T, rtol=0, atol=1e-14)
+    assert np.max(np.abs(g["domega1"])) > 1e-3
+
+
+def test_zero_mixing_matrix():
+    p = _tiny(seed=8)
+    p["M"] = np.zeros_like(p["M"])
+    Y, _ = _fwd(p)
+    np.testing.assert_allclose(Y, p["x"] @ p["W"] + p["b"] + np.cos(p["phi2"]) @ p["W_up"],
+                               rtol=0, atol=1e-13)
+    g = _bwd(p)
+    for k in ("domega1", "dphi1", "dW_down"):
+        np.testing.assert_array_equal(g[k], 0.0, err_msg=k)
+    assert np.max(np.abs(g["dM"])) > 1e-3
+    # dM = C1^T dH2 with C1 = cos(H w1 + p1), dH2 = -sin(p2) * dC2 * w2
+    C1 = np.cos((p["x"] @ p["W_down"]) * p["omega1"] + p["phi1"])
+    dH2 = -np.sin(p["phi2"]) * (p["dy"] @ p["W_up"].T) * p["omega2"]
+    np.testing.assert_allclose(g["dM"], C1.T @ dH2, rtol=0, atol=1e-12)
+
+
+# --------------------------------------------------------------- invariants --
+
+@pytest.mark.parametrize("k", [1, 2])
+def test_evenness_of_cosine(k):
+    p = _tiny(seed=9)
+    q = dict(p)
+    q[f"omega{k}"] = -p[f"omega{k}"]
+    q[f"phi{k}"] = -p[f"phi{k}"]
+    Yp, _ = _fwd(p)
+    Yq, _ = _fwd(q)
+    np.testing.assert_allclose(Yq, Yp, rtol=0, atol=1e-12)
+    gp, gq = _bwd(p), _bwd(q)
+    for n in ("dx", "dW", "dW_down", "dM", "dW_up", "db"):
+        np.testing.assert_allclose(gq[n], gp[n], rtol=0, atol=1e-11, err_msg=n)
+    for n in (f"domega{k}", f"dphi{k}"):
+        np.testing.assert_allclose(gq[n], -gp[n], rtol=0, atol=1e-11, err_msg=n)
+
+
+def test_phase_periodicity():
+    p = _tiny(seed=10)
+    q = dict(p, phi1=p["phi1"] + 2 * np.pi, phi2=p["phi2"] - 2 * np.pi)
+    np.testing.assert_allclose(_fwd(q)[0], _fwd(p)[0], rtol=0, atol=1e-12)
+    gp, gq = _bwd(p), _bwd(q)
+    for n in GRADS:
+        np.testing.assert_allclose(gq[n], gp[n], rtol=0, atol=1e-11, err_msg=n)
+
+
+def test_down_projection_rescaling():
+    p = _tiny(seed=12)
+    s = np.array([0.5, 2.0, -1.5])
+    q = dict(p, W_down=p["W_down"] * s, omega1=p["omega1"] / s)
+    np.testing.assert_allclose(_fwd(q)[0], _fwd(p)[0], rtol=0, atol=1e-12)
+    gp, gq = _bwd(p), _bwd(q)
+    np.testing.assert_allclose(gq["domega1"], s * gp["domega1"], rtol=0, atol=1e-11)
+    np.testing.assert_allclose(gq["dW_down"], gp["dW_down"] / s, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(gq["dx"], gp["dx"], rtol=0, atol=1e-11)
+
+
+def test_row_permutation():
+    p = _tiny(seed=13, T=11)
+    perm = np.random.default_rng(0).permutation(11)
+    q = dict(p, x=p["x"][perm], dy=p["dy"][perm])
+    np.testing.assert_allclose(_fwd(q)[0], _fwd(p)[0][perm], rtol=0, atol=1e-13)
+    gp, gq = _bwd(p), _bwd(q)
+    np.testing.assert_allclose(gq["dx"], gp["dx"][perm], rtol=0, atol=1e-12)
+    for n in GRADS[1:]:
+        np.testing.assert_allclose(gq[n], gp[n], rtol=0, atol=1e-11, err_msg=n)
+
+
+def test_branch_bound():
+    p = _tiny(seed=14, T=64, d_in=32, d_out=48, r=8)
+    Y, _ = _fwd(p)
+    dev = np.abs(Y - p["x"] @ p["W"] - p["b"])
+    assert np.all(dev <= np.abs(p["W_up"]).sum(axis=0)[None, :] + 1e-12)
+
+
+def test_row_selection_matches_full():
+    p = _tiny(seed=15, T=17, d_in=9, d_out=10, r=4)
+    rows = np.array([0, 5, 16])
+    Y, _ = _fwd(p)
+    Ys, _ = _fwd(dict(p, x=p["x"][rows]))
+    np.testing.assert_allclose(Ys, Y[rows], rtol=0, atol=1e-13)
+    g = _bwd(p)
+    gs = _bwd(p, dx_rows=rows, dW_rows=np.array([1, 8]))
+    np.testing.assert_allclose(gs["dx"], g["dx"][rows], rtol=0, atol=1e-13)
+    np.testing.assert_allclose(gs["dW"], g["dW"][[1, 8]], rtol=0, atol=1e-13)
+
+
+# ----------------------------------------------------------- input recipe ----
+
+def test_bf16_rounding_matches_torch():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(1)
+    a = (rng.standard_normal(100000) * np.exp(rng.uniform(-20, 20, 100000))).astype(np.float32)
+    # exact ties: low 16 bits 0x8000 with even and odd bf16 mantissas
+    ties = np.array([0x3F808000, 0x3F818000, 0xBF808000, 0x40490000 | 0x8000], dtype=np.uint32).view(np.float32)
+    a = np.concatenate([a, ties])
+    mine = inp.bf16_bits(a)
+    ref = torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(mine, ref)
+
+
+def test_input_recipe_is_seeded_and_shaped():
+    p = inp.draw_workload_projection("llm250m_r64", 0, T=64)
+    q = inp.draw_workload_projection("llm250m_r64", 0, T=64)
+    for k in p.arrays:
+        np.testing.assert_array_equal(p[k], q[k])
+    assert p["x"].shape == (64, 1024) and p["W"].shape == (1024, 3072)
+    assert p["W_down"].shape == (1024, 64) and p["M"].shape == (64, 64)
+    assert p["W_up"].shape == (64, 3072) and p["dy"].shape == (64, 3072)
+    # bf16 storage tensors hold bf16-exact values
+    for k in inp.STORAGE:
+        np.testing.assert_array_equal(inp.round_bf16(p[k]), p[k])
+    assert np.all(p["b"] == 0)
+    assert 0 <= p["phi1"].min() and p["phi1"].max() < 2 * np.pi
