@@ -1,0 +1,224 @@
+#!/usr/bin/env python3
+"""Throughput of the NOBLE-CosNet linear layer (forward + backward) on one MI355X.
+
+A step is the forward of every projection of the workload in order, then the
+backward of each in reverse order, on one stream (inputs already resident in
+HBM).  The default workload is one block of the 1.5B-style LLM: T = 8 x 1024
+tokens, d = 2048, r = 128, projections QKV 2048->6144, O 2048->2048, FFN up
+2048->8192, FFN down 8192->2048.
+
+Reported: algorithmic TFLOP/s, 6 T [d_in d_out + r (d_in + d_out) + r^2] per
+projection over the step time; the same step with r = 0 (plain linear, same
+kernels) and the overhead over it; the roofline of the main MFMA GEMM; and the
+fp64 oracle's throughput on a bounded sample on the host cores.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15   # dense bf16 MFMA, MI355X
+PEAK_F32 = 157.3e12  # dense fp32 MFMA, MI355X
+METRIC = "NOBLE linear fwd+bwd TFLOP/s, % bf16 MFMA peak, overhead vs plain GEMM"
+
+
+def flop_alg(T, d_in, d_out, r):
+    return 6.0 * T * (d_in * d_out + r * (d_in + d_out) + r * r)
+
+
+def cpu_baseline(workload: str, budget_s: float = 12.0):
+    """fp64 oracle fwd+bwd on a prefix sample of tokens of the same workload."""
+    import oracle  # test infrastructure: only this leg of the bench uses it
+    from paper_2603_06492_amd import inputs as inp
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    shapes = inp.workload_shapes(workload)
+    T_full = shapes[0][1]
+    Ts = 128
+    while True:
+        projs = [inp.draw_workload_projection(workload, i, T=Ts) for i in range(len(shapes))]
+        t0 = time.perf_counter()
+        for p in projs:
+            a = p.arrays
+            oracle.forward(a["x"], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"],
+                           a["omega2"], a["phi2"], a["W_up"])
+            oracle.backward(a["dy"], a["x"], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"],
+                            a["omega2"], a["phi2"], a["W_up"])
+        dt = time.perf_counter() - t0
+        if dt >= budget_s / 4 or Ts * 2 > T_full:
+            break
+        Ts *= 2
+    flops = sum(flop_alg(Ts, di, do, r) for (_, _, di, do, r) in shapes)
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{Ts} of {T_full} tokens of every projection, numpy float64, one fwd+bwd pass",
+            "seconds": round(dt, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llm1p5b_block_r128")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--roofline-launches", type=int, default=20,
+                    help="timed launches of the plain main GEMM for the roofline entry")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build's kernels run on a single MI355X and "
+              "have no multi-GPU path (rerun with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2603_06492_amd import inputs as inp
+    from paper_2603_06492_amd.runner import DeviceProblem
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+
+    wl = inp.WORKLOADS[args.workload]
+    shapes = inp.workload_shapes(args.workload)
+    print(f"[bench] workload {args.workload}: {len(shapes)} projections, T={wl['T']}, r={wl['r']}",
+          file=sys.stderr, flush=True)
+    probs, plain = [], []
+    for i in range(len(shapes)):
+        p = inp.draw_workload_projection(args.workload, i)
+        dp = DeviceProblem(p)
+        probs.append(dp)
+        plain.append(DeviceProblem(p, branch=False, inputs_from=dp))
+        del p
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def step(ps):
+        for dp in ps:
+            dp.fwd()
+        for dp in reversed(ps):
+            dp.bwd()
+
+    def timed(ps, K, W):
+        for _ in range(W):
+            step(ps)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        ev0.record(stream)
+        for _ in range(K):
+            step(ps)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return ev0.elapsed_time(ev1) / K, wall / K * 1e3
+
+    ms_noble, wall_noble = timed(probs, args.steps, args.warmup)
+    print(f"[bench] noble step {ms_noble:.3f} ms", file=sys.stderr, flush=True)
+    ms_plain, wall_plain = timed(plain, args.steps, args.warmup)
+    print(f"[bench] plain step {ms_plain:.3f} ms", file=sys.stderr, flush=True)
+
+    # Per-projection fwd / bwd times (events between calls on the same stream).
+    per = []
+    for dp, d0 in zip(probs, plain):
+        T, di, do, r = dp.p.T, dp.p.d_in, dp.p.d_out, dp.p.r
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        reps = max(3, args.steps // 2)
+        for _ in range(2):
+            dp.fwd(); dp.bwd(); d0.fwd(); d0.bwd()
+        torch.cuda.synchronize()
+        evs[0].record(stream)
+        for _ in range(reps):
+            dp.fwd()
+        evs[1].record(stream)
+        for _ in range(reps):
+            dp.bwd()
+        evs[2].record(stream)
+        for _ in range(reps):
+            d0.fwd()
+        evs[3].record(stream)
+        for _ in range(reps):
+            d0.bwd()
+        evs[4].record(stream)
+        torch.cuda.synchronize()
+        tf, tb, pf, pb = (evs[i].elapsed_time(evs[i + 1]) / reps for i in range(4))
+        fl = flop_alg(T, di, do, r)
+        per.append({"projection": dp.p.name.split("/")[-1], "T": T, "d_in": di, "d_out": do, "r": r,
+                    "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4), "plain_fwd_ms": round(pf, 4),
+                    "plain_bwd_ms": round(pb, 4), "tflops": round(fl / ((tf + tb) * 1e-3) / 1e12, 2),
+                    "overhead": round((tf + tb) / (pf + pb) - 1, 4),
+                    "overhead_floor": round((r * (di + do) + r * r) / (di * do), 4)})
+
+    # Roofline entry: the main bf16 MFMA GEMM (x W, plain forward: exactly one
+    # kernel launch per call), timed over its own launches with HIP events on
+    # the stream it runs on.  Algorithmic FLOPs per launch = 2 T d_in d_out.
+    dom = max(plain, key=lambda d: d.p.d_in * d.p.d_out)
+    for _ in range(3):
+        dom.fwd()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.roofline_launches):
+        dom.fwd()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_launch = e0.elapsed_time(e1) / args.roofline_launches * 1e-3
+    gemm_flops = 2.0 * dom.p.T * dom.p.d_in * dom.p.d_out
+    ach = gemm_flops / t_launch / 1e12
+    roofline = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
+                "frac": round(ach / (PEAK_BF16 / 1e12), 4), "traffic": None,
+                "kernel": f"gemm_kernel x W (plain forward) {dom.p.name.split('/')[-1]} "
+                          f"T={dom.p.T} {dom.p.d_in}->{dom.p.d_out}",
+                "avg_launch_us": round(t_launch * 1e6, 2), "flop_per_launch": gemm_flops}
+
+    flops_step = sum(flop_alg(T, di, do, r) for (_, T, di, do, r) in shapes)
+    main_flops = sum(6.0 * T * di * do for (_, T, di, do, r) in shapes)
+    value = flops_step / (ms_noble * 1e-3) / 1e12
+    floor = sum(T * (r * (di + do) + r * r) for (_, T, di, do, r) in shapes) / \
+        sum(T * di * do for (_, T, di, do, r) in shapes)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_noble, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl["dtype"],
+        "data": "synthetic",
+        "config": {"workload": args.workload, "T": wl["T"], "r": wl["r"],
+                   "projections": [f"{n} {di}->{do}" for (n, _, di, do, _) in shapes]},
+        "pct_bf16_peak": round(100 * value / (PEAK_BF16 / 1e12), 2),
+        "plain_ms_per_step": round(ms_plain, 4),
+        "overhead_vs_plain": round(ms_noble / ms_plain - 1, 4),
+        "overhead_floor": round(floor, 4),
+        "main_gemm_pct_peak": round(100 * main_flops / (ms_plain * 1e-3) / PEAK_BF16, 2),
+        "wall_ms_per_step": round(wall_noble, 4),
+        "roofline": roofline,
+        "per_projection": per,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (fp64 oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(args.workload)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

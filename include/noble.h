@@ -1,0 +1,141 @@
+/*
+ * noble.h - C ABI of libnoble: the NOBLE-CosNet augmented linear layer on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The layer (arXiv 2603.06492, Sec. 3.1 Eq. 1 with the CosNet nonlinearity of
+ * Sec. 3.2 Eq. 2, restated in App. A), rows = tokens:
+ *
+ *   H  = x W_down                       [T, r]
+ *   C1 = cos(H (.) omega1 + phi1)       [T, r]   (per-rank frequency/phase)
+ *   H2 = C1 M                           [T, r]   (M stored [r_in, r_out])
+ *   C2 = cos(H2 (.) omega2 + phi2)      [T, r]
+ *   y  = x W + b + C2 W_up              [T, d_out]
+ *
+ * The backward computes every gradient of L = sum(dy (.) y) by the chain rule
+ * (the paper prints none; d cos(u)/du = -sin(u)), recomputing the cosines from
+ * the saved H instead of storing them.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - All tensors are dense, row-major and contiguous, in device memory owned
+ *    and allocated by the caller.  The library never allocates, frees or
+ *    synchronises, and keeps no state between calls.
+ *  - desc->dtype is the storage type of x, W, W_down, M, W_up, y, dy and dx.
+ *    b, omega1, phi1, omega2, phi2 and every parameter gradient are float32.
+ *    Arithmetic: bf16 operands with float32 accumulation on the bf16 path
+ *    (cosine arguments, cos and sin in float32; C1, C2, dH and the mixing
+ *    gradients are rounded to bf16 only where they feed a matrix product),
+ *    float32 throughout on the f32 path.
+ *  - Shapes: T >= 0 (any value); d_in, d_out >= 8 and multiples of 8;
+ *    r = 0 (plain linear: every branch pointer is ignored and may be NULL) or
+ *    8 <= r <= 128 with r a multiple of 8.  Every pointer must be 16-byte
+ *    aligned.  Outputs must not alias inputs or each other.
+ *  - Argument checking is complete before any HIP call: on any error the call
+ *    returns a status and enqueues nothing.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
+ *    and the call returns without waiting.  Device faults surface at the
+ *    caller's next synchronisation.  Concurrent calls must use separate
+ *    scratch buffers.
+ *  - Only gfx950 devices are supported (NOBLE_ERR_UNSUPPORTED_DEVICE otherwise).
+ */
+#ifndef NOBLE_H
+#define NOBLE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum noble_dtype {
+    NOBLE_BF16 = 0, /* bfloat16 storage, float32 accumulation */
+    NOBLE_F32 = 1   /* float32 storage and arithmetic */
+} noble_dtype;
+
+typedef enum noble_status {
+    NOBLE_OK = 0,
+    NOBLE_ERR_NULL_ARG = 1,          /* a required pointer is NULL */
+    NOBLE_ERR_BAD_SHAPE = 2,         /* dimension out of the ranges above */
+    NOBLE_ERR_BAD_DTYPE = 3,         /* desc->dtype is not a noble_dtype */
+    NOBLE_ERR_MISALIGNED = 4,        /* a pointer is not 16-byte aligned */
+    NOBLE_ERR_WORKSPACE_TOO_SMALL = 5, /* scratch_bytes below the required size */
+    NOBLE_ERR_UNSUPPORTED_DEVICE = 6,  /* current device is not gfx950 */
+    NOBLE_ERR_HIP = 7                /* a HIP runtime call or launch failed */
+} noble_status;
+
+/* Problem description.  `dtype` holds a noble_dtype value. */
+typedef struct noble_linear_desc {
+    int64_t T;      /* tokens (rows of x, y, dy, dx) */
+    int64_t d_in;   /* input features */
+    int64_t d_out;  /* output features */
+    int64_t r;      /* bottleneck rank; 0 = plain linear */
+    int32_t dtype;  /* noble_dtype */
+    int32_t reserved; /* must be 0 */
+} noble_linear_desc;
+
+/* Sizes of the two caller-owned work buffers for `desc`.
+ *   reserve_bytes: written by noble_linear_fwd (H = x W_down, float32 [T, r])
+ *                  and read by the matching noble_linear_bwd; keep it intact
+ *                  in between.  4*T*r bytes.
+ *   scratch_bytes: temporary space used within one call (fwd or bwd) only.
+ * Either output pointer may be NULL.  Returns NOBLE_ERR_NULL_ARG (desc NULL),
+ * NOBLE_ERR_BAD_SHAPE or NOBLE_ERR_BAD_DTYPE; makes no HIP call. */
+noble_status noble_linear_workspace_size(const noble_linear_desc* desc,
+                                         size_t* reserve_bytes,
+                                         size_t* scratch_bytes);
+
+/* Forward, Eq. 1 with the CosNet of Eq. 2:
+ *   y = x W + b + cos(omega2 (.) (cos(omega1 (.) (x W_down) + phi1) M) + phi2) W_up
+ * Inputs : x [T, d_in], W [d_in, d_out], b [d_out] f32 (nullable = no bias),
+ *          W_down [d_in, r], omega1/phi1/omega2/phi2 [r] f32, M [r, r],
+ *          W_up [r, d_out].
+ * Outputs: y [T, d_out]; reserve (>= reserve_bytes) receives H for the
+ *          backward.  scratch must hold scratch_bytes. */
+noble_status noble_linear_fwd(const noble_linear_desc* desc,
+                              const void* x, const void* W, const float* b,
+                              const void* W_down,
+                              const float* omega1, const float* phi1,
+                              const void* M,
+                              const float* omega2, const float* phi2,
+                              const void* W_up,
+                              void* y, void* reserve,
+                              void* scratch, size_t scratch_bytes,
+                              void* stream);
+
+/* Backward of the forward above for upstream gradient dy [T, d_out], using
+ * the reserve written by the matching forward (same inputs, same desc).
+ * Every gradient buffer is overwritten (not accumulated):
+ *   dx [T, d_in] (storage dtype), dW [d_in, d_out], db [d_out] (nullable =
+ *   not computed), dW_down [d_in, r], dM [r, r], dW_up [r, d_out],
+ *   domega1, dphi1, domega2, dphi2 [r]  (all float32).
+ * With T = 0 the parameter gradients are set to zero.  Sums over tokens use
+ * float atomics, so results may differ in the last bits between runs. */
+noble_status noble_linear_bwd(const noble_linear_desc* desc,
+                              const void* dy, const void* x, const void* W,
+                              const void* W_down,
+                              const float* omega1, const float* phi1,
+                              const void* M,
+                              const float* omega2, const float* phi2,
+                              const void* W_up,
+                              const void* reserve,
+                              void* dx, float* dW, float* db,
+                              float* dW_down, float* dM, float* dW_up,
+                              float* domega1, float* dphi1,
+                              float* domega2, float* dphi2,
+                              void* scratch, size_t scratch_bytes,
+                              void* stream);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char* noble_status_string(int status);
+
+/* ABI version of this header (bumped on incompatible changes). */
+int noble_abi_version(void);
+
+#define NOBLE_ABI_VERSION 1
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NOBLE_H */

@@ -1,0 +1,412 @@
+// libnoble: C ABI of the NOBLE-CosNet linear layer (include/noble.h).
+//
+// Host side: argument validation (complete before any HIP call), workspace
+// layout, launch planning (tile choice, split-K) and kernel launches on the
+// caller's stream.  The library is stateless apart from a per-device cache of
+// the architecture check.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstring>
+
+#include "noble.h"
+#include "noble_kernels.hpp"
+
+using namespace noble;
+
+namespace {
+
+constexpr int64_t kMaxDim = int64_t(1) << 30;
+constexpr int64_t kMaxTokens = (int64_t(1) << 31) - 4096;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+noble_status check_desc(const noble_linear_desc* d) {
+    if (!d) return NOBLE_ERR_NULL_ARG;
+    if (d->dtype != NOBLE_BF16 && d->dtype != NOBLE_F32) return NOBLE_ERR_BAD_DTYPE;
+    if (d->T < 0 || d->T > kMaxTokens) return NOBLE_ERR_BAD_SHAPE;
+    if (d->d_in < 8 || d->d_in % 8 || d->d_in > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
+    if (d->d_out < 8 || d->d_out % 8 || d->d_out > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
+    if (d->r < 0 || (d->r > 0 && (d->r < 8 || d->r % 8 || d->r > 128))) return NOBLE_ERR_BAD_SHAPE;
+    return NOBLE_OK;
+}
+
+size_t elt_size(const noble_linear_desc* d) { return d->dtype == NOBLE_BF16 ? 2 : 4; }
+
+// Scratch layout: four [T, r] storage-type regions, each 256-byte aligned:
+// C1, C2, dH2, dH (the forward uses only C2).
+size_t scratch_region(const noble_linear_desc* d) { return align_up((size_t)d->T * d->r * elt_size(d)); }
+size_t scratch_need(const noble_linear_desc* d) { return d->r > 0 ? 4 * scratch_region(d) : 0; }
+size_t reserve_need(const noble_linear_desc* d) { return (size_t)d->T * d->r * 4; }
+
+// A required buffer: non-NULL and 16-byte aligned, unless it holds no bytes.
+noble_status need(const void* p, bool nonempty) {
+    if (!p) return nonempty ? NOBLE_ERR_NULL_ARG : NOBLE_OK;
+    return aligned16(p) ? NOBLE_OK : NOBLE_ERR_MISALIGNED;
+}
+noble_status optional(const void* p) { return (!p || aligned16(p)) ? NOBLE_OK : NOBLE_ERR_MISALIGNED; }
+
+#define NOBLE_TRY(expr)                              \
+    do {                                             \
+        noble_status s_ = (expr);                    \
+        if (s_ != NOBLE_OK) return s_;               \
+    } while (0)
+
+// gfx950 check, cached per device ordinal (0 unknown, 1 ok, 2 unsupported).
+std::atomic<int> g_arch_ok[256];
+
+noble_status check_device() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return NOBLE_ERR_HIP;
+    if (dev < 0 || dev >= 256) return NOBLE_ERR_UNSUPPORTED_DEVICE;
+    int s = g_arch_ok[dev].load(std::memory_order_relaxed);
+    if (s == 0) {
+        hipDeviceProp_t prop;
+        if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return NOBLE_ERR_HIP;
+        s = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+        g_arch_ok[dev].store(s, std::memory_order_relaxed);
+    }
+    return s == 1 ? NOBLE_OK : NOBLE_ERR_UNSUPPORTED_DEVICE;
+}
+
+noble_status last_launch() { return hipGetLastError() == hipSuccess ? NOBLE_OK : NOBLE_ERR_HIP; }
+
+int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+Seg seg(const void* p, int64_t ld, int64_t klen) {
+    Seg s;
+    s.ptr = static_cast<const char*>(p);
+    s.ld = ld;
+    s.klen = (int)klen;
+    s.pad_ = 0;
+    return s;
+}
+
+Operand operand1(Seg s0, int64_t rows) {
+    Operand o;
+    o.s[0] = s0;
+    o.s[1] = s0;
+    o.nk1 = 1 << 30;
+    o.rows = (int)rows;
+    return o;
+}
+
+// Two-segment operand: K chunks [0, nk1) from s0 (K extent K0, chunk BK), then s1.
+Operand operand2(Seg s0, Seg s1, int nk1, int64_t rows) {
+    Operand o;
+    o.s[0] = s0;
+    o.s[1] = s1;
+    o.nk1 = nk1;
+    o.rows = (int)rows;
+    return o;
+}
+
+// Main-product tile shape.
+constexpr int kBM = 128, kBN = 128, kWM = 2, kWN = 2;
+
+struct Batch {
+    GemmBatch b{};
+    int blocks = 0;
+    void add(const Operand& A, const Operand& B, int M, int N, int nk, void* C, int64_t ldc, bool out_f32,
+             const float* bias, float* bsum, int split) {
+        GemmProblem& p = b.p[b.count++];
+        p.A = A;
+        p.B = B;
+        p.C = C;
+        p.ldc = ldc;
+        p.bias = bias;
+        p.bsum = bsum;
+        p.M = M;
+        p.N = N;
+        p.nk = nk;
+        p.split = split;
+        p.tiles_n = cdiv(N, kBN);
+        p.tile_begin = blocks;
+        p.out_f32 = out_f32 ? 1 : 0;
+        p.atomic = split > 1 ? 1 : 0;
+        blocks += cdiv(M, kBM) * p.tiles_n * split;
+    }
+};
+
+// Split-K factor: enough blocks to cover the chip twice over, at least four
+// K chunks per piece.
+int choose_split(int tiles, int nk) {
+    int s = 1;
+    while (tiles * s < 512 && s * 2 * 4 <= nk) s *= 2;
+    return s;
+}
+
+template <typename E, bool AK, bool BKM>
+noble_status launch_gemm(const Batch& bt, hipStream_t st) {
+    if (bt.blocks == 0) return NOBLE_OK;
+    hipLaunchKernelGGL((gemm_kernel<E, kBM, kBN, kWM, kWN, AK, BKM>), dim3(bt.blocks), dim3(kThreads), 0, st,
+                       bt.b);
+    return last_launch();
+}
+
+template <typename E>
+noble_status launch_chain(bool fwd, int RP, const ChainArgs& a, int T, hipStream_t st) {
+    const dim3 grid(cdiv(T, kChainRows)), block(kThreads);
+#define NOBLE_CHAIN(RPV)                                                          \
+    if (RP == RPV) {                                                              \
+        if (fwd)                                                                  \
+            hipLaunchKernelGGL((fwd_chain_kernel<E, RPV>), grid, block, 0, st, a); \
+        else                                                                      \
+            hipLaunchKernelGGL((bwd_chain_kernel<E, RPV>), grid, block, 0, st, a); \
+        return last_launch();                                                     \
+    }
+    if constexpr (sizeof(E) == 4) {
+        NOBLE_CHAIN(32)
+        NOBLE_CHAIN(64)
+        NOBLE_CHAIN(128)
+    } else {
+        NOBLE_CHAIN(64)
+        NOBLE_CHAIN(128)
+    }
+#undef NOBLE_CHAIN
+    return NOBLE_ERR_BAD_SHAPE;
+}
+
+// Padded rank of the chain kernels: a multiple of the K chunk, instantiated
+// for 64 and 128 (bf16) and 32, 64 and 128 (f32).
+template <typename E>
+int chain_rp(int64_t r) {
+    if (sizeof(E) == 4 && r <= 32) return 32;
+    return r <= 64 ? 64 : 128;
+}
+
+template <typename E>
+noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, const float* b, const void* Wd,
+                      const float* w1, const float* p1, const void* M, const float* w2, const float* p2,
+                      const void* Wu, void* y, void* reserve, void* scratch, hipStream_t st) {
+    constexpr int BK = Elt<E>::BK;
+    const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
+    char* C2s = static_cast<char*>(scratch) + scratch_region(d);
+    if (r > 0) {
+        ChainArgs a{};
+        a.A = operand1(seg(x, din, din), T);
+        a.B = operand1(seg(Wd, r, din), r);
+        a.M = static_cast<const char*>(M);
+        a.w1 = w1;
+        a.p1 = p1;
+        a.w2 = w2;
+        a.p2 = p2;
+        a.H = static_cast<float*>(reserve);
+        a.C2s = C2s;
+        a.T = (int)T;
+        a.r = (int)r;
+        a.nk = cdiv(din, BK);
+        NOBLE_TRY(launch_chain<E>(true, chain_rp<E>(r), a, (int)T, st));
+    }
+    // y = [x | C2] [W ; W_up] + b
+    const int nk1 = cdiv(din, BK);
+    const int nk = nk1 + (r > 0 ? cdiv(r, BK) : 0);
+    Batch bt;
+    bt.add(operand2(seg(x, din, din), seg(C2s, r, r), nk1, T), operand2(seg(W, dout, din), seg(Wu, dout, r), nk1, dout),
+           (int)T, (int)dout, nk, y, dout, sizeof(E) == 4, b, nullptr, 1);
+    return launch_gemm<E, true, false>(bt, st);
+}
+
+template <typename E>
+noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x, const void* W, const void* Wd,
+                      const float* w1, const float* p1, const void* M, const float* w2, const float* p2,
+                      const void* Wu, const void* reserve, void* dx, float* dW, float* db, float* dWd, float* dM,
+                      float* dWu, float* dw1, float* dp1, float* dw2, float* dp2, void* scratch, hipStream_t st) {
+    constexpr int BK = Elt<E>::BK;
+    const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
+    const size_t reg = scratch_region(d);
+    char* base = static_cast<char*>(scratch);
+    char* C1s = base;
+    char* C2s = base + reg;
+    char* dH2s = base + 2 * reg;
+    char* dHs = base + 3 * reg;
+
+    // Plan the weight-gradient batch first: dW needs zeroing only if split.
+    const int nkT = cdiv(T, BK);
+    const int split_dW = T > 0 ? choose_split(cdiv(din, kBM) * cdiv(dout, kBN), nkT) : 1;
+
+    ZeroList z{};
+    auto zero = [&](float* p, int64_t n) {
+        if (p && n > 0) {
+            z.ptr[z.count] = p;
+            z.n[z.count] = n;
+            ++z.count;
+        }
+    };
+    if (T == 0 || split_dW > 1) zero(dW, din * dout);
+    zero(db, dout);
+    if (r > 0) {
+        zero(dWd, din * r);
+        zero(dM, r * r);
+        zero(dWu, r * dout);
+        zero(dw1, r);
+        zero(dp1, r);
+        zero(dw2, r);
+        zero(dp2, r);
+    }
+    if (z.count > 0) {
+        hipLaunchKernelGGL(zero_kernel, dim3(512), dim3(256), 0, st, z);
+        NOBLE_TRY(last_launch());
+    }
+    if (T == 0) return NOBLE_OK;
+
+    if (r > 0) {
+        ChainArgs a{};
+        a.A = operand1(seg(dy, dout, dout), T);
+        a.B = operand1(seg(Wu, dout, dout), r);   // B(k=j, n=q) = W_up[q][j]
+        a.M = static_cast<const char*>(M);
+        a.w1 = w1;
+        a.p1 = p1;
+        a.w2 = w2;
+        a.p2 = p2;
+        a.H = static_cast<float*>(const_cast<void*>(reserve));
+        a.C1s = C1s;
+        a.C2s = C2s;
+        a.dH2s = dH2s;
+        a.dHs = dHs;
+        a.dw1 = dw1;
+        a.dp1 = dp1;
+        a.dw2 = dw2;
+        a.dp2 = dp2;
+        a.T = (int)T;
+        a.r = (int)r;
+        a.nk = cdiv(dout, BK);
+        NOBLE_TRY(launch_chain<E>(false, chain_rp<E>(r), a, (int)T, st));
+    }
+
+    // dx = [dy | dH] [W^T ; W_down^T]   (B(k, n) stored [n][k]: K-major)
+    {
+        const int nk1 = cdiv(dout, BK);
+        const int nk = nk1 + (r > 0 ? cdiv(r, BK) : 0);
+        Batch bt;
+        bt.add(operand2(seg(dy, dout, dout), seg(dHs, r, r), nk1, T), operand2(seg(W, dout, dout), seg(Wd, r, r), nk1, din),
+               (int)T, (int)din, nk, dx, din, sizeof(E) == 4, nullptr, nullptr, 1);
+        NOBLE_TRY((launch_gemm<E, true, true>(bt, st)));
+    }
+
+    // Weight gradients, reduced over tokens (K = T), A and B both MN-major.
+    {
+        Batch bt;
+        const Operand xT = operand1(seg(x, din, T), din);
+        const Operand dyN = operand1(seg(dy, dout, T), dout);
+        bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, split_dW);
+        if (r > 0) {
+            const Operand dHN = operand1(seg(dHs, r, T), r);
+            const Operand C2T = operand1(seg(C2s, r, T), r);
+            const Operand C1T = operand1(seg(C1s, r, T), r);
+            const Operand dH2N = operand1(seg(dH2s, r, T), r);
+            bt.add(xT, dHN, (int)din, (int)r, nkT, dWd, r, true, nullptr, nullptr,
+                   choose_split(cdiv(din, kBM), nkT));
+            bt.add(C2T, dyN, (int)r, (int)dout, nkT, dWu, dout, true, nullptr, nullptr,
+                   choose_split(cdiv(dout, kBN), nkT));
+            bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM, r, true, nullptr, nullptr, choose_split(1, nkT));
+        }
+        NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
+    }
+    return NOBLE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int noble_abi_version(void) { return NOBLE_ABI_VERSION; }
+
+const char* noble_status_string(int status) {
+    switch (status) {
+        case NOBLE_OK: return "NOBLE_OK";
+        case NOBLE_ERR_NULL_ARG: return "NOBLE_ERR_NULL_ARG: a required pointer is NULL";
+        case NOBLE_ERR_BAD_SHAPE: return "NOBLE_ERR_BAD_SHAPE: dimension outside the supported ranges";
+        case NOBLE_ERR_BAD_DTYPE: return "NOBLE_ERR_BAD_DTYPE: dtype is not NOBLE_BF16 or NOBLE_F32";
+        case NOBLE_ERR_MISALIGNED: return "NOBLE_ERR_MISALIGNED: a pointer is not 16-byte aligned";
+        case NOBLE_ERR_WORKSPACE_TOO_SMALL: return "NOBLE_ERR_WORKSPACE_TOO_SMALL: scratch buffer too small";
+        case NOBLE_ERR_UNSUPPORTED_DEVICE: return "NOBLE_ERR_UNSUPPORTED_DEVICE: current device is not gfx950";
+        case NOBLE_ERR_HIP: return "NOBLE_ERR_HIP: a HIP runtime call or kernel launch failed";
+        default: return "NOBLE_ERR_UNKNOWN: not a noble_status value";
+    }
+}
+
+noble_status noble_linear_workspace_size(const noble_linear_desc* desc, size_t* reserve_bytes,
+                                         size_t* scratch_bytes) {
+    NOBLE_TRY(check_desc(desc));
+    if (reserve_bytes) *reserve_bytes = reserve_need(desc);
+    if (scratch_bytes) *scratch_bytes = scratch_need(desc);
+    return NOBLE_OK;
+}
+
+noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, const void* W, const float* b,
+                              const void* W_down, const float* omega1, const float* phi1, const void* M,
+                              const float* omega2, const float* phi2, const void* W_up, void* y, void* reserve,
+                              void* scratch, size_t scratch_bytes, void* stream) {
+    NOBLE_TRY(check_desc(desc));
+    const bool rows = desc->T > 0, br = desc->r > 0;
+    NOBLE_TRY(need(x, rows));
+    NOBLE_TRY(need(W, true));
+    NOBLE_TRY(optional(b));
+    NOBLE_TRY(need(y, rows));
+    if (br) {
+        NOBLE_TRY(need(W_down, true));
+        NOBLE_TRY(need(omega1, true));
+        NOBLE_TRY(need(phi1, true));
+        NOBLE_TRY(need(M, true));
+        NOBLE_TRY(need(omega2, true));
+        NOBLE_TRY(need(phi2, true));
+        NOBLE_TRY(need(W_up, true));
+        NOBLE_TRY(need(reserve, rows));
+        NOBLE_TRY(need(scratch, rows));
+        if (scratch_bytes < scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
+    }
+    if (!rows) return NOBLE_OK;
+    NOBLE_TRY(check_device());
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (desc->dtype == NOBLE_BF16)
+        return fwd_impl<uint16_t>(desc, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch, st);
+    return fwd_impl<float>(desc, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch, st);
+}
+
+noble_status noble_linear_bwd(const noble_linear_desc* desc, const void* dy, const void* x, const void* W,
+                              const void* W_down, const float* omega1, const float* phi1, const void* M,
+                              const float* omega2, const float* phi2, const void* W_up, const void* reserve, void* dx,
+                              float* dW, float* db, float* dW_down, float* dM, float* dW_up, float* domega1,
+                              float* dphi1, float* domega2, float* dphi2, void* scratch, size_t scratch_bytes,
+                              void* stream) {
+    NOBLE_TRY(check_desc(desc));
+    const bool rows = desc->T > 0, br = desc->r > 0;
+    NOBLE_TRY(need(dy, rows));
+    NOBLE_TRY(need(x, rows));
+    NOBLE_TRY(need(W, true));
+    NOBLE_TRY(need(dx, rows));
+    NOBLE_TRY(need(dW, true));
+    NOBLE_TRY(optional(db));
+    if (br) {
+        NOBLE_TRY(need(W_down, true));
+        NOBLE_TRY(need(omega1, true));
+        NOBLE_TRY(need(phi1, true));
+        NOBLE_TRY(need(M, true));
+        NOBLE_TRY(need(omega2, true));
+        NOBLE_TRY(need(phi2, true));
+        NOBLE_TRY(need(W_up, true));
+        NOBLE_TRY(need(reserve, rows));
+        NOBLE_TRY(need(dW_down, true));
+        NOBLE_TRY(need(dM, true));
+        NOBLE_TRY(need(dW_up, true));
+        NOBLE_TRY(need(domega1, true));
+        NOBLE_TRY(need(dphi1, true));
+        NOBLE_TRY(need(domega2, true));
+        NOBLE_TRY(need(dphi2, true));
+        NOBLE_TRY(need(scratch, rows));
+        if (scratch_bytes < scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
+    }
+    NOBLE_TRY(check_device());
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (desc->dtype == NOBLE_BF16)
+        return bwd_impl<uint16_t>(desc, dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve, dx, dW, db,
+                                  dW_down, dM, dW_up, domega1, dphi1, domega2, dphi2, scratch, st);
+    return bwd_impl<float>(desc, dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve, dx, dW, db, dW_down,
+                           dM, dW_up, domega1, dphi1, domega2, dphi2, scratch, st);
+}
+
+}  // extern "C"

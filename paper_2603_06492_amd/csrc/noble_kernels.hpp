@@ -1,0 +1,434 @@
+// NOBLE-CosNet linear layer kernels for gfx950.
+//
+// Forward (Eq. 1 with the CosNet of Eq. 2):
+//   fwd_chain_kernel : H = x W_down (MFMA), C1 = cos(H w1 + p1), H2 = C1 M
+//                      (MFMA from LDS), C2 = cos(H2 w2 + p2).  Writes H (f32,
+//                      the reserve) and C2 (storage type, scratch).
+//   gemm_kernel      : y = [x | C2] [W ; W_up] + b  (the rank-r up-projection
+//                      is a K-extension of the main product).
+// Backward (chain rule, cosines recomputed from H):
+//   bwd_chain_kernel : dC2 = dy W_up^T (MFMA), then the chain backwards with
+//                      both r x r mixings on MFMA; writes C1, C2, dH2, dH
+//                      (scratch) and reduces dw/dp with wave shuffles and one
+//                      atomic per column per wave.
+//   gemm_kernel      : dx = [dy | dH] [W^T ; W_down^T]      (K-extension)
+//   gemm_kernel      : dW = x^T dy, dW_down = x^T dH, dW_up = C2^T dy,
+//                      dM = C1^T dH2 as one grouped launch with split-K over
+//                      tokens; db = column sums of dy, taken from the dy tiles
+//                      the dW problem already stages.
+#pragma once
+
+#include "noble_tiles.hpp"
+
+namespace noble {
+
+// ---------------------------------------------------------------- zero fill --
+
+constexpr int kMaxZero = 10;
+struct ZeroList {
+    float* ptr[kMaxZero];
+    int64_t n[kMaxZero];
+    int count;
+};
+
+__global__ __launch_bounds__(256) void zero_kernel(ZeroList z) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int s = 0; s < z.count; ++s) {
+        float* p = z.ptr[s];
+        const int64_t n = z.n[s];
+        const int64_t n4 = n >> 2;
+        for (int64_t i = gid; i < n4; i += stride)
+            reinterpret_cast<f32x4*>(p)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int64_t i = (n4 << 2) + gid; i < n; i += stride) p[i] = 0.f;
+    }
+}
+
+// ------------------------------------------------------------ grouped GEMM --
+
+struct GemmProblem {
+    Operand A, B;
+    void* C;
+    int64_t ldc;
+    const float* bias;  // per output column, added by K piece 0 (nullable)
+    float* bsum;        // column sums of B over K, atomically added (nullable)
+    int M, N;
+    int nk;             // K chunks (both segments)
+    int split;          // K pieces; each piece accumulates atomically if > 1
+    int tiles_n;
+    int tile_begin;     // first block index of this problem
+    int out_f32;        // C holds float (1) or the storage type (0)
+    int atomic;         // atomicAdd into a zeroed float C
+};
+
+constexpr int kMaxProblems = 4;
+struct GemmBatch {
+    GemmProblem p[kMaxProblems];
+    int count;
+    int pad_;
+};
+
+template <typename E, int BM, int BN, int WM, int WN, bool AK, bool BKM>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmBatch batch) {
+    constexpr int TM = BM / WM / 16, TN = BN / WN / 16;
+    __shared__ __attribute__((aligned(16))) char lds[2 * (BM + BN) * kRowBytes];
+    const int bid = blockIdx.x;
+    int q = 0;
+#pragma unroll
+    for (int t = 1; t < kMaxProblems; ++t)
+        if (t < batch.count && bid >= batch.p[t].tile_begin) q = t;
+    const GemmProblem& P = batch.p[q];
+    const int local = bid - P.tile_begin;
+    const int piece = local % P.split, tile = local / P.split;
+    const int tm = tile / P.tiles_n, tn = tile % P.tiles_n;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kc0 = (int)((int64_t)P.nk * piece / P.split);
+    const int kc1 = (int)((int64_t)P.nk * (piece + 1) / P.split);
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm0 = (wave / WN) * (BM / WM), wn0 = (wave % WN) * (BN / WN);
+    const int r16 = lane & 15, g = lane >> 4;
+
+    // Column sums of B (db = sum over tokens of dy) come from the B tiles this
+    // block stages anyway: one tile row of blocks, one wave row within it.
+    const bool do_bsum = (P.bsum != nullptr) && tm == 0 && (wave / WN) == 0;
+    float bs[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bs[j] = 0.f;
+
+    {
+        constexpr int STAGE = (BM + BN) * kRowBytes;
+        if (kc0 < kc1) {
+            Stage<E, BM, AK> sa;
+            Stage<E, BN, BKM> sb;
+            sa.load(P.A, m0, kc0, tid);
+            sb.load(P.B, n0, kc0, tid);
+            sa.store(lds, tid);
+            sb.store(lds + BM * kRowBytes, tid);
+            __syncthreads();
+            for (int kc = kc0; kc < kc1; ++kc) {
+                char* cur = lds + ((kc - kc0) & 1) * STAGE;
+                char* nxt = lds + (((kc - kc0) & 1) ^ 1) * STAGE;
+                const bool more = kc + 1 < kc1;
+                if (more) {
+                    sa.load(P.A, m0, kc + 1, tid);
+                    sb.load(P.B, n0, kc + 1, tid);
+                }
+                mma_chunk<E, TM, TN>(cur, cur + BM * kRowBytes, wm0, wn0, lane, acc);
+                if (do_bsum) {
+                    const char* ldsB = cur + BM * kRowBytes;
+#pragma unroll
+                    for (int s = 0; s < 2; ++s)
+#pragma unroll
+                        for (int j = 0; j < TN; ++j) {
+                            const u32x4 b = *reinterpret_cast<const u32x4*>(
+                                ldsB + lds_off(wn0 + 16 * j + r16, 4 * s + g));
+#pragma unroll
+                            for (int w = 0; w < 4; ++w) {
+                                if constexpr (sizeof(E) == 2)
+                                    bs[j] += bf2f(b[w] & 0xffffu) + bf2f(b[w] >> 16);
+                                else
+                                    bs[j] += __uint_as_float(b[w]);
+                            }
+                        }
+                }
+                if (more) {
+                    sa.store(nxt, tid);
+                    sb.store(nxt + BM * kRowBytes, tid);
+                }
+                __syncthreads();
+            }
+        }
+    }
+
+    if (do_bsum) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            float s = bs[j];
+            s += __shfl_xor(s, 16);
+            s += __shfl_xor(s, 32);
+            const int col = n0 + wn0 + 16 * j + r16;
+            if (g == 0 && col < P.N) unsafeAtomicAdd(P.bsum + col, s);
+        }
+    }
+
+    const bool add_bias = (P.bias != nullptr) && piece == 0;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = n0 + wn0 + 16 * j + r16;
+        if (col >= P.N) continue;
+        const float bcol = add_bias ? P.bias[col] : 0.f;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = m0 + wm0 + 16 * i + 4 * g + v;
+                if (row >= P.M) continue;
+                const float val = acc[i][j][v] + bcol;
+                const int64_t off = (int64_t)row * P.ldc + col;
+                if (P.atomic)
+                    unsafeAtomicAdd(reinterpret_cast<float*>(P.C) + off, val);
+                else if (P.out_f32)
+                    reinterpret_cast<float*>(P.C)[off] = val;
+                else
+                    reinterpret_cast<E*>(P.C)[off] = to_elt<E>(val);
+            }
+    }
+}
+
+// ------------------------------------------------------------- chain kernels --
+
+struct ChainArgs {
+    Operand A;          // fwd: x [T, d_in];  bwd: dy [T, d_out]   (K-major)
+    Operand B;          // fwd: W_down [d_in, r] (MN-major);  bwd: W_up as W_up^T (K-major)
+    const char* M;      // [r, r] storage type
+    const float* w1;
+    const float* p1;
+    const float* w2;
+    const float* p2;
+    float* H;           // reserve [T, r]: written by fwd, read by bwd
+    char* C1s;          // scratch [T, r] storage type (bwd)
+    char* C2s;          // scratch [T, r] storage type
+    char* dH2s;         // scratch [T, r] storage type (bwd)
+    char* dHs;          // scratch [T, r] storage type (bwd)
+    float* dw1;
+    float* dp1;
+    float* dw2;
+    float* dp2;
+    int T, r, nk, pad_;
+};
+
+constexpr int kChainRows = 32;  // tokens per workgroup in the chain kernels
+
+template <typename E, int RP>
+struct ChainShape {
+    static constexpr int BK = Elt<E>::BK;
+    static constexpr int NKB = RP / BK;     // K chunks of the r x r mixing
+    static constexpr int TN = RP / 32;      // 16-wide tiles per wave (waves 2 x 2)
+    static constexpr int MAIN = 2 * (kChainRows + RP) * kRowBytes;
+    static constexpr int MIX = NKB * (kChainRows + RP) * kRowBytes;
+    static constexpr int LDS = MAIN > MIX ? MAIN : MIX;
+    static_assert(RP % BK == 0, "RP must be a multiple of the K chunk");
+};
+
+// Element (row, col) of a kChainRows x RP operand tile laid out as NKB K chunks.
+template <typename E>
+__device__ __forceinline__ int tile_elem_off(int row, int col, int rows) {
+    constexpr int BK = Elt<E>::BK, VEC = Elt<E>::VEC;
+    return (col / BK) * rows * kRowBytes + lds_off(row, (col % BK) / VEC) + (col % VEC) * (int)sizeof(E);
+}
+
+// Stage the r x r matrix M as the B operand of a mixing product, all K chunks.
+// KMAJ = false: B(k, n) = M[k][n] (for C1 M).  KMAJ = true: B(k, n) = M[n][k]
+// (for dH2 M^T).
+template <typename E, int RP, bool KMAJ>
+__device__ __forceinline__ void stage_mix_matrix(const char* M, int r, char* dst, int tid) {
+    Operand om;
+    om.s[0].ptr = M;
+    om.s[0].ld = r;
+    om.s[0].klen = r;
+    om.s[1] = om.s[0];
+    om.nk1 = 1 << 30;
+    om.rows = r;
+#pragma unroll
+    for (int kb = 0; kb < ChainShape<E, RP>::NKB; ++kb) {
+        Stage<E, RP, KMAJ> st;
+        st.load(om, 0, kb, tid);
+        st.store(dst + kb * RP * kRowBytes, tid);
+    }
+}
+
+// Sum over the 16-row slab of a wave, per column; lanes 0..15 return the total.
+__device__ __forceinline__ float wave_colsum(float x) {
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 32);
+    return x;
+}
+
+template <typename E, int RP>
+__global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
+    using S = ChainShape<E, RP>;
+    constexpr int TN = S::TN;
+    __shared__ __attribute__((aligned(16))) char lds[S::LDS];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r16 = lane & 15, g = lane >> 4;
+    const int wm0 = (wave >> 1) * 16, wn0 = (wave & 1) * (RP / 2);
+    const int m0 = blockIdx.x * kChainRows;
+    const int r = a.r;
+
+    f32x4 acc[1][TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    mainloop<E, kChainRows, RP, 2, 2, true, false>(a.A, a.B, m0, 0, 0, a.nk, lds, acc);
+
+    char* Cb = lds;
+    char* Mb = lds + S::NKB * kChainRows * kRowBytes;
+    stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
+
+    // H -> reserve; C1 = cos(H w1 + p1) -> LDS (A operand of the mixing)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = wn0 + 16 * j + r16;
+        const bool cv = col < r;
+        const float w = cv ? a.w1[col] : 0.f, p = cv ? a.p1[col] : 0.f;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = wm0 + 4 * g + v, grow = m0 + row;
+            const float h = acc[0][j][v];
+            if (cv && grow < a.T) a.H[(int64_t)grow * r + col] = h;
+            const float c1 = cv ? cosf(h * w + p) : 0.f;
+            *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = to_elt<E>(c1);
+        }
+    }
+    __syncthreads();
+
+    f32x4 mix[1][TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) mix[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < S::NKB; ++kb)
+        mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, mix);
+
+    // C2 = cos(H2 w2 + p2) -> scratch
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = wn0 + 16 * j + r16;
+        if (col >= r) continue;
+        const float w = a.w2[col], p = a.p2[col];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int grow = m0 + wm0 + 4 * g + v;
+            if (grow < a.T)
+                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = to_elt<E>(cosf(mix[0][j][v] * w + p));
+        }
+    }
+}
+
+template <typename E, int RP>
+__global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
+    using S = ChainShape<E, RP>;
+    constexpr int TN = S::TN;
+    __shared__ __attribute__((aligned(16))) char lds[S::LDS];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r16 = lane & 15, g = lane >> 4;
+    const int wm0 = (wave >> 1) * 16, wn0 = (wave & 1) * (RP / 2);
+    const int m0 = blockIdx.x * kChainRows;
+    const int r = a.r;
+
+    // dC2 = dy W_up^T
+    f32x4 dc2[1][TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) dc2[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    mainloop<E, kChainRows, RP, 2, 2, true, true>(a.A, a.B, m0, 0, 0, a.nk, lds, dc2);
+
+    char* Cb = lds;
+    char* Mb = lds + S::NKB * kChainRows * kRowBytes;
+    stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
+
+    // Recompute A1 = H w1 + p1, C1 = cos A1 (-> LDS and scratch), keep H, sin A1.
+    float hr[TN][4], s1[TN][4];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = wn0 + 16 * j + r16;
+        const bool cv = col < r;
+        const float w = cv ? a.w1[col] : 0.f, p = cv ? a.p1[col] : 0.f;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = wm0 + 4 * g + v, grow = m0 + row;
+            const bool ok = cv && grow < a.T;
+            const float h = ok ? a.H[(int64_t)grow * r + col] : 0.f;
+            float sn = 0.f, cs = 0.f;
+            if (cv) sincosf(h * w + p, &sn, &cs);
+            hr[j][v] = h;
+            s1[j][v] = sn;
+            const E c1 = to_elt<E>(cs);
+            *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = c1;
+            if (ok) reinterpret_cast<E*>(a.C1s)[(int64_t)grow * r + col] = c1;
+        }
+    }
+    __syncthreads();
+
+    // H2 = C1 M
+    f32x4 h2[1][TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) h2[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < S::NKB; ++kb)
+        mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, h2);
+    __syncthreads();  // every wave is done with C1 and M in LDS
+
+    stage_mix_matrix<E, RP, true>(a.M, r, Mb, tid);
+
+    // A2 = H2 w2 + p2; C2 = cos A2 -> scratch; dA2 = -sin(A2) dC2;
+    // dw2 += dA2 H2, dp2 += dA2; dH2 = dA2 w2 -> LDS and scratch.
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = wn0 + 16 * j + r16;
+        const bool cv = col < r;
+        const float w = cv ? a.w2[col] : 0.f, p = cv ? a.p2[col] : 0.f;
+        float sw = 0.f, sp = 0.f;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = wm0 + 4 * g + v, grow = m0 + row;
+            const bool ok = cv && grow < a.T;
+            float sn = 0.f, cs = 0.f;
+            if (cv) sincosf(h2[0][j][v] * w + p, &sn, &cs);
+            const float da2 = ok ? -sn * dc2[0][j][v] : 0.f;
+            sw += da2 * h2[0][j][v];
+            sp += da2;
+            const E dh2 = to_elt<E>(da2 * w);
+            *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = dh2;
+            if (ok) {
+                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = to_elt<E>(cs);
+                reinterpret_cast<E*>(a.dH2s)[(int64_t)grow * r + col] = dh2;
+            }
+        }
+        sw = wave_colsum(sw);
+        sp = wave_colsum(sp);
+        if (g == 0 && cv) {
+            unsafeAtomicAdd(a.dw2 + col, sw);
+            unsafeAtomicAdd(a.dp2 + col, sp);
+        }
+    }
+    __syncthreads();
+
+    // dC1 = dH2 M^T
+    f32x4 dc1[1][TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) dc1[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < S::NKB; ++kb)
+        mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, dc1);
+
+    // dA1 = -sin(A1) dC1; dw1 += dA1 H, dp1 += dA1; dH = dA1 w1 -> scratch
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = wn0 + 16 * j + r16;
+        const bool cv = col < r;
+        const float w = cv ? a.w1[col] : 0.f;
+        float sw = 0.f, sp = 0.f;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int grow = m0 + wm0 + 4 * g + v;
+            const bool ok = cv && grow < a.T;
+            const float da1 = ok ? -s1[j][v] * dc1[0][j][v] : 0.f;
+            sw += da1 * hr[j][v];
+            sp += da1;
+            if (ok) reinterpret_cast<E*>(a.dHs)[(int64_t)grow * r + col] = to_elt<E>(da1 * w);
+        }
+        sw = wave_colsum(sw);
+        sp = wave_colsum(sp);
+        if (g == 0 && cv) {
+            unsafeAtomicAdd(a.dw1 + col, sw);
+            unsafeAtomicAdd(a.dp1 + col, sp);
+        }
+    }
+}
+
+}  // namespace noble

@@ -1,0 +1,260 @@
+"""Python binding of libnoble (include/noble.h): argument marshalling only.
+
+Every step of the layer runs in the HIP kernels of ``libnoble.so``; this module
+only checks tensors, passes their device pointers and the current HIP stream,
+and turns status codes into exceptions.  There is no fallback: if the library
+is not built, or the device is not gfx950, calls raise.
+
+Functions keep the C names: ``noble_linear_workspace_size``,
+``noble_linear_fwd``, ``noble_linear_bwd``, ``noble_status_string``.
+``NobleLinearFunction`` wraps the pair as a ``torch.autograd.Function``.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libnoble.so")
+
+NOBLE_BF16 = 0
+NOBLE_F32 = 1
+
+STATUS = {
+    0: "NOBLE_OK",
+    1: "NOBLE_ERR_NULL_ARG",
+    2: "NOBLE_ERR_BAD_SHAPE",
+    3: "NOBLE_ERR_BAD_DTYPE",
+    4: "NOBLE_ERR_MISALIGNED",
+    5: "NOBLE_ERR_WORKSPACE_TOO_SMALL",
+    6: "NOBLE_ERR_UNSUPPORTED_DEVICE",
+    7: "NOBLE_ERR_HIP",
+}
+
+
+class NobleError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {noble_status_string(status)}")
+
+
+class noble_linear_desc(ctypes.Structure):
+    _fields_ = [
+        ("T", ctypes.c_int64),
+        ("d_in", ctypes.c_int64),
+        ("d_out", ctypes.c_int64),
+        ("r", ctypes.c_int64),
+        ("dtype", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
+_lib = None
+_vp = ctypes.c_void_p
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libnoble.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(or python -m paper_2603_06492_amd._build)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.noble_status_string.restype = ctypes.c_char_p
+        L.noble_status_string.argtypes = [ctypes.c_int]
+        L.noble_abi_version.restype = ctypes.c_int
+        L.noble_abi_version.argtypes = []
+        L.noble_linear_workspace_size.restype = ctypes.c_int
+        L.noble_linear_workspace_size.argtypes = [ctypes.POINTER(noble_linear_desc),
+                                                  ctypes.POINTER(ctypes.c_size_t),
+                                                  ctypes.POINTER(ctypes.c_size_t)]
+        L.noble_linear_fwd.restype = ctypes.c_int
+        L.noble_linear_fwd.argtypes = [ctypes.POINTER(noble_linear_desc)] + [_vp] * 13 + [ctypes.c_size_t, _vp]
+        L.noble_linear_bwd.restype = ctypes.c_int
+        L.noble_linear_bwd.argtypes = [ctypes.POINTER(noble_linear_desc)] + [_vp] * 22 + [ctypes.c_size_t, _vp]
+        _lib = L
+    return _lib
+
+
+def noble_status_string(status: int) -> str:
+    return lib().noble_status_string(int(status)).decode()
+
+
+def make_desc(T: int, d_in: int, d_out: int, r: int, dtype: int) -> noble_linear_desc:
+    return noble_linear_desc(int(T), int(d_in), int(d_out), int(r), int(dtype), 0)
+
+
+def noble_linear_workspace_size(T: int, d_in: int, d_out: int, r: int, dtype: int) -> Tuple[int, int]:
+    """(reserve_bytes, scratch_bytes) for the problem."""
+    d = make_desc(T, d_in, d_out, r, dtype)
+    res, scr = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    st = lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(res), ctypes.byref(scr))
+    if st != 0:
+        raise NobleError(st, "noble_linear_workspace_size")
+    return res.value, scr.value
+
+
+# ----------------------------------------------------------------- tensors --
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return NOBLE_BF16
+    if t.dtype == torch.float32:
+        return NOBLE_F32
+    raise TypeError(f"storage tensors must be bfloat16 or float32, got {t.dtype}")
+
+
+def _ptr(t, name: str, dtype=None, shape=None) -> Optional[int]:
+    if t is None:
+        return None
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t.data_ptr() or None
+
+
+def _stream(stream) -> Optional[int]:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream or None
+
+
+def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
+                     stream=None) -> None:
+    """Enqueue the forward on ``stream`` (default: torch's current stream).
+
+    Storage tensors (x, W, W_down, M, W_up, y) share one dtype (bf16 or f32);
+    b, omega*, phi* are float32.  reserve/scratch are byte (uint8) tensors of
+    at least the sizes from noble_linear_workspace_size.  With r = 0 pass None
+    for the branch tensors.
+    """
+    torch = _torch()
+    T, d_in = x.shape
+    d_out = W.shape[1]
+    r = 0 if W_down is None else W_down.shape[1]
+    dt = _dtype_code(x)
+    sd = x.dtype
+    f32 = torch.float32
+    d = make_desc(T, d_in, d_out, r, dt)
+    args = [
+        _ptr(x, "x", sd, (T, d_in)), _ptr(W, "W", sd, (d_in, d_out)), _ptr(b, "b", f32, (d_out,)),
+        _ptr(W_down, "W_down", sd, (d_in, r)), _ptr(omega1, "omega1", f32, (r,)), _ptr(phi1, "phi1", f32, (r,)),
+        _ptr(M, "M", sd, (r, r)), _ptr(omega2, "omega2", f32, (r,)), _ptr(phi2, "phi2", f32, (r,)),
+        _ptr(W_up, "W_up", sd, (r, d_out)), _ptr(y, "y", sd, (T, d_out)),
+        _ptr(reserve, "reserve"), _ptr(scratch, "scratch"),
+    ]
+    nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
+    st = lib().noble_linear_fwd(ctypes.byref(d), *args, nbytes, _stream(stream))
+    if st != 0:
+        raise NobleError(st, "noble_linear_fwd")
+
+
+def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve,
+                     dx, dW, db, dW_down, dM, dW_up, domega1, dphi1, domega2, dphi2, scratch,
+                     stream=None) -> None:
+    """Enqueue the backward on ``stream``; overwrites every gradient tensor.
+
+    dx has the storage dtype; dW, db (optional), dW_down, dM, dW_up and the
+    four frequency/phase gradients are float32.
+    """
+    torch = _torch()
+    T, d_in = x.shape
+    d_out = W.shape[1]
+    r = 0 if W_down is None else W_down.shape[1]
+    dt = _dtype_code(x)
+    sd = x.dtype
+    f32 = torch.float32
+    d = make_desc(T, d_in, d_out, r, dt)
+    args = [
+        _ptr(dy, "dy", sd, (T, d_out)), _ptr(x, "x", sd, (T, d_in)), _ptr(W, "W", sd, (d_in, d_out)),
+        _ptr(W_down, "W_down", sd, (d_in, r)), _ptr(omega1, "omega1", f32, (r,)), _ptr(phi1, "phi1", f32, (r,)),
+        _ptr(M, "M", sd, (r, r)), _ptr(omega2, "omega2", f32, (r,)), _ptr(phi2, "phi2", f32, (r,)),
+        _ptr(W_up, "W_up", sd, (r, d_out)), _ptr(reserve, "reserve"),
+        _ptr(dx, "dx", sd, (T, d_in)), _ptr(dW, "dW", f32, (d_in, d_out)), _ptr(db, "db", f32, (d_out,)),
+        _ptr(dW_down, "dW_down", f32, (d_in, r)), _ptr(dM, "dM", f32, (r, r)),
+        _ptr(dW_up, "dW_up", f32, (r, d_out)),
+        _ptr(domega1, "domega1", f32, (r,)), _ptr(dphi1, "dphi1", f32, (r,)),
+        _ptr(domega2, "domega2", f32, (r,)), _ptr(dphi2, "dphi2", f32, (r,)),
+        _ptr(scratch, "scratch"),
+    ]
+    nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
+    st = lib().noble_linear_bwd(ctypes.byref(d), *args, nbytes, _stream(stream))
+    if st != 0:
+        raise NobleError(st, "noble_linear_bwd")
+
+
+# ------------------------------------------------------------ conveniences --
+
+def alloc_workspace(T, d_in, d_out, r, dtype_code, device="cuda"):
+    """(reserve, scratch) uint8 tensors of the required sizes."""
+    torch = _torch()
+    res, scr = noble_linear_workspace_size(T, d_in, d_out, r, dtype_code)
+    return (torch.empty(max(res, 16), dtype=torch.uint8, device=device),
+            torch.empty(max(scr, 16), dtype=torch.uint8, device=device))
+
+
+def _make_function():
+    torch = _torch()
+
+    class NobleLinearFunction(torch.autograd.Function):
+        """y = x W + b + CosNet(x W_down) W_up with the libnoble kernels.
+
+        Parameter gradients are float32 (master-weight convention)."""
+
+        @staticmethod
+        def forward(ctx, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up):
+            T, d_in = x.shape
+            d_out, r = W.shape[1], W_down.shape[1]
+            dt = _dtype_code(x)
+            reserve, scratch = alloc_workspace(T, d_in, d_out, r, dt, x.device)
+            y = torch.empty((T, d_out), dtype=x.dtype, device=x.device)
+            noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch)
+            ctx.save_for_backward(x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve)
+            ctx.has_bias = b is not None
+            return y
+
+        @staticmethod
+        def backward(ctx, dy):
+            x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve = ctx.saved_tensors
+            T, d_in = x.shape
+            d_out, r = W.shape[1], W_down.shape[1]
+            dev, f32 = x.device, torch.float32
+            dy = dy.contiguous().to(x.dtype)
+            _, scratch = alloc_workspace(T, d_in, d_out, r, _dtype_code(x), dev)
+            dx = torch.empty_like(x)
+            g = {n: torch.empty(s, dtype=f32, device=dev) for n, s in (
+                ("dW", (d_in, d_out)), ("db", (d_out,)), ("dW_down", (d_in, r)), ("dM", (r, r)),
+                ("dW_up", (r, d_out)), ("domega1", (r,)), ("dphi1", (r,)), ("domega2", (r,)), ("dphi2", (r,)))}
+            noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve,
+                             dx, g["dW"], g["db"], g["dW_down"], g["dM"], g["dW_up"],
+                             g["domega1"], g["dphi1"], g["domega2"], g["dphi2"], scratch)
+            return (dx, g["dW"].to(W.dtype), g["db"] if ctx.has_bias else None, g["dW_down"].to(W_down.dtype),
+                    g["domega1"], g["dphi1"], g["dM"].to(M.dtype), g["domega2"], g["dphi2"],
+                    g["dW_up"].to(W_up.dtype))
+
+    return NobleLinearFunction
+
+
+def __getattr__(name):
+    if name == "NobleLinearFunction":
+        fn = _make_function()
+        globals()[name] = fn
+        return fn
+    raise AttributeError(name)

@@ -1,0 +1,45 @@
+"""Parity metric and oracle references for the GPU tests (test helpers only)."""
+
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+
+# max over rows of max_j |gpu - ref| / (max_j |ref| + 1e-6): bf16 operands with
+# float32 accumulation, and the float32 path
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+OUTPUTS = ("y", "dx", "dW", "db", "dW_down", "dM", "dW_up", "domega1", "dphi1", "domega2", "dphi2")
+
+
+def row_err(gpu: np.ndarray, ref: np.ndarray) -> float:
+    gpu = np.atleast_2d(np.asarray(gpu, dtype=np.float64))
+    ref = np.atleast_2d(np.asarray(ref, dtype=np.float64))
+    assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
+    if ref.size == 0:
+        return 0.0
+    denom = np.max(np.abs(ref), axis=1) + 1e-6
+    return float(np.max(np.max(np.abs(gpu - ref), axis=1) / denom))
+
+
+def oracle_outputs(p, *, with_bias=True, branch=True, rows=None, dw_rows=None):
+    """fp64 oracle y and gradients for projection ``p`` (optionally row-sampled)."""
+    a = p.arrays
+    if branch:
+        br = {k: a[k] for k in ("W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up")}
+    else:
+        z = np.zeros
+        br = {"W_down": z((p.d_in, 0)), "omega1": z(0), "phi1": z(0), "M": z((0, 0)),
+              "omega2": z(0), "phi2": z(0), "W_up": z((0, p.d_out))}
+    b = a["b"] if with_bias else None
+    x = a["x"] if rows is None else a["x"][rows]
+    Y, _ = oracle.forward(x, a["W"], b, br["W_down"], br["omega1"], br["phi1"], br["M"],
+                          br["omega2"], br["phi2"], br["W_up"])
+    g = oracle.backward(a["dy"], a["x"], a["W"], br["W_down"], br["omega1"], br["phi1"], br["M"],
+                        br["omega2"], br["phi2"], br["W_up"], dx_rows=rows, dW_rows=dw_rows)
+    g["y"] = Y
+    return g
+
+
+def parity_report(gpu: dict, ref: dict, names=OUTPUTS) -> dict:
+    return {n: row_err(gpu[n], ref[n]) for n in names if gpu.get(n) is not None and ref.get(n) is not None}

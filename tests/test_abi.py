@@ -1,0 +1,145 @@
+"""C ABI of libnoble on the CPU: the library loads, exports every function
+include/noble.h declares, sizes workspaces, and rejects bad arguments before
+any HIP call.  Every fwd/bwd call here carries exactly one defect that the
+validation catches, so nothing can reach a device."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2603_06492_amd import noble
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "noble.h")
+
+OK, NULL, SHAPE, DTYPE, MISAL, WS = 0, 1, 2, 3, 4, 5
+
+# fake, 16-byte aligned addresses: never dereferenced because every call below
+# fails validation first
+FAKE = [0x100000 + 0x1000 * i for i in range(32)]
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(noble_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    names = _declared_functions()
+    assert set(names) == {"noble_linear_workspace_size", "noble_linear_fwd", "noble_linear_bwd",
+                          "noble_status_string", "noble_abi_version"}
+    L = noble.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.noble_abi_version() == 1
+
+
+def test_status_strings():
+    for code, name in noble.STATUS.items():
+        assert noble.noble_status_string(code).startswith(name)
+    assert "UNKNOWN" in noble.noble_status_string(99)
+
+
+def _ws(T, di, do, r, dt):
+    d = noble.make_desc(T, di, do, r, dt)
+    a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    st = noble.lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(a), ctypes.byref(b))
+    return st, a.value, b.value
+
+
+def test_workspace_sizes():
+    st, res, scr = _ws(8192, 2048, 2048, 128, noble.NOBLE_BF16)
+    assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2
+    st, res, scr = _ws(256, 64, 64, 8, noble.NOBLE_F32)
+    assert st == OK and res == 4 * 256 * 8 and scr == 4 * 256 * 8 * 4
+    st, res, scr = _ws(1000, 64, 64, 0, noble.NOBLE_BF16)
+    assert st == OK and res == 0 and scr == 0
+    st, res, scr = _ws(0, 64, 64, 32, noble.NOBLE_BF16)
+    assert st == OK and res == 0
+    # each region of the scratch is 256-byte aligned
+    st, res, scr = _ws(3, 64, 64, 8, noble.NOBLE_BF16)
+    assert st == OK and scr == 4 * 256
+    assert noble.lib().noble_linear_workspace_size(None, None, None) == NULL
+
+
+@pytest.mark.parametrize("shape,code", [
+    ((-1, 64, 64, 8), SHAPE), ((16, 0, 64, 8), SHAPE), ((16, 12, 64, 8), SHAPE),
+    ((16, 64, 60, 8), SHAPE), ((16, 64, 64, 4), SHAPE), ((16, 64, 64, 12), SHAPE),
+    ((16, 64, 64, 136), SHAPE), ((16, 64, 64, -8), SHAPE), ((16, 64, 64, 128), OK),
+    ((16, 64, 64, 0), OK), ((1 << 31, 64, 64, 8), SHAPE),
+])
+def test_shape_validation(shape, code):
+    assert _ws(*shape, noble.NOBLE_BF16)[0] == code
+
+
+def test_dtype_validation():
+    assert _ws(16, 64, 64, 8, 2)[0] == DTYPE
+    assert _ws(16, 64, 64, 8, -1)[0] == DTYPE
+
+
+def _fwd(desc, ptrs, scratch_bytes):
+    return noble.lib().noble_linear_fwd(ctypes.byref(desc), *ptrs, scratch_bytes, None)
+
+
+def _bwd(desc, ptrs, scratch_bytes):
+    return noble.lib().noble_linear_bwd(ctypes.byref(desc), *ptrs, scratch_bytes, None)
+
+
+FWD_ARGS = ["x", "W", "b", "W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up", "y", "reserve", "scratch"]
+BWD_ARGS = ["dy", "x", "W", "W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up", "reserve", "dx", "dW",
+            "db", "dW_down", "dM", "dW_up", "domega1", "dphi1", "domega2", "dphi2", "scratch"]
+NULLABLE = {"b", "db"}
+
+
+@pytest.mark.parametrize("which", FWD_ARGS)
+def test_fwd_rejects_null_and_misaligned(which):
+    d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_BF16)
+    _, scr = noble.noble_linear_workspace_size(64, 64, 64, 16, noble.NOBLE_BF16)
+    ptrs = list(FAKE[:len(FWD_ARGS)])
+    i = FWD_ARGS.index(which)
+    if which not in NULLABLE:
+        ptrs[i] = None
+        assert _fwd(d, ptrs, scr) == NULL
+    ptrs[i] = FAKE[i] + 4
+    assert _fwd(d, ptrs, scr) == MISAL
+
+
+@pytest.mark.parametrize("which", BWD_ARGS)
+def test_bwd_rejects_null_and_misaligned(which):
+    d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_F32)
+    _, scr = noble.noble_linear_workspace_size(64, 64, 64, 16, noble.NOBLE_F32)
+    ptrs = list(FAKE[:len(BWD_ARGS)])
+    i = BWD_ARGS.index(which)
+    if which not in NULLABLE:
+        ptrs[i] = None
+        assert _bwd(d, ptrs, scr) == NULL
+    ptrs[i] = FAKE[i] + 8
+    assert _bwd(d, ptrs, scr) == MISAL
+
+
+def test_workspace_too_small():
+    d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_BF16)
+    _, scr = noble.noble_linear_workspace_size(64, 64, 64, 16, noble.NOBLE_BF16)
+    assert _fwd(d, FAKE[:13], scr - 1) == WS
+    assert _bwd(d, FAKE[:22], scr - 256) == WS
+
+
+def test_bad_desc_rejected_by_fwd_and_bwd():
+    for d, code in ((noble.make_desc(64, 64, 64, 16, 7), DTYPE), (noble.make_desc(64, 64, 64, 20, 0), SHAPE)):
+        assert _fwd(d, FAKE[:13], 1 << 30) == code
+        assert _bwd(d, FAKE[:22], 1 << 30) == code
+    assert noble.lib().noble_linear_fwd(None, *FAKE[:13], 0, None) == NULL
+
+
+def test_plain_linear_branch_pointers_unchecked():
+    """With r = 0 the branch pointers are ignored (may be NULL); a NULL x is
+    still rejected, proving validation ran past them."""
+    d = noble.make_desc(64, 64, 64, 0, noble.NOBLE_BF16)
+    ptrs = list(FAKE[:13])
+    for k in ("W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up", "reserve", "scratch"):
+        ptrs[FWD_ARGS.index(k)] = None
+    ptrs[0] = None
+    assert _fwd(d, ptrs, 0) == NULL
