@@ -11,13 +11,14 @@
 #include <cstring>
 
 #include "noble.h"
+#include "noble_gemm_dma.hpp"
 #include "noble_kernels.hpp"
 
 using namespace noble;
 
 namespace {
 
-constexpr int64_t kMaxDim = int64_t(1) << 30;
+constexpr int64_t kMaxDim = int64_t(1) << 20;
 constexpr int64_t kMaxTokens = (int64_t(1) << 31) - 4096;
 constexpr size_t kAlign = 256;
 
@@ -104,8 +105,8 @@ Operand operand2(Seg s0, Seg s1, int nk1, int64_t rows) {
     return o;
 }
 
-// Main-product tile shape.
-constexpr int kBM = 128, kBN = 128, kWM = 2, kWN = 2;
+// Tile shape of the large products.
+constexpr int kBM = 256, kBN = 256;
 
 struct Batch {
     GemmBatch b{};
@@ -123,27 +124,33 @@ struct Batch {
         p.N = N;
         p.nk = nk;
         p.split = split;
+        p.tiles_m = cdiv(M, kBM);
         p.tiles_n = cdiv(N, kBN);
         p.tile_begin = blocks;
+        p.nblocks = p.tiles_m * p.tiles_n * split;
         p.out_f32 = out_f32 ? 1 : 0;
         p.atomic = split > 1 ? 1 : 0;
-        blocks += cdiv(M, kBM) * p.tiles_n * split;
+        blocks += p.nblocks;
     }
 };
 
-// Split-K factor: enough blocks to cover the chip twice over, at least four
-// K chunks per piece.
+// Split-K factor over tokens: enough blocks to give every CU one, while
+// keeping at least eight K chunks per piece.
 int choose_split(int tiles, int nk) {
     int s = 1;
-    while (tiles * s < 512 && s * 2 * 4 <= nk) s *= 2;
+    while (tiles * s < 256 && s * 2 * 8 <= nk) s *= 2;
     return s;
 }
 
 template <typename E, bool AK, bool BKM>
 noble_status launch_gemm(const Batch& bt, hipStream_t st) {
     if (bt.blocks == 0) return NOBLE_OK;
-    hipLaunchKernelGGL((gemm_kernel<E, kBM, kBN, kWM, kWN, AK, BKM>), dim3(bt.blocks), dim3(kThreads), 0, st,
-                       bt.b);
+    if constexpr (sizeof(E) == 2)
+        hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKM, !AK && !BKM>), dim3(bt.blocks), dim3(kDmaThreads), 0, st,
+                           bt.b);
+    else
+        hipLaunchKernelGGL((gemm_kernel<E, kBM, kBN, AK, BKM, !AK && !BKM>), dim3(bt.blocks), dim3(kThreads), 0,
+                           st, bt.b);
     return last_launch();
 }
 

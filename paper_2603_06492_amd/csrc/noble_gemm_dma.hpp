@@ -1,0 +1,298 @@
+// bf16 grouped MFMA GEMM for gfx950 with direct-to-LDS operand loads.
+//
+// Same problems and epilogue as gemm_kernel (noble_gemm.hpp), but operand
+// tiles never pass through VGPRs: buffer_load_dwordx4 ... lds writes each
+// lane's 16 bytes to LDS at (M0 base + 16 * lane).  Every operand keeps its
+// HBM orientation in LDS:
+//  - K-major tiles (rows of x, dy, W as W^T rows, C2, dH): [256 rows][128 B],
+//    16-byte chunk c of row r stored at physical chunk c ^ (r & 7); MFMA
+//    fragments come from ds_read_b128.
+//  - MN-major tiles (W in the forward, x and dy in the weight gradients):
+//    [64 k][512 B], 16-byte segment s of k-row k stored at physical segment
+//    s ^ 4(k & 3); fragments come from two ds_read_b64_tr_b16, each of which
+//    transposes a 4 (k) x 16 (m or n) block across a 16-lane group.
+// The swizzles make the fragment reads of each half-wave cover all 64 banks
+// once.  Two LDS stages: the loads of chunk k+1 are issued before chunk k is
+// multiplied.
+#pragma once
+
+#include <type_traits>
+
+#include "noble_gemm.hpp"
+#include "noble_tiles.hpp"
+
+namespace noble {
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+#define NOBLE_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor words (base, stride 0, num_records, gfx9 format word).
+__device__ __forceinline__ i32x4 make_desc(const char* base, int64_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const int n = bytes <= 0 ? 0 : (bytes >= 0x7fffffff ? 0x7fffffff : (int)bytes);
+    i32x4 d;
+    d[0] = (int)(uint32_t)a;
+    d[1] = (int)((uint32_t)(a >> 32) & 0xffffu);
+    d[2] = n;
+    d[3] = 0x00020000;
+    return d;
+}
+
+// 16 bytes per lane from the buffer into LDS at lds_dst + 16 * lane.  Issued
+// from asm: the compiler then does not treat later LDS reads of the other
+// stage as depending on this load; the kernel waits on vmcnt itself before
+// the barrier that publishes the stage.
+__device__ __forceinline__ void dma16(i32x4 desc, char* lds_dst, uint32_t voff, uint32_t soff) {
+    const uint32_t m0 = (uint32_t)reinterpret_cast<uintptr_t>(NOBLE_LDS(lds_dst));
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "buffer_load_dwordx4 %1, %2, %3 offen lds"
+        :
+        : "s"(m0), "v"(voff), "s"(desc), "s"(soff)
+        : "memory", "m0");
+}
+
+__device__ __forceinline__ uint64_t ds_read_tr(const char* p) {
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+    return __builtin_bit_cast(uint64_t, v);
+}
+
+// Issue the loads of one 256-row operand tile (one 64-element K chunk) into
+// `dst` (32 KB): 32 instructions of 1 KB shared by NW waves.
+template <bool KMAJ, int NW>
+__device__ __forceinline__ void dma_tile(const Operand& op, int row0, int kc, char* dst, int wave, int lane) {
+    constexpr int ES = 2, PERW = 32 / NW;
+    const bool second = kc >= op.nk1;
+    const char* ptr = second ? op.s[1].ptr : op.s[0].ptr;
+    const int64_t ld = second ? op.s[1].ld : op.s[0].ld;
+    const int klen = second ? op.s[1].klen : op.s[0].klen;
+    const int k0 = (second ? kc - op.nk1 : kc) * 64;
+    if constexpr (KMAJ) {
+        // block b = NW i + wave holds rows 8b .. 8b+7; lane p -> row 8b + p/8,
+        // physical chunk p%8 = logical chunk (p%8) ^ (p/8)
+        const i32x4 rs = make_desc(ptr + (int64_t)row0 * ld * ES, (int64_t)(op.rows - row0) * ld * ES);
+        const int rr = lane >> 3, c = (lane & 7) ^ rr;
+        const int k = k0 + c * 8;
+        const uint32_t vo = k < klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
+#pragma unroll
+        for (int i = 0; i < PERW; ++i) {
+            const int b = NW * i + wave;
+            dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)8 * b * ld * ES));
+        }
+    } else {
+        // instruction i of wave w holds k-rows 2(NW i + w) and the next; lane p
+        // -> k-row kr = 2(NW i + w) + p/32, physical segment p%32 holds logical
+        // segment (p%32) ^ 4(kr & 3)
+        const i32x4 rs = make_desc(ptr + (int64_t)k0 * ld * ES, (int64_t)(klen - k0) * ld * ES);
+        const int kq = lane >> 5;
+        const int seg = (lane & 31) ^ (4 * ((2 * wave + kq) & 3));
+        const int col = row0 + 8 * seg;
+        const uint32_t vo = col < op.rows ? (uint32_t)(((int64_t)kq * ld + col) * ES) : kOOB;
+#pragma unroll
+        for (int i = 0; i < PERW; ++i) {
+            const int kr = 2 * (NW * i + wave);
+            dma16(rs, dst + kr * 512, vo, (uint32_t)((int64_t)kr * ld * ES));
+        }
+    }
+}
+
+// MFMA fragment reads (32 x 32 x 16 bf16) of a wave whose block starts at
+// row/column w0 of the tile.
+//  K-major: fragment (i, s) at (kbase ^ s<<5) + 4096 i.
+//  MN-major: half t of fragment (i, s) at mbase + col[i] + (16 s + 4 t) 512,
+//  col[i] = 64 ((w0/32 + i) ^ c), c = (lane % 16) / 4.
+template <bool KMAJ, int T>
+struct FragAddr {
+    uint32_t base;
+    uint32_t col[T];
+    __device__ __forceinline__ FragAddr(int w0, int lane) {
+        if constexpr (KMAJ) {
+            const int r32 = lane & 31, h = lane >> 5;
+            base = (uint32_t)((w0 + r32) * 128 + ((h ^ (r32 & 7)) << 4));
+        } else {
+            const int g = lane >> 4, j = lane & 15, c = j >> 2;
+            const int x = 2 * (g & 1) + ((j & 3) >> 1);
+            base = (uint32_t)((8 * (g >> 1) + c) * 512 + 16 * x + 8 * (j & 1));
+#pragma unroll
+            for (int i = 0; i < T; ++i) col[i] = (uint32_t)(64 * (((w0 >> 5) + i) ^ c));
+        }
+    }
+    __device__ __forceinline__ u32x4 read(const char* tile, int i, int s) const {
+        if constexpr (KMAJ) {
+            return *reinterpret_cast<const u32x4*>(tile + ((base ^ ((uint32_t)s << 5)) + 4096u * i));
+        } else {
+            const char* p = tile + (base + col[i] + 512u * 16 * s);
+            const uint64_t lo = ds_read_tr(p);
+            const uint64_t hi = ds_read_tr(p + 4 * 512);
+            u32x4 v;
+            v[0] = (uint32_t)lo;
+            v[1] = (uint32_t)(lo >> 32);
+            v[2] = (uint32_t)hi;
+            v[3] = (uint32_t)(hi >> 32);
+            return v;
+        }
+    }
+};
+
+constexpr int kDmaWM = 2, kDmaWN = 4, kDmaThreads = 64 * kDmaWM * kDmaWN;
+
+template <bool AK, bool BKM, bool HAS_BSUM>
+__global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch batch) {
+    constexpr int BM = 256, BN = 256, NW = kDmaWM * kDmaWN;
+    constexpr int WTM = BM / kDmaWM, WTN = BN / kDmaWN;   // wave tile 128 x 64
+    constexpr int TM = WTM / 32, TN = WTN / 32;
+    constexpr int TILE = 256 * 128;   // bytes of one operand tile per stage
+    constexpr int STAGE = 2 * TILE;
+    // Two stages as two objects, so the compiler can tell the stage being
+    // filled by DMA from the one being read.
+    __shared__ __attribute__((aligned(1024))) char lds0[STAGE];
+    __shared__ __attribute__((aligned(1024))) char lds1[STAGE];
+
+    const int bid = blockIdx.x;
+    int q = 0;
+#pragma unroll
+    for (int t = 1; t < kMaxProblems; ++t)
+        if (t < batch.count && bid >= batch.p[t].tile_begin) q = t;
+    const GemmProblem& P = batch.p[q];
+
+    int L = bid - P.tile_begin;
+    if ((P.nblocks & 7) == 0) L = (L & 7) * (P.nblocks >> 3) + (L >> 3);
+    const int ntiles = P.tiles_m * P.tiles_n;
+    const int piece = L / ntiles;
+    const int tile = L - piece * ntiles;
+    const int span = kGroupM * P.tiles_n;
+    const int grp = tile / span, in = tile - grp * span;
+    const int first_m = grp * kGroupM;
+    const int gsz = min(P.tiles_m - first_m, kGroupM);
+    const int tm = first_m + in % gsz, tn = in / gsz;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kc0 = (int)((int64_t)P.nk * piece / P.split);
+    const int kc1 = (int)((int64_t)P.nk * (piece + 1) / P.split);
+
+    // The wave index is uniform; say so, so DMA offsets and LDS bases stay
+    // in SGPRs.
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm0 = (wave / kDmaWN) * WTM, wn0 = (wave % kDmaWN) * WTN;
+    const int r32 = lane & 31, h = lane >> 5;
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    const bool do_bsum = HAS_BSUM && (P.bsum != nullptr) && tm == 0 && wm0 == 0;
+    float bs[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bs[j] = 0.f;
+
+    if (kc0 < kc1) {
+        const FragAddr<AK, TM> fa(wm0, lane);
+        const FragAddr<BKM, TN> fb(wn0, lane);
+        dma_tile<AK, NW>(P.A, m0, kc0, lds0, wave, lane);
+        dma_tile<BKM, NW>(P.B, n0, kc0, lds0 + TILE, wave, lane);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+
+        // Multiply chunk kc from `cur` while chunk kc + 1 streams into `nxt`.
+        auto chunk = [&](int kc, const char* cur, char* nxt, auto bs_c) {
+            constexpr bool BS = decltype(bs_c)::value;
+            const char* ldsA = cur;
+            const char* ldsB = cur + TILE;
+            if (kc + 1 < kc1) {
+                dma_tile<AK, NW>(P.A, m0, kc + 1, nxt, wave, lane);
+                dma_tile<BKM, NW>(P.B, n0, kc + 1, nxt + TILE, wave, lane);
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                u32x4 a[TM], b[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) a[i] = fa.read(ldsA, i, s);
+#pragma unroll
+                for (int j = 0; j < TN; ++j) b[j] = fb.read(ldsB, j, s);
+                if constexpr (BS) {
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+#pragma unroll
+                        for (int w = 0; w < 4; ++w) bs[j] += bf2f(b[j][w] & 0xffffu) + bf2f(b[j][w] >> 16);
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) mma32<uint16_t>(acc[i][j], a[i], b[j]);
+            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+        };
+        auto run = [&](auto bs_c) {
+            int kc = kc0;
+            for (; kc + 1 < kc1; kc += 2) {
+                chunk(kc, lds0, lds1, bs_c);
+                chunk(kc + 1, lds1, lds0, bs_c);
+            }
+            if (kc < kc1) chunk(kc, lds0, lds1, bs_c);
+        };
+        if constexpr (HAS_BSUM) {
+            if (do_bsum)
+                run(std::true_type{});
+            else
+                run(std::false_type{});
+        } else {
+            run(std::false_type{});
+        }
+    }
+
+    if (do_bsum) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const float s = bs[j] + __shfl_xor(bs[j], 32);
+            const int col = n0 + wn0 + 32 * j + r32;
+            if (h == 0 && col < P.N) unsafeAtomicAdd(P.bsum + col, s);
+        }
+    }
+
+    // Output element v of acc[i][j] in lane l sits at row
+    // 32i + 8(v/4) + 4(l/32) + v%4, column 32j + l%32 of the wave block.
+    const bool add_bias = (P.bias != nullptr) && piece == 0;
+    const int es = P.out_f32 ? 4 : 2;
+    const __amdgpu_buffer_rsrc_t rc =
+        make_rsrc(static_cast<const char*>(P.C) + (int64_t)m0 * P.ldc * es, (int64_t)(P.M - m0) * P.ldc * es);
+    uint32_t voff[TM][TN];
+    float bcol[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = n0 + wn0 + 32 * j + r32;
+        bcol[j] = (add_bias && col < P.N) ? P.bias[col] : 0.f;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+            voff[i][j] = col < P.N ? (uint32_t)(((int64_t)(wm0 + 32 * i + 4 * h) * P.ldc + col) * es) : kOOB;
+    }
+    auto epilogue = [&](auto store) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    store(acc[i][j][v] + bcol[j], voff[i][j],
+                          (uint32_t)((int64_t)(8 * (v >> 2) + (v & 3)) * P.ldc * es));
+    };
+    if (P.atomic)
+        epilogue([&](float val, uint32_t vo, uint32_t so) {
+            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(val, rc, vo, so, 0);
+        });
+    else if (P.out_f32)
+        epilogue([&](float val, uint32_t vo, uint32_t so) {
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), rc, vo, so, 0);
+        });
+    else
+        epilogue([&](float val, uint32_t vo, uint32_t so) {
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(val), rc, vo, so, 0);
+        });
+}
+
+}  // namespace noble

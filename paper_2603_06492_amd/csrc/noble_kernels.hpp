@@ -18,6 +18,7 @@
 //                      the dW problem already stages.
 #pragma once
 
+#include "noble_gemm.hpp"
 #include "noble_tiles.hpp"
 
 namespace noble {
@@ -41,144 +42,6 @@ __global__ __launch_bounds__(256) void zero_kernel(ZeroList z) {
         for (int64_t i = gid; i < n4; i += stride)
             reinterpret_cast<f32x4*>(p)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
         for (int64_t i = (n4 << 2) + gid; i < n; i += stride) p[i] = 0.f;
-    }
-}
-
-// ------------------------------------------------------------ grouped GEMM --
-
-struct GemmProblem {
-    Operand A, B;
-    void* C;
-    int64_t ldc;
-    const float* bias;  // per output column, added by K piece 0 (nullable)
-    float* bsum;        // column sums of B over K, atomically added (nullable)
-    int M, N;
-    int nk;             // K chunks (both segments)
-    int split;          // K pieces; each piece accumulates atomically if > 1
-    int tiles_n;
-    int tile_begin;     // first block index of this problem
-    int out_f32;        // C holds float (1) or the storage type (0)
-    int atomic;         // atomicAdd into a zeroed float C
-};
-
-constexpr int kMaxProblems = 4;
-struct GemmBatch {
-    GemmProblem p[kMaxProblems];
-    int count;
-    int pad_;
-};
-
-template <typename E, int BM, int BN, int WM, int WN, bool AK, bool BKM>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmBatch batch) {
-    constexpr int TM = BM / WM / 16, TN = BN / WN / 16;
-    __shared__ __attribute__((aligned(16))) char lds[2 * (BM + BN) * kRowBytes];
-    const int bid = blockIdx.x;
-    int q = 0;
-#pragma unroll
-    for (int t = 1; t < kMaxProblems; ++t)
-        if (t < batch.count && bid >= batch.p[t].tile_begin) q = t;
-    const GemmProblem& P = batch.p[q];
-    const int local = bid - P.tile_begin;
-    const int piece = local % P.split, tile = local / P.split;
-    const int tm = tile / P.tiles_n, tn = tile % P.tiles_n;
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int kc0 = (int)((int64_t)P.nk * piece / P.split);
-    const int kc1 = (int)((int64_t)P.nk * (piece + 1) / P.split);
-
-    f32x4 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm0 = (wave / WN) * (BM / WM), wn0 = (wave % WN) * (BN / WN);
-    const int r16 = lane & 15, g = lane >> 4;
-
-    // Column sums of B (db = sum over tokens of dy) come from the B tiles this
-    // block stages anyway: one tile row of blocks, one wave row within it.
-    const bool do_bsum = (P.bsum != nullptr) && tm == 0 && (wave / WN) == 0;
-    float bs[TN];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) bs[j] = 0.f;
-
-    {
-        constexpr int STAGE = (BM + BN) * kRowBytes;
-        if (kc0 < kc1) {
-            Stage<E, BM, AK> sa;
-            Stage<E, BN, BKM> sb;
-            sa.load(P.A, m0, kc0, tid);
-            sb.load(P.B, n0, kc0, tid);
-            sa.store(lds, tid);
-            sb.store(lds + BM * kRowBytes, tid);
-            __syncthreads();
-            for (int kc = kc0; kc < kc1; ++kc) {
-                char* cur = lds + ((kc - kc0) & 1) * STAGE;
-                char* nxt = lds + (((kc - kc0) & 1) ^ 1) * STAGE;
-                const bool more = kc + 1 < kc1;
-                if (more) {
-                    sa.load(P.A, m0, kc + 1, tid);
-                    sb.load(P.B, n0, kc + 1, tid);
-                }
-                mma_chunk<E, TM, TN>(cur, cur + BM * kRowBytes, wm0, wn0, lane, acc);
-                if (do_bsum) {
-                    const char* ldsB = cur + BM * kRowBytes;
-#pragma unroll
-                    for (int s = 0; s < 2; ++s)
-#pragma unroll
-                        for (int j = 0; j < TN; ++j) {
-                            const u32x4 b = *reinterpret_cast<const u32x4*>(
-                                ldsB + lds_off(wn0 + 16 * j + r16, 4 * s + g));
-#pragma unroll
-                            for (int w = 0; w < 4; ++w) {
-                                if constexpr (sizeof(E) == 2)
-                                    bs[j] += bf2f(b[w] & 0xffffu) + bf2f(b[w] >> 16);
-                                else
-                                    bs[j] += __uint_as_float(b[w]);
-                            }
-                        }
-                }
-                if (more) {
-                    sa.store(nxt, tid);
-                    sb.store(nxt + BM * kRowBytes, tid);
-                }
-                __syncthreads();
-            }
-        }
-    }
-
-    if (do_bsum) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            float s = bs[j];
-            s += __shfl_xor(s, 16);
-            s += __shfl_xor(s, 32);
-            const int col = n0 + wn0 + 16 * j + r16;
-            if (g == 0 && col < P.N) unsafeAtomicAdd(P.bsum + col, s);
-        }
-    }
-
-    const bool add_bias = (P.bias != nullptr) && piece == 0;
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int col = n0 + wn0 + 16 * j + r16;
-        if (col >= P.N) continue;
-        const float bcol = add_bias ? P.bias[col] : 0.f;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int row = m0 + wm0 + 16 * i + 4 * g + v;
-                if (row >= P.M) continue;
-                const float val = acc[i][j][v] + bcol;
-                const int64_t off = (int64_t)row * P.ldc + col;
-                if (P.atomic)
-                    unsafeAtomicAdd(reinterpret_cast<float*>(P.C) + off, val);
-                else if (P.out_f32)
-                    reinterpret_cast<float*>(P.C)[off] = val;
-                else
-                    reinterpret_cast<E*>(P.C)[off] = to_elt<E>(val);
-            }
     }
 }
 

@@ -61,11 +61,24 @@ struct Operand {
     int rows;   // valid extent along M (operand A) or N (operand B)
 };
 
+// Raw buffer resource over [base, base + bytes).  Loads at offsets at or past
+// the end return zero, which is how tile edges and K tails are zero-filled
+// without branches.  Offsets inside one tile stay below 2^31.
+constexpr uint32_t kOOB = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const char* base, int64_t bytes) {
+    const int n = bytes <= 0 ? 0 : (bytes >= 0x7fffffff ? 0x7fffffff : (int)bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), (short)0, n, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t soff) {
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0);
+}
+
 // Global -> registers -> LDS staging of one R-row operand tile for one K chunk.
 template <typename E, int R, bool KMAJ>
 struct Stage {
     static constexpr int VEC = Elt<E>::VEC;
     static constexpr int BK = Elt<E>::BK;
+    static constexpr int ES = (int)sizeof(E);
     static constexpr int NB = R / VEC;                     // MN-major: vector columns
     static constexpr int UNITS = KMAJ ? R * 8 : 8 * NB;     // 16B chunks or VECxVEC blocks
     static constexpr int PER = (UNITS + kThreads - 1) / kThreads;
@@ -78,29 +91,31 @@ struct Stage {
         const int64_t ld = second ? op.s[1].ld : op.s[0].ld;
         const int klen = second ? op.s[1].klen : op.s[0].klen;
         const int k0 = (second ? kc - op.nk1 : kc) * BK;
+        if constexpr (KMAJ) {
+            // Tile rows row0.. of a [rows, ld] matrix; thread t loads rows
+            // t/8 + 32i, chunk t%8.  Rows past the matrix fall past the end.
+            static_assert(kThreads % 8 == 0 && (UNITS % kThreads == 0), "whole passes");
+            const __amdgpu_buffer_rsrc_t rs =
+                make_rsrc(ptr + (int64_t)row0 * ld * ES, (int64_t)(op.rows - row0) * ld * ES);
+            const int r = tid >> 3, k = k0 + (tid & 7) * VEC;
+            const uint32_t vo = k < klen ? (uint32_t)(((int64_t)r * ld + k) * ES) : kOOB;
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int u = tid + i * kThreads;
-            const bool live = (UNITS % kThreads == 0) || u < UNITS;
-            if constexpr (KMAJ) {
-                const int row = row0 + (u >> 3);
-                const int k = k0 + (u & 7) * VEC;
-                u32x4 val = {0u, 0u, 0u, 0u};
-                if (live && row < op.rows && k < klen)
-                    val = *reinterpret_cast<const u32x4*>(ptr + ((int64_t)row * ld + k) * (int64_t)sizeof(E));
-                v[i] = val;
-            } else {
+            for (int i = 0; i < PER; ++i)
+                v[i] = buf_load16(rs, vo, (uint32_t)((int64_t)i * (kThreads / 8) * ld * ES));
+        } else {
+            // K rows k0.. of a [klen, ld] matrix; VEC rows of one VEC-wide column
+            // block per thread.  K rows past the end fall past the end.
+            const __amdgpu_buffer_rsrc_t rs =
+                make_rsrc(ptr + (int64_t)k0 * ld * ES, (int64_t)(klen - k0) * ld * ES);
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                const int u = tid + i * kThreads;
                 const int kb = u / NB, nb = u % NB;
                 const int col = row0 + nb * VEC;
-                const bool okc = live && col < op.rows;
+                const bool ok = ((UNITS % kThreads == 0) || u < UNITS) && col < op.rows;
+                const uint32_t vo = ok ? (uint32_t)(((int64_t)kb * VEC * ld + col) * ES) : kOOB;
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    const int k = k0 + kb * VEC + e;
-                    u32x4 val = {0u, 0u, 0u, 0u};
-                    if (okc && k < klen)
-                        val = *reinterpret_cast<const u32x4*>(ptr + ((int64_t)k * ld + col) * (int64_t)sizeof(E));
-                    v[i * VEC + e] = val;
-                }
+                for (int e = 0; e < VEC; ++e) v[i * VEC + e] = buf_load16(rs, vo, (uint32_t)((int64_t)e * ld * ES));
             }
         }
     }
@@ -136,6 +151,66 @@ struct Stage {
                         for (int j = 0; j < 4; ++j) o[j] = v[i * 4 + j][n];
                         *reinterpret_cast<u32x4*>(lds + lds_off(nb * 4 + n, kb)) = o;
                     }
+                }
+            }
+        }
+    }
+
+    // Split staging for software pipelining: part p of NP.  K-major operands
+    // split their loads and stores evenly.  MN-major operands (a VEC x VEC
+    // transpose per thread needs all VEC rows) store everything and reload
+    // everything in part 0, which leaves the reload a whole K chunk of cover.
+    template <int NP>
+    __device__ __forceinline__ void load_part(const Operand& op, int row0, int kc, int tid, int p) {
+        static_assert(PER % NP == 0 || !KMAJ, "even split");
+        if constexpr (KMAJ) {
+            const bool second = kc >= op.nk1;
+            const char* ptr = second ? op.s[1].ptr : op.s[0].ptr;
+            const int64_t ld = second ? op.s[1].ld : op.s[0].ld;
+            const int klen = second ? op.s[1].klen : op.s[0].klen;
+            const int k0 = (second ? kc - op.nk1 : kc) * BK;
+            const __amdgpu_buffer_rsrc_t rs =
+                make_rsrc(ptr + (int64_t)row0 * ld * ES, (int64_t)(op.rows - row0) * ld * ES);
+            const int r = tid >> 3, k = k0 + (tid & 7) * VEC;
+            const uint32_t vo = k < klen ? (uint32_t)(((int64_t)r * ld + k) * ES) : kOOB;
+#pragma unroll
+            for (int i = p * (PER / NP); i < (p + 1) * (PER / NP); ++i)
+                v[i] = buf_load16(rs, vo, (uint32_t)((int64_t)i * (kThreads / 8) * ld * ES));
+        } else {
+            if (p == 0) load(op, row0, kc, tid);
+        }
+    }
+
+    template <int NP>
+    __device__ __forceinline__ void store_part(char* lds, int tid, int p) const {
+        if constexpr (KMAJ) {
+#pragma unroll
+            for (int i = p * (PER / NP); i < (p + 1) * (PER / NP); ++i) {
+                const int u = tid + i * kThreads;
+                *reinterpret_cast<u32x4*>(lds + lds_off(u >> 3, u & 7)) = v[i];
+            }
+        } else {
+            if (p != 0) return;
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                const int u = tid + i * kThreads;
+                if (!((UNITS % kThreads == 0) || u < UNITS)) continue;
+                const int kb = u / NB, nb = u % NB;
+#pragma unroll
+                for (int n = 0; n < VEC; ++n) {
+                    u32x4 o;
+                    if constexpr (VEC == 8) {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const uint32_t lo = v[i * 8 + 2 * j][n >> 1];
+                            const uint32_t hi = v[i * 8 + 2 * j + 1][n >> 1];
+                            o[j] = (n & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+                        }
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) o[j] = v[i * 4 + j][n];
+                    }
+                    *reinterpret_cast<u32x4*>(lds + lds_off(nb * VEC + n, kb)) = o;
                 }
             }
         }
