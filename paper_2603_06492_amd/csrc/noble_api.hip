@@ -13,6 +13,7 @@
 #include "noble.h"
 #include "noble_gemm_dma.hpp"
 #include "noble_kernels.hpp"
+#include "noble_skinny.hpp"
 
 using namespace noble;
 
@@ -154,6 +155,7 @@ noble_status launch_gemm(const Batch& bt, hipStream_t st) {
     return last_launch();
 }
 
+// float32 path: chain kernels with their own rank projection.
 template <typename E>
 noble_status launch_chain(bool fwd, int RP, const ChainArgs& a, int T, hipStream_t st) {
     const dim3 grid(cdiv(T, kChainRows)), block(kThreads);
@@ -175,6 +177,36 @@ noble_status launch_chain(bool fwd, int RP, const ChainArgs& a, int T, hipStream
     }
 #undef NOBLE_CHAIN
     return NOBLE_ERR_BAD_SHAPE;
+}
+
+// bf16 path: fused rank projection + CosNet chain (forward or backward).
+noble_status launch_branch(bool fwd, const ChainArgs& c, hipStream_t st) {
+    BranchArgs a{};
+    a.A = c.A;
+    a.B = c.B;
+    a.M = reinterpret_cast<const uint16_t*>(c.M);
+    a.w1 = c.w1;
+    a.p1 = c.p1;
+    a.w2 = c.w2;
+    a.p2 = c.p2;
+    a.H = c.H;
+    a.C1s = reinterpret_cast<uint16_t*>(c.C1s);
+    a.C2s = reinterpret_cast<uint16_t*>(c.C2s);
+    a.dH2s = reinterpret_cast<uint16_t*>(c.dH2s);
+    a.dHs = reinterpret_cast<uint16_t*>(c.dHs);
+    a.dw1 = c.dw1;
+    a.dp1 = c.dp1;
+    a.dw2 = c.dw2;
+    a.dp2 = c.dp2;
+    a.T = c.T;
+    a.r = c.r;
+    a.nk = c.nk;
+    const dim3 grid(cdiv(c.T, kSkRows)), block(kThreads);
+    if (fwd)
+        hipLaunchKernelGGL(branch_fwd_kernel, grid, block, 0, st, a);
+    else
+        hipLaunchKernelGGL(branch_bwd_kernel, grid, block, 0, st, a);
+    return last_launch();
 }
 
 // Padded rank of the chain kernels: a multiple of the K chunk, instantiated
@@ -206,7 +238,10 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
         a.T = (int)T;
         a.r = (int)r;
         a.nk = cdiv(din, BK);
-        NOBLE_TRY(launch_chain<E>(true, chain_rp<E>(r), a, (int)T, st));
+        if constexpr (sizeof(E) == 2)
+            NOBLE_TRY(launch_branch(true, a, st));
+        else
+            NOBLE_TRY(launch_chain<E>(true, chain_rp<E>(r), a, (int)T, st));
     }
     // y = [x | C2] [W ; W_up] + b
     const int nk1 = cdiv(din, BK);
@@ -281,7 +316,10 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         a.T = (int)T;
         a.r = (int)r;
         a.nk = cdiv(dout, BK);
-        NOBLE_TRY(launch_chain<E>(false, chain_rp<E>(r), a, (int)T, st));
+        if constexpr (sizeof(E) == 2)
+            NOBLE_TRY(launch_branch(false, a, st));
+        else
+            NOBLE_TRY(launch_chain<E>(false, chain_rp<E>(r), a, (int)T, st));
     }
 
     // dx = [dy | dH] [W^T ; W_down^T]   (B(k, n) stored [n][k]: K-major)

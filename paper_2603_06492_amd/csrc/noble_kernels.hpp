@@ -1,4 +1,6 @@
-// NOBLE-CosNet linear layer kernels for gfx950.
+// NOBLE-CosNet linear layer kernels for gfx950: the zero fill used before the
+// atomically reduced gradients, and the float32-path chain kernels (the bf16
+// path uses the fused branch kernels of noble_skinny.hpp).
 //
 // Forward (Eq. 1 with the CosNet of Eq. 2):
 //   fwd_chain_kernel : H = x W_down (MFMA), C1 = cos(H w1 + p1), H2 = C1 M

@@ -1,0 +1,390 @@
+// The rank-r side of the layer, bf16 path, as two fused kernels on gfx950:
+//
+//   branch_fwd_kernel:  H = x W_down (MFMA), then per token the CosNet chain
+//                       C1 = cos(H w1 + p1), H2 = C1 M (MFMA), C2 = cos(H2 w2 + p2).
+//                       Writes H (float32, the reserve) and C2 (bf16, scratch).
+//   branch_bwd_kernel:  dC2 = dy W_up^T (MFMA), then the chain backwards from
+//                       the saved H: C1, sin A1, H2 = C1 M, C2, sin A2,
+//                       dA2 = -sin(A2) dC2, dH2 = dA2 w2, dC1 = dH2 M^T (MFMA),
+//                       dA1 = -sin(A1) dC1, dH = dA1 w1.  Writes C1, C2, dH2, dH
+//                       (bf16 scratch, operands of the weight-gradient products)
+//                       and reduces dw1, dp1, dw2, dp2 over its tokens with wave
+//                       shuffles, then one float atomic per column.
+//
+// Both stream a [T, K] bf16 operand once (x or dy) against a rank operand that
+// stays in L2, so the main loop is built for bytes in flight: 32 tokens x 128
+// ranks per workgroup, a five-stage LDS ring filled by buffer_load ... lds.
+// Four waves each own 32 of the 128 rank columns (one 32x32x16 MFMA per K
+// step).  M [r, r] is loaded into LDS once per workgroup, at the start, in its
+// HBM layout [r_in][r_out]; C1 M reads it with ds_read_b64_tr_b16 and
+// dH2 M^T with ds_read_b128.
+#pragma once
+
+#include "noble_gemm_dma.hpp"
+
+namespace noble {
+
+constexpr int kSkRows = 32;     // tokens per workgroup
+constexpr int kSkN = 128;       // padded rank columns
+constexpr int kSkStages = 5;
+constexpr int kSkA = kSkRows * 128;       // A bytes per stage (32 rows x 128 B)
+constexpr int kSkB = kSkN * 128;          // B bytes per stage (16 KB either layout)
+constexpr int kSkStage = kSkA + kSkB;
+constexpr int kSkM = kSkN * kSkN * 2;     // M tile, 128 x 128 bf16
+constexpr int kSkC = kSkRows * kSkN * 2;  // C1 / dH2 operand tile, 32 x 128 bf16
+constexpr int kSkLds = kSkStages * kSkStage + kSkM + kSkC;
+constexpr int kSkLoads = 5;               // DMA instructions per wave per K chunk
+
+struct BranchArgs {
+    Operand A;            // [T, K] K-major: x (forward) or dy (backward)
+    Operand B;            // W_down [K, r] MN-major (forward) or W_up [r, K] K-major (backward)
+    const uint16_t* M;    // [r, r]
+    const float* w1;
+    const float* p1;
+    const float* w2;
+    const float* p2;
+    float* H;             // reserve [T, r] float32
+    uint16_t* C1s;        // scratch [T, r] bf16 (backward)
+    uint16_t* C2s;        // scratch [T, r] bf16
+    uint16_t* dH2s;       // scratch [T, r] bf16 (backward)
+    uint16_t* dHs;        // scratch [T, r] bf16 (backward)
+    float* dw1;
+    float* dp1;
+    float* dw2;
+    float* dp2;
+    int T, r, nk, pad_;
+};
+
+// s_waitcnt with only the vector-memory count constrained (gfx9 encoding).
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// sin and cos of x: reduction to one period in turns (x / 2 pi minus the
+// nearest integer), then the hardware v_sin_f32 / v_cos_f32, which take their
+// argument in turns.  Absolute error about 1e-6 for |x| in the range the
+// layer produces, far below the bf16 operand rounding that follows.
+__device__ __forceinline__ float turns(float x) {
+    const float t = x * 0.15915494309189535f;
+    return t - __builtin_rintf(t);
+}
+__device__ __forceinline__ float fast_cos(float x) { return __builtin_amdgcn_cosf(turns(x)); }
+__device__ __forceinline__ void fast_sincos(float x, float& s, float& c) {
+    const float t = turns(x);
+    s = __builtin_amdgcn_sinf(t);
+    c = __builtin_amdgcn_cosf(t);
+}
+
+// One K chunk of the rank projection: 5 DMA instructions per wave.
+template <bool BKM>
+__device__ __forceinline__ void branch_dma(const BranchArgs& a, int row0, int kc, char* st, int wave, int lane) {
+    constexpr int ES = 2;
+    // A: 32 rows, wave w loads rows 8w .. 8w+7 (lane p: row 8w + p/8, physical
+    // chunk p%8 holding logical chunk (p%8) ^ (p/8)).
+    {
+        const Operand& op = a.A;
+        const int64_t ld = op.s[0].ld;
+        const int k0 = kc * 64;
+        const i32x4 rs = make_desc(op.s[0].ptr + (int64_t)row0 * ld * ES, (int64_t)(op.rows - row0) * ld * ES);
+        const int rr = lane >> 3, c = (lane & 7) ^ rr;
+        const int k = k0 + c * 8;
+        const uint32_t vo = k < op.s[0].klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
+        dma16(rs, st + wave * 1024, vo, (uint32_t)((int64_t)8 * wave * ld * ES));
+    }
+    const Operand& op = a.B;
+    const int64_t ld = op.s[0].ld;
+    const int klen = op.s[0].klen;
+    const int k0 = kc * 64;
+    char* dst = st + kSkA;
+    if constexpr (BKM) {
+        // 128 rows (ranks) x 128 B, block b = 4i + w holds rows 8b .. 8b+7
+        const i32x4 rs = make_desc(op.s[0].ptr, (int64_t)op.rows * ld * ES);
+        const int rr = lane >> 3, c = (lane & 7) ^ rr;
+        const int k = k0 + c * 8;
+        const uint32_t vo = k < klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int b = 4 * i + wave;
+            dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)8 * b * ld * ES));
+        }
+    } else {
+        // 64 k-rows x 256 B, block b = 4i + w holds k-rows 4b .. 4b+3; lane p ->
+        // k-row 4b + p/16, physical segment p%16 holding logical (p%16) ^ 4(p/16)
+        const i32x4 rs = make_desc(op.s[0].ptr + (int64_t)k0 * ld * ES, (int64_t)(klen - k0) * ld * ES);
+        const int kq = lane >> 4;
+        const int seg = (lane & 15) ^ (4 * kq);
+        const int col = 8 * seg;
+        const uint32_t vo = col < op.rows ? (uint32_t)(((int64_t)kq * ld + col) * ES) : kOOB;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int b = 4 * i + wave;
+            dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)4 * b * ld * ES));
+        }
+    }
+}
+
+// M [r, r] into LDS as [128 r_in][256 B], 16-byte segment s of row p at
+// physical segment s ^ 4(p & 3); rows / columns past r read as zero.
+__device__ __forceinline__ void m_dma(const uint16_t* M, int r, char* dst, int wave, int lane) {
+    const i32x4 rs = make_desc(reinterpret_cast<const char*>(M), (int64_t)r * r * 2);
+    const int kq = lane >> 4;
+    const int seg = (lane & 15) ^ (4 * kq);
+    const int col = 8 * seg;
+    const uint32_t vo = col < r ? (uint32_t)(((int64_t)kq * r + col) * 2) : kOOB;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int b = 4 * i + wave;   // rows 4b .. 4b+3
+        dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)4 * b * r * 2));
+    }
+}
+
+// Transposed 8-row read of a [k][256 B] tile (16-byte segments swizzled by
+// 4(k & 3)): lane l receives the column 32 w + l % 32 for k rows
+// 8 (l / 32) .. +7 of K step s.
+__device__ __forceinline__ uint32_t tr_base(int w, int lane) {
+    const int g = lane >> 4, j = lane & 15, c = j >> 2;
+    const int x = 2 * (g & 1) + ((j & 3) >> 1);
+    return (uint32_t)((8 * (g >> 1) + c) * 256 + 64 * (w ^ c) + 16 * x + 8 * (j & 1));
+}
+__device__ __forceinline__ u32x4 tr_read8(const char* tile, uint32_t base, int s) {
+    const char* p = tile + base + 256u * 16 * s;
+    const uint64_t lo = ds_read_tr(p);
+    const uint64_t hi = ds_read_tr(p + 4 * 256);
+    u32x4 v;
+    v[0] = (uint32_t)lo;
+    v[1] = (uint32_t)(lo >> 32);
+    v[2] = (uint32_t)hi;
+    v[3] = (uint32_t)(hi >> 32);
+    return v;
+}
+
+// Byte offset of element (row, col) of the 32 x 128 bf16 operand tile, laid
+// out K-major as two 64-column chunks of [32 rows][128 B], chunk c of row
+// stored at c ^ (row & 7).
+__device__ __forceinline__ int ctile_off(int row, int col) {
+    return (col >> 6) * 4096 + row * 128 + ((((col >> 3) & 7) ^ (row & 7)) << 4) + (col & 7) * 2;
+}
+
+// acc (one 32x32 block per wave) over K steps of a [32 x 128] tile in LDS
+// (A, K-major) times the M tile, either M itself (TRANS_M = false: B(k, n) =
+// M[k][n]) or M^T (B(k, n) = M[n][k]).
+template <bool TRANS_M>
+__device__ __forceinline__ void mix_mma(const char* ctile, const char* mt, int wave, int lane, f32x16& acc) {
+    const int r32 = lane & 31, h = lane >> 5;
+    const uint32_t tb = tr_base(wave, lane);
+    const int p = 32 * wave + r32;   // row of M for the M^T product
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        const int q = 2 * s + h;  // 8-element K group of this lane
+        const u32x4 av = *reinterpret_cast<const u32x4*>(ctile + (q >> 3) * 4096 + r32 * 128 +
+                                                         ((((q & 7) ^ (r32 & 7))) << 4));
+        u32x4 bv;
+        if constexpr (!TRANS_M)
+            bv = tr_read8(mt, tb, s);
+        else
+            bv = *reinterpret_cast<const u32x4*>(mt + p * 256 + ((q ^ (4 * (p & 3))) << 4));
+        mma32<uint16_t>(acc, av, bv);
+    }
+}
+
+// Main loop of the rank projection: acc (rows 8(v/4) + 4(l/32) + v%4, rank
+// column 32 wave + l%32) = A rows [row0, row0 + 32) times B over all K.
+template <bool BKM>
+__device__ __forceinline__ void branch_mainloop(const BranchArgs& a, int row0, char* lds, int wave, int lane,
+                                                f32x16& acc) {
+    const int r32 = lane & 31, h = lane >> 5;
+    const int nk = a.nk;
+    const uint32_t fa = (uint32_t)(r32 * 128 + ((h ^ (r32 & 7)) << 4));
+    uint32_t fb;
+    if constexpr (BKM)
+        fb = (uint32_t)((32 * wave + r32) * 128 + ((h ^ (r32 & 7)) << 4));
+    else
+        fb = tr_base(wave, lane);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+#pragma unroll
+    for (int c = 0; c < kSkStages - 1; ++c)
+        if (c < nk) branch_dma<BKM>(a, row0, c, lds + c * kSkStage, wave, lane);
+    for (int kc = 0; kc < nk; ++kc) {
+        // chunk kc has landed once at most (stages - 2) later chunks are in flight
+        const int ahead = min(nk - 1 - kc, kSkStages - 2);
+        if (ahead >= 3)
+            wait_vmcnt<3 * kSkLoads>();
+        else if (ahead == 2)
+            wait_vmcnt<2 * kSkLoads>();
+        else if (ahead == 1)
+            wait_vmcnt<kSkLoads>();
+        else
+            wait_vmcnt<0>();
+        __syncthreads();
+        if (kc + kSkStages - 1 < nk)
+            branch_dma<BKM>(a, row0, kc + kSkStages - 1, lds + ((kc + kSkStages - 1) % kSkStages) * kSkStage, wave,
+                            lane);
+        const char* st = lds + (kc % kSkStages) * kSkStage;
+        const char* sb = st + kSkA;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const u32x4 av = *reinterpret_cast<const u32x4*>(st + (fa ^ ((uint32_t)s << 5)));
+            u32x4 bv;
+            if constexpr (BKM)
+                bv = *reinterpret_cast<const u32x4*>(sb + (fb ^ ((uint32_t)s << 5)));
+            else
+                bv = tr_read8(sb, fb, s);
+            mma32<uint16_t>(acc, av, bv);
+        }
+    }
+}
+
+// Sum over the 32 rows of a wave's block, per column (lanes l and l ^ 32
+// hold the same column); every lane returns the column total.
+__device__ __forceinline__ float block_colsum(const float (&x)[16]) {
+    float s = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s += x[v];
+    return s + __shfl_xor(s, 32);
+}
+
+__global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
+    __shared__ __attribute__((aligned(1024))) char lds[kSkLds];
+    char* mt = lds + kSkStages * kSkStage;
+    char* ct = mt + kSkM;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r32 = lane & 31, h = lane >> 5;
+    const int row0 = blockIdx.x * kSkRows;
+    const int r = a.r;
+
+    m_dma(a.M, r, mt, wave, lane);   // lands while the projection streams
+    f32x16 acc;
+    branch_mainloop<false>(a, row0, lds, wave, lane, acc);
+
+    // acc[v]: token row0 + 8(v/4) + 4h + v%4, rank column 32 wave + r32
+    const int col = 32 * wave + r32;
+    const bool cv = col < r;
+    const float w1 = cv ? a.w1[col] : 0.f, p1 = cv ? a.p1[col] : 0.f;
+    const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
+    const __amdgpu_buffer_rsrc_t rh =
+        make_rsrc(reinterpret_cast<const char*>(a.H) + (int64_t)row0 * r * 4, (int64_t)(a.T - row0) * r * 4);
+    const __amdgpu_buffer_rsrc_t rc =
+        make_rsrc(reinterpret_cast<const char*>(a.C2s) + (int64_t)row0 * r * 2, (int64_t)(a.T - row0) * r * 2);
+    const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
+    const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * r + col) * 2) : kOOB;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4,
+                                              (uint32_t)((8 * (v >> 2) + (v & 3)) * r * 4), 0);
+        const float c1 = cv ? fast_cos(acc[v] * w1 + p1) : 0.f;
+        *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = (uint16_t)f2bf(c1);
+    }
+    __syncthreads();   // C1 tile complete; M landed (the main loop drained vmcnt)
+
+    f32x16 h2;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) h2[v] = 0.f;
+    mix_mma<false>(ct, mt, wave, lane, h2);
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(fast_cos(h2[v] * w2 + p2)), rc, vo2,
+                                              (uint32_t)((8 * (v >> 2) + (v & 3)) * r * 2), 0);
+}
+
+__global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
+    __shared__ __attribute__((aligned(1024))) char lds[kSkLds];
+    char* mt = lds + kSkStages * kSkStage;
+    char* ct = mt + kSkM;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r32 = lane & 31, h = lane >> 5;
+    const int row0 = blockIdx.x * kSkRows;
+    const int r = a.r;
+
+    m_dma(a.M, r, mt, wave, lane);
+    f32x16 dc2;
+    branch_mainloop<true>(a, row0, lds, wave, lane, dc2);   // dC2 = dy W_up^T
+
+    const int col = 32 * wave + r32;
+    const bool cv = col < r;
+    const float w1 = cv ? a.w1[col] : 0.f, p1 = cv ? a.p1[col] : 0.f;
+    const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
+    const int64_t rows_left = a.T - row0;
+    const __amdgpu_buffer_rsrc_t rh =
+        make_rsrc(reinterpret_cast<const char*>(a.H) + (int64_t)row0 * r * 4, rows_left * r * 4);
+    auto rs16 = [&](uint16_t* base) {
+        return make_rsrc(reinterpret_cast<const char*>(base) + (int64_t)row0 * r * 2, rows_left * r * 2);
+    };
+    const __amdgpu_buffer_rsrc_t rc1 = rs16(a.C1s), rc2 = rs16(a.C2s), rdh2 = rs16(a.dH2s), rdh = rs16(a.dHs);
+    const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
+    const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * r + col) * 2) : kOOB;
+    auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * r * es); };
+
+    // H from the reserve (rows past T and columns past r read as zero)
+    float hr[16], s1[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+        hr[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rh, vo4, soff(v, 4), 0));
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
+        float sn = 0.f, cs = 0.f;
+        if (cv) fast_sincos(hr[v] * w1 + p1, sn, cs);
+        s1[v] = sn;
+        const uint16_t c1 = (uint16_t)f2bf(cs);
+        *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = c1;
+        __builtin_amdgcn_raw_buffer_store_b16(c1, rc1, vo2, soff(v, 2), 0);
+    }
+    __syncthreads();
+
+    f32x16 h2;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) h2[v] = 0.f;
+    mix_mma<false>(ct, mt, wave, lane, h2);   // H2 = C1 M
+    __syncthreads();                           // done reading C1 from LDS
+
+    float da2h2[16], da2[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
+        const bool ok = cv && row < rows_left;
+        float sn = 0.f, cs = 0.f;
+        if (cv) fast_sincos(h2[v] * w2 + p2, sn, cs);
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(cs), rc2, vo2, soff(v, 2), 0);
+        const float d = ok ? -sn * dc2[v] : 0.f;   // dA2
+        da2[v] = d;
+        da2h2[v] = d * h2[v];
+        const uint16_t dh2 = (uint16_t)f2bf(d * w2);
+        *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = dh2;
+        __builtin_amdgcn_raw_buffer_store_b16(dh2, rdh2, vo2, soff(v, 2), 0);
+    }
+    {
+        const float sw = block_colsum(da2h2), sp = block_colsum(da2);
+        if (h == 0 && cv) {
+            unsafeAtomicAdd(a.dw2 + col, sw);
+            unsafeAtomicAdd(a.dp2 + col, sp);
+        }
+    }
+    __syncthreads();   // dH2 tile complete
+
+    f32x16 dc1;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dc1[v] = 0.f;
+    mix_mma<true>(ct, mt, wave, lane, dc1);   // dC1 = dH2 M^T
+
+    float da1h[16], da1[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
+        const bool ok = cv && row < rows_left;
+        const float d = ok ? -s1[v] * dc1[v] : 0.f;   // dA1
+        da1[v] = d;
+        da1h[v] = d * hr[v];
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(d * w1), rdh, vo2, soff(v, 2), 0);
+    }
+    const float sw = block_colsum(da1h), sp = block_colsum(da1);
+    if (h == 0 && cv) {
+        unsafeAtomicAdd(a.dw1 + col, sw);
+        unsafeAtomicAdd(a.dp1 + col, sp);
+    }
+}
+
+}  // namespace noble

@@ -51,6 +51,7 @@ def _ws(T, di, do, r, dt):
 
 
 def test_workspace_sizes():
+    # four storage-type [T, r] regions
     st, res, scr = _ws(8192, 2048, 2048, 128, noble.NOBLE_BF16)
     assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2
     st, res, scr = _ws(256, 64, 64, 8, noble.NOBLE_F32)
