@@ -209,6 +209,12 @@ noble_status launch_branch(bool fwd, const ChainArgs& c, hipStream_t st) {
     return last_launch();
 }
 
+// K chunk of the large products (128 bytes of a row: 64 bf16 or 32 f32).
+template <typename E>
+constexpr int gemm_bk() {
+    return Elt<E>::BK;
+}
+
 // Padded rank of the chain kernels: a multiple of the K chunk, instantiated
 // for 64 and 128 (bf16) and 32, 64 and 128 (f32).
 template <typename E>
@@ -244,8 +250,9 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
             NOBLE_TRY(launch_chain<E>(true, chain_rp<E>(r), a, (int)T, st));
     }
     // y = [x | C2] [W ; W_up] + b
-    const int nk1 = cdiv(din, BK);
-    const int nk = nk1 + (r > 0 ? cdiv(r, BK) : 0);
+    constexpr int GBK = gemm_bk<E>();
+    const int nk1 = cdiv(din, GBK);
+    const int nk = nk1 + (r > 0 ? cdiv(r, GBK) : 0);
     Batch bt;
     bt.add(operand2(seg(x, din, din), seg(C2s, r, r), nk1, T), operand2(seg(W, dout, din), seg(Wu, dout, r), nk1, dout),
            (int)T, (int)dout, nk, y, dout, sizeof(E) == 4, b, nullptr, 1);
@@ -267,7 +274,8 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     char* dHs = base + 3 * reg;
 
     // Plan the weight-gradient batch first: dW needs zeroing only if split.
-    const int nkT = cdiv(T, BK);
+    constexpr int GBK = gemm_bk<E>();
+    const int nkT = cdiv(T, GBK);
     const int split_dW = T > 0 ? choose_split(cdiv(din, kBM) * cdiv(dout, kBN), nkT) : 1;
 
     ZeroList z{};
@@ -324,8 +332,8 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
 
     // dx = [dy | dH] [W^T ; W_down^T]   (B(k, n) stored [n][k]: K-major)
     {
-        const int nk1 = cdiv(dout, BK);
-        const int nk = nk1 + (r > 0 ? cdiv(r, BK) : 0);
+        const int nk1 = cdiv(dout, GBK);
+        const int nk = nk1 + (r > 0 ? cdiv(r, GBK) : 0);
         Batch bt;
         bt.add(operand2(seg(dy, dout, dout), seg(dHs, r, r), nk1, T), operand2(seg(W, dout, dout), seg(Wd, r, r), nk1, din),
                (int)T, (int)din, nk, dx, din, sizeof(E) == 4, nullptr, nullptr, 1);

@@ -5,15 +5,16 @@
 // lane's 16 bytes to LDS at (M0 base + 16 * lane).  Every operand keeps its
 // HBM orientation in LDS:
 //  - K-major tiles (rows of x, dy, W as W^T rows, C2, dH): [256 rows][128 B],
-//    16-byte chunk c of row r stored at physical chunk c ^ (r & 7); MFMA
-//    fragments come from ds_read_b128.
+//    16-byte chunk c of row r stored at physical chunk c ^ ((r ^ r/8) & 7);
+//    MFMA fragments come from ds_read_b128.
 //  - MN-major tiles (W in the forward, x and dy in the weight gradients):
 //    [64 k][512 B], 16-byte segment s of k-row k stored at physical segment
 //    s ^ 4(k & 3); fragments come from two ds_read_b64_tr_b16, each of which
 //    transposes a 4 (k) x 16 (m or n) block across a 16-lane group.
-// The swizzles make the fragment reads of each half-wave cover all 64 banks
-// once.  Two LDS stages: the loads of chunk k+1 are issued before chunk k is
-// multiplied.
+// The swizzles make every fragment read pass cover the 64 LDS banks once.
+// Two LDS stages: the loads of chunk k+1 are issued before chunk k is
+// multiplied; fragment reads of the next K step are interleaved one-to-one
+// with the MFMAs of the current one.
 #pragma once
 
 #include <type_traits>
@@ -71,14 +72,16 @@ __device__ __forceinline__ void dma_tile(const Operand& op, int row0, int kc, ch
     const int k0 = (second ? kc - op.nk1 : kc) * 64;
     if constexpr (KMAJ) {
         // block b = NW i + wave holds rows 8b .. 8b+7; lane p -> row 8b + p/8,
-        // physical chunk p%8 = logical chunk (p%8) ^ (p/8)
+        // physical chunk p%8 = logical chunk (p%8) ^ swz(row), where
+        // swz(row) = (row ^ row/8) & 7 = (p/8) ^ (b & 7).
         const i32x4 rs = make_desc(ptr + (int64_t)row0 * ld * ES, (int64_t)(op.rows - row0) * ld * ES);
-        const int rr = lane >> 3, c = (lane & 7) ^ rr;
-        const int k = k0 + c * 8;
-        const uint32_t vo = k < klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
+        const int rr = lane >> 3;
 #pragma unroll
         for (int i = 0; i < PERW; ++i) {
             const int b = NW * i + wave;
+            const int c = (lane & 7) ^ rr ^ (b & 7);
+            const int k = k0 + c * 8;
+            const uint32_t vo = k < klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
             dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)8 * b * ld * ES));
         }
     } else {
@@ -98,9 +101,18 @@ __device__ __forceinline__ void dma_tile(const Operand& op, int row0, int kc, ch
     }
 }
 
+// s_waitcnt with only the vector-memory count constrained (gfx9 encoding).
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // MFMA fragment reads (32 x 32 x 16 bf16) of a wave whose block starts at
-// row/column w0 of the tile.
-//  K-major: fragment (i, s) at (kbase ^ s<<5) + 4096 i.
+// row/column w0 of the tile (w0 a multiple of 64).
+//  K-major: fragment (i, s) at (kbase ^ s<<5 ^ (i&1)<<6) + 4096 i; with
+//  swz(row) = (row ^ row/8) & 7 a 16-lane pass of ds_read_b128 (16
+//  consecutive rows, one logical chunk) covers all 64 banks.
 //  MN-major: half t of fragment (i, s) at mbase + col[i] + (16 s + 4 t) 512,
 //  col[i] = 64 ((w0/32 + i) ^ c), c = (lane % 16) / 4.
 template <bool KMAJ, int T>
@@ -110,7 +122,7 @@ struct FragAddr {
     __device__ __forceinline__ FragAddr(int w0, int lane) {
         if constexpr (KMAJ) {
             const int r32 = lane & 31, h = lane >> 5;
-            base = (uint32_t)((w0 + r32) * 128 + ((h ^ (r32 & 7)) << 4));
+            base = (uint32_t)((w0 + r32) * 128 + ((h ^ (r32 & 7) ^ (r32 >> 3)) << 4));
         } else {
             const int g = lane >> 4, j = lane & 15, c = j >> 2;
             const int x = 2 * (g & 1) + ((j & 3) >> 1);
@@ -121,7 +133,8 @@ struct FragAddr {
     }
     __device__ __forceinline__ u32x4 read(const char* tile, int i, int s) const {
         if constexpr (KMAJ) {
-            return *reinterpret_cast<const u32x4*>(tile + ((base ^ ((uint32_t)s << 5)) + 4096u * i));
+            return *reinterpret_cast<const u32x4*>(tile + ((base ^ ((uint32_t)s << 5) ^ ((uint32_t)(i & 1) << 6)) +
+                                                           4096u * i));
         } else {
             const char* p = tile + (base + col[i] + 512u * 16 * s);
             const uint64_t lo = ds_read_tr(p);
@@ -207,23 +220,42 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
                 dma_tile<AK, NW>(P.A, m0, kc + 1, nxt, wave, lane);
                 dma_tile<BKM, NW>(P.B, n0, kc + 1, nxt + TILE, wave, lane);
             }
+            // Fragments of K step s + 1 are read while the MFMAs of step s run:
+            // one LDS read issued per MFMA (schedule pinned below).
+            constexpr int NREAD = TM * (AK ? 1 : 2) + TN * (BKM ? 1 : 2);
+            constexpr int NMFMA = TM * TN;
+            u32x4 a[2][TM], b[2][TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) a[0][i] = fa.read(ldsA, i, 0);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) b[0][j] = fb.read(ldsB, j, 0);
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                u32x4 a[TM], b[TN];
+                const int cb = s & 1, nb = cb ^ 1;
+                __builtin_amdgcn_sched_barrier(0);
+                if (s + 1 < 4) {
 #pragma unroll
-                for (int i = 0; i < TM; ++i) a[i] = fa.read(ldsA, i, s);
+                    for (int i = 0; i < TM; ++i) a[nb][i] = fa.read(ldsA, i, s + 1);
 #pragma unroll
-                for (int j = 0; j < TN; ++j) b[j] = fb.read(ldsB, j, s);
+                    for (int j = 0; j < TN; ++j) b[nb][j] = fb.read(ldsB, j, s + 1);
+                }
                 if constexpr (BS) {
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
 #pragma unroll
-                        for (int w = 0; w < 4; ++w) bs[j] += bf2f(b[j][w] & 0xffffu) + bf2f(b[j][w] >> 16);
+                        for (int w = 0; w < 4; ++w) bs[j] += bf2f(b[cb][j][w] & 0xffffu) + bf2f(b[cb][j][w] >> 16);
                 }
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
-                    for (int j = 0; j < TN; ++j) mma32<uint16_t>(acc[i][j], a[i], b[j]);
+                    for (int j = 0; j < TN; ++j) mma32<uint16_t>(acc[i][j], a[cb][i], b[cb][j]);
+                if (s + 1 < 4) {
+#pragma unroll
+                    for (int qq = 0; qq < NMFMA; ++qq) {
+                        if (qq < NREAD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                   // MFMA
+                    }
+                }
             }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             __syncthreads();

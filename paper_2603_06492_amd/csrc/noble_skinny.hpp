@@ -55,13 +55,6 @@ struct BranchArgs {
     int T, r, nk, pad_;
 };
 
-// s_waitcnt with only the vector-memory count constrained (gfx9 encoding).
-template <int VM>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(VM >= 0 && VM < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 // sin and cos of x: reduction to one period in turns (x / 2 pi minus the
 // nearest integer), then the hardware v_sin_f32 / v_cos_f32, which take their
 // argument in turns.  Absolute error about 1e-6 for |x| in the range the
@@ -81,14 +74,17 @@ __device__ __forceinline__ void fast_sincos(float x, float& s, float& c) {
 template <bool BKM>
 __device__ __forceinline__ void branch_dma(const BranchArgs& a, int row0, int kc, char* st, int wave, int lane) {
     constexpr int ES = 2;
+    // K-major tiles store logical 16-byte chunk c of row q at physical chunk
+    // c ^ swz(q), swz(q) = (q ^ q/8) & 7, so a 16-row pass of ds_read_b128
+    // covers all banks.
     // A: 32 rows, wave w loads rows 8w .. 8w+7 (lane p: row 8w + p/8, physical
-    // chunk p%8 holding logical chunk (p%8) ^ (p/8)).
+    // chunk p%8 holding logical chunk (p%8) ^ (p/8) ^ w).
     {
         const Operand& op = a.A;
         const int64_t ld = op.s[0].ld;
         const int k0 = kc * 64;
         const i32x4 rs = make_desc(op.s[0].ptr + (int64_t)row0 * ld * ES, (int64_t)(op.rows - row0) * ld * ES);
-        const int rr = lane >> 3, c = (lane & 7) ^ rr;
+        const int rr = lane >> 3, c = (lane & 7) ^ rr ^ wave;
         const int k = k0 + c * 8;
         const uint32_t vo = k < op.s[0].klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
         dma16(rs, st + wave * 1024, vo, (uint32_t)((int64_t)8 * wave * ld * ES));
@@ -99,14 +95,16 @@ __device__ __forceinline__ void branch_dma(const BranchArgs& a, int row0, int kc
     const int k0 = kc * 64;
     char* dst = st + kSkA;
     if constexpr (BKM) {
-        // 128 rows (ranks) x 128 B, block b = 4i + w holds rows 8b .. 8b+7
+        // 128 rows (ranks) x 128 B, block b = 4i + w holds rows 8b .. 8b+7;
+        // swz(8b + p/8) = (p/8) ^ (b & 7) = (p/8) ^ w ^ 4(i & 1)
         const i32x4 rs = make_desc(op.s[0].ptr, (int64_t)op.rows * ld * ES);
-        const int rr = lane >> 3, c = (lane & 7) ^ rr;
-        const int k = k0 + c * 8;
-        const uint32_t vo = k < klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
+        const int rr = lane >> 3;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int b = 4 * i + wave;
+            const int c = (lane & 7) ^ rr ^ wave ^ (4 * (i & 1));
+            const int k = k0 + c * 8;
+            const uint32_t vo = k < klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
             dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)8 * b * ld * ES));
         }
     } else {
@@ -162,9 +160,9 @@ __device__ __forceinline__ u32x4 tr_read8(const char* tile, uint32_t base, int s
 
 // Byte offset of element (row, col) of the 32 x 128 bf16 operand tile, laid
 // out K-major as two 64-column chunks of [32 rows][128 B], chunk c of row
-// stored at c ^ (row & 7).
+// stored at c ^ swz(row).
 __device__ __forceinline__ int ctile_off(int row, int col) {
-    return (col >> 6) * 4096 + row * 128 + ((((col >> 3) & 7) ^ (row & 7)) << 4) + (col & 7) * 2;
+    return (col >> 6) * 4096 + row * 128 + ((((col >> 3) & 7) ^ ((row ^ (row >> 3)) & 7)) << 4) + (col & 7) * 2;
 }
 
 // acc (one 32x32 block per wave) over K steps of a [32 x 128] tile in LDS
@@ -179,7 +177,7 @@ __device__ __forceinline__ void mix_mma(const char* ctile, const char* mt, int w
     for (int s = 0; s < 8; ++s) {
         const int q = 2 * s + h;  // 8-element K group of this lane
         const u32x4 av = *reinterpret_cast<const u32x4*>(ctile + (q >> 3) * 4096 + r32 * 128 +
-                                                         ((((q & 7) ^ (r32 & 7))) << 4));
+                                                         ((((q & 7) ^ (r32 & 7) ^ (r32 >> 3))) << 4));
         u32x4 bv;
         if constexpr (!TRANS_M)
             bv = tr_read8(mt, tb, s);
@@ -196,10 +194,10 @@ __device__ __forceinline__ void branch_mainloop(const BranchArgs& a, int row0, c
                                                 f32x16& acc) {
     const int r32 = lane & 31, h = lane >> 5;
     const int nk = a.nk;
-    const uint32_t fa = (uint32_t)(r32 * 128 + ((h ^ (r32 & 7)) << 4));
+    const uint32_t fa = (uint32_t)(r32 * 128 + ((h ^ (r32 & 7) ^ (r32 >> 3)) << 4));
     uint32_t fb;
-    if constexpr (BKM)
-        fb = (uint32_t)((32 * wave + r32) * 128 + ((h ^ (r32 & 7)) << 4));
+    if constexpr (BKM)   // rows 32 wave + r32: swz = (r32 & 7) ^ (r32 >> 3) ^ 4(wave & 1)
+        fb = (uint32_t)((32 * wave + r32) * 128 + ((h ^ (r32 & 7) ^ (r32 >> 3) ^ (4 * (wave & 1))) << 4));
     else
         fb = tr_base(wave, lane);
 #pragma unroll
