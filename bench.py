@@ -18,8 +18,10 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -36,6 +38,36 @@ METRIC = "NOBLE linear fwd+bwd TFLOP/s, % bf16 MFMA peak, overhead vs plain GEMM
 
 def flop_alg(T, d_in, d_out, r):
     return 6.0 * T * (d_in * d_out + r * (d_in + d_out) + r * r)
+
+
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "gemm_fwd_plain_ffn_up_T8192_traffic.md")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2603_06492_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        h.update(f.encode())
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kernel: str, workgroups: int):
+    """HBM bytes per launch of the roofline kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None when that record was taken on
+    other kernel sources or another launch shape."""
+    try:
+        with open(TRAFFIC_RECORD) as fh:
+            m = re.search(r"^traffic_record: (\{.*\})$", fh.read(), re.M)
+        rec = json.loads(m.group(1))
+    except (OSError, AttributeError, ValueError):
+        return None
+    if rec.get("source_sha256_16") != kernel_source_hash():
+        return None
+    if rec.get("workgroups") != workgroups or not kernel.startswith(rec.get("kernel", "?")[5:45]):
+        return None
+    return rec.get("traffic_bytes")
 
 
 def cpu_baseline(workload: str, budget_s: float = 12.0):
@@ -78,6 +110,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--roofline-launches", type=int, default=20,
                     help="timed launches of the plain main GEMM for the roofline entry")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one device-to-device copy of this many MiB (a kernel of known "
+                         "traffic, for scaling FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -179,11 +214,21 @@ def main():
     t_launch = e0.elapsed_time(e1) / args.roofline_launches * 1e-3
     gemm_flops = 2.0 * dom.p.T * dom.p.d_in * dom.p.d_out
     ach = gemm_flops / t_launch / 1e12
+    wgs = -(-dom.p.T // 256) * -(-dom.p.d_out // 256)
+    kname = "noble::gemm_bf16_kernel<true, false, false, 1>"
     roofline = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
-                "frac": round(ach / (PEAK_BF16 / 1e12), 4), "traffic": None,
-                "kernel": f"gemm_kernel x W (plain forward) {dom.p.name.split('/')[-1]} "
-                          f"T={dom.p.T} {dom.p.d_in}->{dom.p.d_out}",
+                "frac": round(ach / (PEAK_BF16 / 1e12), 4), "traffic": recorded_traffic(kname, wgs),
+                "kernel": f"{kname} (plain forward x W, "
+                          f"{dom.p.name.split('/')[-1]} T={dom.p.T} {dom.p.d_in}->{dom.p.d_out}, {wgs} workgroups)",
                 "avg_launch_us": round(t_launch * 1e6, 2), "flop_per_launch": gemm_flops}
+
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20)
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     flops_step = sum(flop_alg(T, di, do, r) for (_, T, di, do, r) in shapes)
     main_flops = sum(6.0 * T * di * do for (_, T, di, do, r) in shapes)

@@ -143,13 +143,19 @@ int choose_split(int tiles, int nk) {
     return s;
 }
 
+// `plain`: the r = 0 forward, launched under its own kernel symbol so that
+// profiles can tell it from the K-extended forward.
 template <typename E, bool AK, bool BKM>
-noble_status launch_gemm(const Batch& bt, hipStream_t st) {
+noble_status launch_gemm(const Batch& bt, hipStream_t st, bool plain = false) {
     if (bt.blocks == 0) return NOBLE_OK;
-    if constexpr (sizeof(E) == 2)
-        hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKM, !AK && !BKM>), dim3(bt.blocks), dim3(kDmaThreads), 0, st,
-                           bt.b);
-    else
+    if constexpr (sizeof(E) == 2) {
+        if (AK && !BKM && plain)
+            hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKM, false, 1>), dim3(bt.blocks), dim3(kDmaThreads), 0, st,
+                               bt.b);
+        else
+            hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKM, !AK && !BKM, 0>), dim3(bt.blocks), dim3(kDmaThreads), 0,
+                               st, bt.b);
+    } else
         hipLaunchKernelGGL((gemm_kernel<E, kBM, kBN, AK, BKM, !AK && !BKM>), dim3(bt.blocks), dim3(kThreads), 0,
                            st, bt.b);
     return last_launch();
@@ -256,7 +262,7 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
     Batch bt;
     bt.add(operand2(seg(x, din, din), seg(C2s, r, r), nk1, T), operand2(seg(W, dout, din), seg(Wu, dout, r), nk1, dout),
            (int)T, (int)dout, nk, y, dout, sizeof(E) == 4, b, nullptr, 1);
-    return launch_gemm<E, true, false>(bt, st);
+    return launch_gemm<E, true, false>(bt, st, r == 0);
 }
 
 template <typename E>

@@ -151,7 +151,9 @@ struct FragAddr {
 
 constexpr int kDmaWM = 2, kDmaWN = 4, kDmaThreads = 64 * kDmaWM * kDmaWN;
 
-template <bool AK, bool BKM, bool HAS_BSUM>
+// TAG only separates launch sites in profiles (1: the plain r = 0 forward);
+// the code is the same.
+template <bool AK, bool BKM, bool HAS_BSUM, int TAG>
 __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch batch) {
     constexpr int BM = 256, BN = 256, NW = kDmaWM * kDmaWN;
     constexpr int WTM = BM / kDmaWM, WTN = BN / kDmaWN;   // wave tile 128 x 64
