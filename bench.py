@@ -116,8 +116,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build's kernels run on a single MI355X and "
-              "have no multi-GPU path (rerun with --gpus 1).", file=sys.stderr)
+        print("bench.py measures one GPU only: the kernels run on a single MI355X and there is "
+              "no multi-GPU path (rerun with --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch

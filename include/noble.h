@@ -78,7 +78,10 @@ typedef struct noble_linear_desc {
  *   reserve_bytes: written by noble_linear_fwd (H = x W_down, float32 [T, r])
  *                  and read by the matching noble_linear_bwd; keep it intact
  *                  in between.  4*T*r bytes.
- *   scratch_bytes: temporary space used within one call (fwd or bwd) only.
+ *   scratch_bytes: temporary space used within one call (fwd or bwd) only;
+ *                  its contents need no initialisation.  The forward uses it
+ *                  only when r > 0; the backward may use it also when r = 0
+ *                  (split-K partial sums of dW), whenever scratch_bytes > 0.
  * Either output pointer may be NULL.  Returns NOBLE_ERR_NULL_ARG (desc NULL),
  * NOBLE_ERR_BAD_SHAPE or NOBLE_ERR_BAD_DTYPE; makes no HIP call. */
 noble_status noble_linear_workspace_size(const noble_linear_desc* desc,
@@ -109,8 +112,11 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc,
  *   dx [T, d_in] (storage dtype), dW [d_in, d_out], db [d_out] (nullable =
  *   not computed), dW_down [d_in, r], dM [r, r], dW_up [r, d_out],
  *   domega1, dphi1, domega2, dphi2 [r]  (all float32).
- * With T = 0 the parameter gradients are set to zero.  Sums over tokens use
- * float atomics, so results may differ in the last bits between runs. */
+ * With T = 0 the parameter gradients are set to zero.  db and the four
+ * omega / phi gradients are summed over tokens with float atomics, so they
+ * may differ in the last bits between runs; the matrix gradients are
+ * reproducible.  scratch (>= scratch_bytes) may be NULL only when
+ * scratch_bytes is 0 or T is 0. */
 noble_status noble_linear_bwd(const noble_linear_desc* desc,
                               const void* dy, const void* x, const void* W,
                               const void* W_down,

@@ -17,12 +17,12 @@ What it computes (the paper, arXiv 2603.06492):
   forward by the chain rule, using d cos(u)/du = -sin(u) (the derivative the
   paper names in §6, "Why Cosine Activations?").
 
-Readings where the paper is silent or ambiguous (each is listed in the design doc):
+Readings where the paper is silent or ambiguous:
 
 * Orientation of M.  Eq. (2) and App. A write ``M h1`` for a column vector.  In
   the row-batch form used here that is ``C1 @ M.T``; this oracle instead uses
-  ``H2 = C1 @ M`` with M stored ``[r_in, r_out]`` (the layer statement this
-  build targets writes ``(cos(...)) M``).  Both parametrise the same function
+  ``H2 = C1 @ M`` with M stored ``[r_in, r_out]``, the ``(cos(...)) M`` form
+  of the row-batch layer statement.  Both parametrise the same function
   class (M.T is just another learned matrix).  A hand-worked example with a
   non-symmetric M (tests/golden/hand_examples.json) pins the choice.
 * No branch scale (Eq. (1) has none; alpha in §3.3 is an init scale only).

@@ -38,10 +38,32 @@ noble_status check_desc(const noble_linear_desc* d) {
 
 size_t elt_size(const noble_linear_desc* d) { return d->dtype == NOBLE_BF16 ? 2 : 4; }
 
-// Scratch layout: four [T, r] storage-type regions, each 256-byte aligned:
-// C1, C2, dH2, dH (the forward uses only C2).
+// Pieces of K for the bf16 rank projection [T, K] x [K, r]: enough
+// workgroups of 128 tokens to cover the CUs, at least kPjMinChunks K chunks
+// per piece, at most kPjMaxSplit pieces.
+int proj_split(int64_t T, int64_t K) {
+    const int64_t blocks = (T + kPjRows - 1) / kPjRows;
+    const int64_t nkc = (K + 63) / 64;
+    int s = 1;
+    while (blocks * s < 256 && 2 * s * kPjMinChunks <= nkc && 2 * s <= kPjMaxSplit) s *= 2;
+    return s;
+}
+
+// Scratch layout, each part 256-byte aligned: four [T, r] storage-type
+// regions C1, C2, dH2, dH (the forward uses only C2); on the bf16 path the
+// float32 projection partials [S][T][r] for the larger split of the forward
+// and backward projections; then the float32 split-K partials of the
+// weight-gradient products (backward only).
 size_t scratch_region(const noble_linear_desc* d) { return align_up((size_t)d->T * d->r * elt_size(d)); }
-size_t scratch_need(const noble_linear_desc* d) { return d->r > 0 ? 4 * scratch_region(d) : 0; }
+size_t partial_need(const noble_linear_desc* d) {
+    if (d->r == 0 || d->dtype != NOBLE_BF16) return 0;
+    const int s = std::max(proj_split(d->T, d->d_in), proj_split(d->T, d->d_out));
+    return align_up((size_t)s * d->T * d->r * 4);
+}
+size_t wgrad_need(const noble_linear_desc* d);
+size_t scratch_need(const noble_linear_desc* d) {
+    return (d->r > 0 ? 4 * scratch_region(d) + partial_need(d) : 0) + wgrad_need(d);
+}
 size_t reserve_need(const noble_linear_desc* d) { return (size_t)d->T * d->r * 4; }
 
 // A required buffer: non-NULL and 16-byte aligned, unless it holds no bytes.
@@ -112,12 +134,15 @@ constexpr int kBM = 256, kBN = 256;
 struct Batch {
     GemmBatch b{};
     int blocks = 0;
+    // split > 1: pieces add atomically into C, or, when `partials` is given,
+    // each stores its float32 partial [M][ldc] at partials + piece * M * ldc.
     void add(const Operand& A, const Operand& B, int M, int N, int nk, void* C, int64_t ldc, bool out_f32,
-             const float* bias, float* bsum, int split) {
+             const float* bias, float* bsum, int split, float* partials = nullptr) {
         GemmProblem& p = b.p[b.count++];
         p.A = A;
         p.B = B;
-        p.C = C;
+        p.C = split > 1 && partials ? partials : C;
+        p.pstride = split > 1 && partials ? (int64_t)M * ldc : 0;
         p.ldc = ldc;
         p.bias = bias;
         p.bsum = bsum;
@@ -130,17 +155,67 @@ struct Batch {
         p.tile_begin = blocks;
         p.nblocks = p.tiles_m * p.tiles_n * split;
         p.out_f32 = out_f32 ? 1 : 0;
-        p.atomic = split > 1 ? 1 : 0;
+        p.atomic = split > 1 && !partials ? 1 : 0;
         blocks += p.nblocks;
     }
 };
 
-// Split-K factor over tokens: enough blocks to give every CU one, while
-// keeping at least eight K chunks per piece.
-int choose_split(int tiles, int nk) {
+// K split of one weight-gradient product (K = T tokens) whose pieces store
+// float32 partials that a reduction sums afterwards.  Cost model: the longest
+// CU's share of 64-element K chunks (waves of 256 workgroups) plus the partial
+// traffic (S writes, S reads, one result write).  A split must beat the
+// unsplit cost by 3%.
+int choose_split_partials(int tiles, int nk, int64_t MN) {
+    constexpr double kChunkUs = 1.7;          // one K chunk of a 256 x 256 tile
+    constexpr double kBytesPerUs = 5.0e6;     // HBM rate of the partials
+    double best = 0;
+    int bs = 1;
+    for (int s = 1; s <= 16; s *= 2) {
+        if (s > 1 && s * 8 > nk) break;
+        const double waves = (double)((int64_t)tiles * s + 255) / 256;
+        const double cost = (int)waves * ((double)nk / s) * kChunkUs + (s > 1 ? (2.0 * s + 1) * MN * 4 / kBytesPerUs : 0);
+        if (s == 1 || cost < best * 0.97) {
+            best = cost;
+            bs = s;
+        }
+    }
+    return bs;
+}
+
+// Split-K factor of the rank-gradient products (dW_down, dW_up, dM), whose
+// pieces add atomically into zeroed outputs of at most a few MB: enough
+// workgroups to give every CU one, at least 8 K chunks per piece.
+int choose_split_atomic(int tiles, int nk) {
     int s = 1;
     while (tiles * s < 256 && s * 2 * 8 <= nk) s *= 2;
     return s;
+}
+
+// Weight-gradient batch plan over K = T: the split of dW (pieces store
+// float32 partials in the scratch, summed by reduce_kernel) and of dW_down,
+// dW_up, dM (atomic).
+struct WgradPlan {
+    int split[4];   // dW, dW_down, dW_up, dM
+    size_t bytes;   // dW partials
+};
+
+WgradPlan plan_wgrad(int64_t T, int64_t din, int64_t dout, int64_t r, int bk) {
+    WgradPlan w{};
+    const int nkT = T > 0 ? cdiv(T, bk) : 0;
+    for (int i = 0; i < 4; ++i) w.split[i] = 1;
+    if (nkT == 0) return w;
+    w.split[0] = choose_split_partials(cdiv(din, kBM) * cdiv(dout, kBN), nkT, din * dout);
+    w.bytes = w.split[0] > 1 ? align_up((size_t)w.split[0] * din * dout * 4) : 0;
+    if (r > 0) {
+        w.split[1] = choose_split_atomic(cdiv(din, kBM), nkT);
+        w.split[2] = choose_split_atomic(cdiv(dout, kBN), nkT);
+        w.split[3] = choose_split_atomic(1, nkT);
+    }
+    return w;
+}
+
+size_t wgrad_need(const noble_linear_desc* d) {
+    return plan_wgrad(d->T, d->d_in, d->d_out, d->r, d->dtype == NOBLE_BF16 ? Elt<uint16_t>::BK : Elt<float>::BK).bytes;
 }
 
 // `plain`: the r = 0 forward, launched under its own kernel symbol so that
@@ -185,11 +260,33 @@ noble_status launch_chain(bool fwd, int RP, const ChainArgs& a, int T, hipStream
     return NOBLE_ERR_BAD_SHAPE;
 }
 
-// bf16 path: fused rank projection + CosNet chain (forward or backward).
-noble_status launch_branch(bool fwd, const ChainArgs& c, hipStream_t st) {
-    BranchArgs a{};
+// bf16 path, step 1: split-K rank projection of c.A against c.B into the
+// float32 partials P [S][T][r] (K = c.nk chunks of 64).
+noble_status launch_proj(bool fwd, const ChainArgs& c, float* P, int S, hipStream_t st) {
+    ProjArgs a{};
     a.A = c.A;
     a.B = c.B;
+    a.P = P;
+    a.pstride = (int64_t)c.T * c.r;
+    a.T = c.T;
+    a.r = c.r;
+    a.nk = c.nk;
+    a.S = S;
+    const dim3 grid(cdiv(c.T, kPjRows) * S), block(kPjThreads);
+    if (fwd)
+        hipLaunchKernelGGL(proj_kernel<false>, grid, block, 0, st, a);
+    else
+        hipLaunchKernelGGL(proj_kernel<true>, grid, block, 0, st, a);
+    return last_launch();
+}
+
+// bf16 path, step 2: CosNet chain (forward or backward) from the summed
+// partials.
+noble_status launch_branch(bool fwd, const ChainArgs& c, const float* P, int S, hipStream_t st) {
+    BranchArgs a{};
+    a.P = P;
+    a.pstride = (int64_t)c.T * c.r;
+    a.S = S;
     a.M = reinterpret_cast<const uint16_t*>(c.M);
     a.w1 = c.w1;
     a.p1 = c.p1;
@@ -206,7 +303,6 @@ noble_status launch_branch(bool fwd, const ChainArgs& c, hipStream_t st) {
     a.dp2 = c.dp2;
     a.T = c.T;
     a.r = c.r;
-    a.nk = c.nk;
     const dim3 grid(cdiv(c.T, kSkRows)), block(kThreads);
     if (fwd)
         hipLaunchKernelGGL(branch_fwd_kernel, grid, block, 0, st, a);
@@ -250,9 +346,12 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
         a.T = (int)T;
         a.r = (int)r;
         a.nk = cdiv(din, BK);
-        if constexpr (sizeof(E) == 2)
-            NOBLE_TRY(launch_branch(true, a, st));
-        else
+        if constexpr (sizeof(E) == 2) {
+            float* P = reinterpret_cast<float*>(static_cast<char*>(scratch) + 4 * scratch_region(d));
+            const int S = proj_split(T, din);
+            NOBLE_TRY(launch_proj(true, a, P, S, st));
+            NOBLE_TRY(launch_branch(true, a, P, S, st));
+        } else
             NOBLE_TRY(launch_chain<E>(true, chain_rp<E>(r), a, (int)T, st));
     }
     // y = [x | C2] [W ; W_up] + b
@@ -279,10 +378,14 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     char* dH2s = base + 2 * reg;
     char* dHs = base + 3 * reg;
 
-    // Plan the weight-gradient batch first: dW needs zeroing only if split.
+    // dW is overwritten by its product (or by the sum of its split-K
+    // partials); db, dW_down, dW_up, dM and the dw / dp vectors are
+    // accumulated atomically and start from zero.  T = 0 zeroes every
+    // gradient.
     constexpr int GBK = gemm_bk<E>();
     const int nkT = cdiv(T, GBK);
-    const int split_dW = T > 0 ? choose_split(cdiv(din, kBM) * cdiv(dout, kBN), nkT) : 1;
+    const WgradPlan wp = plan_wgrad(T, din, dout, r, GBK);
+    float* wpart = reinterpret_cast<float*>(base + (r > 0 ? 4 * reg + partial_need(d) : 0));
 
     ZeroList z{};
     auto zero = [&](float* p, int64_t n) {
@@ -292,7 +395,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             ++z.count;
         }
     };
-    if (T == 0 || split_dW > 1) zero(dW, din * dout);
+    if (T == 0) zero(dW, din * dout);
     zero(db, dout);
     if (r > 0) {
         zero(dWd, din * r);
@@ -330,9 +433,12 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         a.T = (int)T;
         a.r = (int)r;
         a.nk = cdiv(dout, BK);
-        if constexpr (sizeof(E) == 2)
-            NOBLE_TRY(launch_branch(false, a, st));
-        else
+        if constexpr (sizeof(E) == 2) {
+            float* P = reinterpret_cast<float*>(base + 4 * reg);
+            const int S = proj_split(T, dout);
+            NOBLE_TRY(launch_proj(false, a, P, S, st));
+            NOBLE_TRY(launch_branch(false, a, P, S, st));
+        } else
             NOBLE_TRY(launch_chain<E>(false, chain_rp<E>(r), a, (int)T, st));
     }
 
@@ -346,24 +452,34 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         NOBLE_TRY((launch_gemm<E, true, true>(bt, st)));
     }
 
-    // Weight gradients, reduced over tokens (K = T), A and B both MN-major.
+    // Weight gradients, reduced over tokens (K = T), A and B both MN-major; a
+    // split dW stores partials that reduce_kernel then sums into dW.
     {
         Batch bt;
         const Operand xT = operand1(seg(x, din, T), din);
         const Operand dyN = operand1(seg(dy, dout, T), dout);
-        bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, split_dW);
+        bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split[0],
+               wp.split[0] > 1 ? wpart : nullptr);
         if (r > 0) {
             const Operand dHN = operand1(seg(dHs, r, T), r);
             const Operand C2T = operand1(seg(C2s, r, T), r);
             const Operand C1T = operand1(seg(C1s, r, T), r);
             const Operand dH2N = operand1(seg(dH2s, r, T), r);
-            bt.add(xT, dHN, (int)din, (int)r, nkT, dWd, r, true, nullptr, nullptr,
-                   choose_split(cdiv(din, kBM), nkT));
-            bt.add(C2T, dyN, (int)r, (int)dout, nkT, dWu, dout, true, nullptr, nullptr,
-                   choose_split(cdiv(dout, kBN), nkT));
-            bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM, r, true, nullptr, nullptr, choose_split(1, nkT));
+            bt.add(xT, dHN, (int)din, (int)r, nkT, dWd, r, true, nullptr, nullptr, wp.split[1]);
+            bt.add(C2T, dyN, (int)r, (int)dout, nkT, dWu, dout, true, nullptr, nullptr, wp.split[2]);
+            bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM, r, true, nullptr, nullptr, wp.split[3]);
         }
         NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
+        if (wp.split[0] > 1) {
+            ReduceList red{};
+            red.part[0] = wpart;
+            red.out[0] = dW;
+            red.n[0] = din * dout;
+            red.S[0] = wp.split[0];
+            red.count = 1;
+            hipLaunchKernelGGL(reduce_kernel, dim3(1024), dim3(256), 0, st, red);
+            NOBLE_TRY(last_launch());
+        }
     }
     return NOBLE_OK;
 }
@@ -456,8 +572,10 @@ noble_status noble_linear_bwd(const noble_linear_desc* desc, const void* dy, con
         NOBLE_TRY(need(dphi1, true));
         NOBLE_TRY(need(domega2, true));
         NOBLE_TRY(need(dphi2, true));
+    }
+    if (scratch_need(desc) > 0) {
         NOBLE_TRY(need(scratch, rows));
-        if (scratch_bytes < scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
+        if (rows && scratch_bytes < scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
     }
     NOBLE_TRY(check_device());
     hipStream_t st = static_cast<hipStream_t>(stream);

@@ -38,12 +38,15 @@ struct GemmProblem {
     float* bsum;        // column sums of B over K, atomically added (nullable)
     int M, N;
     int nk;             // K chunks (both segments)
-    int split;          // K pieces; pieces accumulate atomically if > 1
+    int split;          // K pieces: with atomic, added into C; else piece p
+                        // stores its partial at C + p * pstride elements
     int tiles_m, tiles_n;
     int tile_begin;     // first block index of this problem
     int nblocks;        // tiles_m * tiles_n * split
     int out_f32;        // C holds float (1) or the storage type (0)
     int atomic;         // atomicAdd into a zeroed float C
+    int pad_;
+    int64_t pstride;    // elements between the partials of consecutive pieces
 };
 
 constexpr int kMaxProblems = 4;
@@ -215,7 +218,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmBatch batch) {
     const bool add_bias = (P.bias != nullptr) && piece == 0;
     const int es = P.out_f32 ? 4 : (int)sizeof(E);
     const __amdgpu_buffer_rsrc_t rc =
-        make_rsrc(static_cast<const char*>(P.C) + (int64_t)m0 * P.ldc * es, (int64_t)(P.M - m0) * P.ldc * es);
+        make_rsrc(static_cast<const char*>(P.C) + (piece * P.pstride + (int64_t)m0 * P.ldc) * es,
+                  (int64_t)(P.M - m0) * P.ldc * es);
     uint32_t voff[TM][TN];
     float bcol[TN];
 #pragma unroll

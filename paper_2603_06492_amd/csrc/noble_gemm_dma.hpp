@@ -208,19 +208,22 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
     if (kc0 < kc1) {
         const FragAddr<AK, TM> fa(wm0, lane);
         const FragAddr<BKM, TN> fb(wn0, lane);
-        dma_tile<AK, NW>(P.A, m0, kc0, lds0, wave, lane);
-        dma_tile<BKM, NW>(P.B, n0, kc0, lds0 + TILE, wave, lane);
+        // Local copies of the operand descriptions: read once from the kernel
+        // arguments instead of once per chunk.
+        const Operand opA = P.A, opB = P.B;
+        dma_tile<AK, NW>(opA, m0, kc0, lds0, wave, lane);
+        dma_tile<BKM, NW>(opB, n0, kc0, lds0 + TILE, wave, lane);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
 
         // Multiply chunk kc from `cur` while chunk kc + 1 streams into `nxt`.
-        auto chunk = [&](int kc, const char* cur, char* nxt, auto bs_c) {
+        auto chunk = [&](int kc, const char* cur, char* nxt, auto bs_c) __attribute__((always_inline)) {
             constexpr bool BS = decltype(bs_c)::value;
             const char* ldsA = cur;
             const char* ldsB = cur + TILE;
             if (kc + 1 < kc1) {
-                dma_tile<AK, NW>(P.A, m0, kc + 1, nxt, wave, lane);
-                dma_tile<BKM, NW>(P.B, n0, kc + 1, nxt + TILE, wave, lane);
+                dma_tile<AK, NW>(opA, m0, kc + 1, nxt, wave, lane);
+                dma_tile<BKM, NW>(opB, n0, kc + 1, nxt + TILE, wave, lane);
             }
             // Fragments of K step s + 1 are read while the MFMAs of step s run:
             // one LDS read issued per MFMA (schedule pinned below).
@@ -262,7 +265,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             __syncthreads();
         };
-        auto run = [&](auto bs_c) {
+        auto run = [&](auto bs_c) __attribute__((always_inline)) {
             int kc = kc0;
             for (; kc + 1 < kc1; kc += 2) {
                 chunk(kc, lds0, lds1, bs_c);
@@ -294,7 +297,8 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
     const bool add_bias = (P.bias != nullptr) && piece == 0;
     const int es = P.out_f32 ? 4 : 2;
     const __amdgpu_buffer_rsrc_t rc =
-        make_rsrc(static_cast<const char*>(P.C) + (int64_t)m0 * P.ldc * es, (int64_t)(P.M - m0) * P.ldc * es);
+        make_rsrc(static_cast<const char*>(P.C) + (piece * P.pstride + (int64_t)m0 * P.ldc) * es,
+                  (int64_t)(P.M - m0) * P.ldc * es);
     uint32_t voff[TM][TN];
     float bcol[TN];
 #pragma unroll

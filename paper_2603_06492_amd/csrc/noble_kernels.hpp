@@ -47,6 +47,38 @@ __global__ __launch_bounds__(256) void zero_kernel(ZeroList z) {
     }
 }
 
+// Split-K partial sums: out[i] = sum over p < S of part[p * n + i], for up to
+// kMaxZero float arrays.
+struct ReduceList {
+    const float* part[kMaxZero];
+    float* out[kMaxZero];
+    int64_t n[kMaxZero];
+    int S[kMaxZero];
+    int count;
+};
+
+__global__ __launch_bounds__(256) void reduce_kernel(ReduceList z) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int s = 0; s < z.count; ++s) {
+        const float* p = z.part[s];
+        float* o = z.out[s];
+        const int64_t n = z.n[s];
+        const int S = z.S[s];
+        const int64_t n4 = n >> 2;
+        for (int64_t i = gid; i < n4; i += stride) {
+            f32x4 acc = reinterpret_cast<const f32x4*>(p)[i];
+            for (int q = 1; q < S; ++q) acc += reinterpret_cast<const f32x4*>(p + q * n)[i];
+            reinterpret_cast<f32x4*>(o)[i] = acc;
+        }
+        for (int64_t i = (n4 << 2) + gid; i < n; i += stride) {
+            float acc = p[i];
+            for (int q = 1; q < S; ++q) acc += p[q * n + i];
+            o[i] = acc;
+        }
+    }
+}
+
 // ------------------------------------------------------------- chain kernels --
 
 struct ChainArgs {

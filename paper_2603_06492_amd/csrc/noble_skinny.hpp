@@ -1,22 +1,27 @@
-// The rank-r side of the layer, bf16 path, as two fused kernels on gfx950:
+// The rank-r side of the layer, bf16 path, on gfx950, in two steps:
 //
-//   branch_fwd_kernel:  H = x W_down (MFMA), then per token the CosNet chain
-//                       C1 = cos(H w1 + p1), H2 = C1 M (MFMA), C2 = cos(H2 w2 + p2).
-//                       Writes H (float32, the reserve) and C2 (bf16, scratch).
-//   branch_bwd_kernel:  dC2 = dy W_up^T (MFMA), then the chain backwards from
-//                       the saved H: C1, sin A1, H2 = C1 M, C2, sin A2,
+//   proj_kernel:        the rank projection, H = x W_down (forward) or
+//                       dC2 = dy W_up^T (backward), as a split-K MFMA product:
+//                       a workgroup owns 128 tokens x all 128 (padded) ranks
+//                       and one of S pieces of K, and writes its float32
+//                       partial sum to scratch.  Streaming 128 tokens against
+//                       the rank operand (instead of 32) cuts the L2 traffic of
+//                       that operand four-fold; the K split keeps every CU busy.
+//   branch_fwd_kernel:  per token, H = the sum of the S partials, then the
+//                       CosNet chain C1 = cos(H w1 + p1), H2 = C1 M (MFMA),
+//                       C2 = cos(H2 w2 + p2).  Writes H (float32, the reserve)
+//                       and C2 (bf16, scratch).
+//   branch_bwd_kernel:  dC2 = the sum of the partials, then the chain backwards
+//                       from the saved H: C1, sin A1, H2 = C1 M, C2, sin A2,
 //                       dA2 = -sin(A2) dC2, dH2 = dA2 w2, dC1 = dH2 M^T (MFMA),
 //                       dA1 = -sin(A1) dC1, dH = dA1 w1.  Writes C1, C2, dH2, dH
 //                       (bf16 scratch, operands of the weight-gradient products)
 //                       and reduces dw1, dp1, dw2, dp2 over its tokens with wave
 //                       shuffles, then one float atomic per column.
 //
-// Both stream a [T, K] bf16 operand once (x or dy) against a rank operand that
-// stays in L2, so the main loop is built for bytes in flight: 32 tokens x 128
-// ranks per workgroup, a five-stage LDS ring filled by buffer_load ... lds.
-// Four waves each own 32 of the 128 rank columns (one 32x32x16 MFMA per K
-// step).  M [r, r] is loaded into LDS once per workgroup, at the start, in its
-// HBM layout [r_in][r_out]; C1 M reads it with ds_read_b64_tr_b16 and
+// The chain kernels run 32 tokens x 128 ranks per workgroup, four waves each
+// owning 32 rank columns.  M [r, r] is loaded into LDS once per workgroup in
+// its HBM layout [r_in][r_out]; C1 M reads it with ds_read_b64_tr_b16 and
 // dH2 M^T with ds_read_b128.
 #pragma once
 
@@ -24,20 +29,33 @@
 
 namespace noble {
 
-constexpr int kSkRows = 32;     // tokens per workgroup
+constexpr int kSkRows = 32;     // tokens per chain workgroup
 constexpr int kSkN = 128;       // padded rank columns
-constexpr int kSkStages = 5;
-constexpr int kSkA = kSkRows * 128;       // A bytes per stage (32 rows x 128 B)
-constexpr int kSkB = kSkN * 128;          // B bytes per stage (16 KB either layout)
-constexpr int kSkStage = kSkA + kSkB;
 constexpr int kSkM = kSkN * kSkN * 2;     // M tile, 128 x 128 bf16
 constexpr int kSkC = kSkRows * kSkN * 2;  // C1 / dH2 operand tile, 32 x 128 bf16
-constexpr int kSkLds = kSkStages * kSkStage + kSkM + kSkC;
-constexpr int kSkLoads = 5;               // DMA instructions per wave per K chunk
+constexpr int kSkLds = kSkM + kSkC;
+
+constexpr int kPjRows = 128;                 // tokens per projection workgroup
+constexpr int kPjThreads = 512;              // eight waves: 4 token blocks x 2 rank halves
+constexpr int kPjStages = 4;                 // LDS ring depth
+constexpr int kPjA = kPjRows * 128;          // A bytes per stage (128 rows x 64 K)
+constexpr int kPjB = kSkN * 128;             // B bytes per stage (16 KB either layout)
+constexpr int kPjStage = kPjA + kPjB;
+constexpr int kPjLoads = 4;                  // DMA instructions per wave per K chunk
+constexpr int kPjMinChunks = 4;              // 64-element K chunks per piece, at least
+constexpr int kPjMaxSplit = 8;
+
+struct ProjArgs {
+    Operand A;          // [T, K] K-major: x (forward) or dy (backward)
+    Operand B;          // W_down [K, r] MN-major (forward) or W_up [r, K] K-major (backward)
+    float* P;           // partials [S][T][r] float32
+    int64_t pstride;    // T * r
+    int T, r, nk, S;    // nk: 64-element K chunks
+};
 
 struct BranchArgs {
-    Operand A;            // [T, K] K-major: x (forward) or dy (backward)
-    Operand B;            // W_down [K, r] MN-major (forward) or W_up [r, K] K-major (backward)
+    const float* P;       // projection partials [S][T][r]
+    int64_t pstride;
     const uint16_t* M;    // [r, r]
     const float* w1;
     const float* p1;
@@ -52,7 +70,7 @@ struct BranchArgs {
     float* dp1;
     float* dw2;
     float* dp2;
-    int T, r, nk, pad_;
+    int T, r, S, pad_;
 };
 
 // sin and cos of x: reduction to one period in turns (x / 2 pi minus the
@@ -70,54 +88,46 @@ __device__ __forceinline__ void fast_sincos(float x, float& s, float& c) {
     c = __builtin_amdgcn_cosf(t);
 }
 
-// One K chunk of the rank projection: 5 DMA instructions per wave.
+// One 64-element K chunk of the projection operands: 4 DMA instructions per
+// wave (two for A, two for B).
 template <bool BKM>
-__device__ __forceinline__ void branch_dma(const BranchArgs& a, int row0, int kc, char* st, int wave, int lane) {
+__device__ __forceinline__ void proj_dma(const ProjArgs& a, int row0, int kc, char* st, int wave, int lane) {
     constexpr int ES = 2;
+    const int k0 = kc * 64;
     // K-major tiles store logical 16-byte chunk c of row q at physical chunk
     // c ^ swz(q), swz(q) = (q ^ q/8) & 7, so a 16-row pass of ds_read_b128
-    // covers all banks.
-    // A: 32 rows, wave w loads rows 8w .. 8w+7 (lane p: row 8w + p/8, physical
-    // chunk p%8 holding logical chunk (p%8) ^ (p/8) ^ w).
-    {
-        const Operand& op = a.A;
+    // covers all banks.  128 rows x 128 B: block b = 8i + w holds rows
+    // 8b .. 8b+7; lane p -> row 8b + p/8, and swz = (p/8) ^ w.
+    auto kmajor = [&](const Operand& op, int64_t row_base, char* dst) {
         const int64_t ld = op.s[0].ld;
-        const int k0 = kc * 64;
-        const i32x4 rs = make_desc(op.s[0].ptr + (int64_t)row0 * ld * ES, (int64_t)(op.rows - row0) * ld * ES);
+        const i32x4 rs = make_desc(op.s[0].ptr + row_base * ld * ES, (int64_t)(op.rows - row_base) * ld * ES);
         const int rr = lane >> 3, c = (lane & 7) ^ rr ^ wave;
         const int k = k0 + c * 8;
         const uint32_t vo = k < op.s[0].klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
-        dma16(rs, st + wave * 1024, vo, (uint32_t)((int64_t)8 * wave * ld * ES));
-    }
-    const Operand& op = a.B;
-    const int64_t ld = op.s[0].ld;
-    const int klen = op.s[0].klen;
-    const int k0 = kc * 64;
-    char* dst = st + kSkA;
-    if constexpr (BKM) {
-        // 128 rows (ranks) x 128 B, block b = 4i + w holds rows 8b .. 8b+7;
-        // swz(8b + p/8) = (p/8) ^ (b & 7) = (p/8) ^ w ^ 4(i & 1)
-        const i32x4 rs = make_desc(op.s[0].ptr, (int64_t)op.rows * ld * ES);
-        const int rr = lane >> 3;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int b = 4 * i + wave;
-            const int c = (lane & 7) ^ rr ^ wave ^ (4 * (i & 1));
-            const int k = k0 + c * 8;
-            const uint32_t vo = k < klen ? (uint32_t)(((int64_t)rr * ld + k) * ES) : kOOB;
+        for (int i = 0; i < 2; ++i) {
+            const int b = 8 * i + wave;
             dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)8 * b * ld * ES));
         }
+    };
+    kmajor(a.A, row0, st);
+    char* dst = st + kPjA;
+    if constexpr (BKM) {
+        kmajor(a.B, 0, dst);
     } else {
-        // 64 k-rows x 256 B, block b = 4i + w holds k-rows 4b .. 4b+3; lane p ->
+        // 64 k-rows x 256 B, block b = 8i + w holds k-rows 4b .. 4b+3; lane p ->
         // k-row 4b + p/16, physical segment p%16 holding logical (p%16) ^ 4(p/16)
+        const Operand& op = a.B;
+        const int64_t ld = op.s[0].ld;
+        const int klen = op.s[0].klen;
         const i32x4 rs = make_desc(op.s[0].ptr + (int64_t)k0 * ld * ES, (int64_t)(klen - k0) * ld * ES);
         const int kq = lane >> 4;
         const int seg = (lane & 15) ^ (4 * kq);
         const int col = 8 * seg;
         const uint32_t vo = col < op.rows ? (uint32_t)(((int64_t)kq * ld + col) * ES) : kOOB;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int b = 4 * i + wave;
+        for (int i = 0; i < 2; ++i) {
+            const int b = 8 * i + wave;
             dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)4 * b * ld * ES));
         }
     }
@@ -187,51 +197,102 @@ __device__ __forceinline__ void mix_mma(const char* ctile, const char* mt, int w
     }
 }
 
-// Main loop of the rank projection: acc (rows 8(v/4) + 4(l/32) + v%4, rank
-// column 32 wave + l%32) = A rows [row0, row0 + 32) times B over all K.
+// Split-K rank projection.  Workgroup g: token block g % blocks, K piece
+// g / blocks.  Wave w owns rows 32 (w / 2) .. +31 and rank columns
+// 64 (w % 2) .. +63 of the 128 x 128 tile (two 32x32x16 MFMAs per K step).
 template <bool BKM>
-__device__ __forceinline__ void branch_mainloop(const BranchArgs& a, int row0, char* lds, int wave, int lane,
-                                                f32x16& acc) {
+__global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
+    __shared__ __attribute__((aligned(1024))) char lds[kPjStages * kPjStage];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
-    const int nk = a.nk;
-    const uint32_t fa = (uint32_t)(r32 * 128 + ((h ^ (r32 & 7) ^ (r32 >> 3)) << 4));
-    uint32_t fb;
-    if constexpr (BKM)   // rows 32 wave + r32: swz = (r32 & 7) ^ (r32 >> 3) ^ 4(wave & 1)
-        fb = (uint32_t)((32 * wave + r32) * 128 + ((h ^ (r32 & 7) ^ (r32 >> 3) ^ (4 * (wave & 1))) << 4));
-    else
-        fb = tr_base(wave, lane);
+    const int blocks = (a.T + kPjRows - 1) / kPjRows;
+    const int piece = blockIdx.x / blocks;
+    const int row0 = (blockIdx.x - piece * blocks) * kPjRows;
+    const int kc0 = (int)((int64_t)a.nk * piece / a.S), kc1 = (int)((int64_t)a.nk * (piece + 1) / a.S);
+    const int wr = wave >> 1, wc = wave & 1;
+
+    // A rows 32 wr + r32: swz = (r32 & 7) ^ (r32 >> 3) ^ 4(wr & 1)
+    const uint32_t fa = (uint32_t)((32 * wr + r32) * 128 + ((h ^ (r32 & 7) ^ (r32 >> 3) ^ (4 * (wr & 1))) << 4));
+    uint32_t fb[2];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+    for (int j = 0; j < 2; ++j) {
+        if constexpr (BKM)   // W_up rows 64 wc + 32 j + r32: swz = (r32 & 7) ^ (r32 >> 3) ^ 4(j & 1)
+            fb[j] = (uint32_t)((64 * wc + 32 * j + r32) * 128 + ((h ^ (r32 & 7) ^ (r32 >> 3) ^ (4 * (j & 1))) << 4));
+        else
+            fb[j] = tr_base(2 * wc + j, lane);
+    }
+    f32x16 acc[2];
 #pragma unroll
-    for (int c = 0; c < kSkStages - 1; ++c)
-        if (c < nk) branch_dma<BKM>(a, row0, c, lds + c * kSkStage, wave, lane);
-    for (int kc = 0; kc < nk; ++kc) {
-        // chunk kc has landed once at most (stages - 2) later chunks are in flight
-        const int ahead = min(nk - 1 - kc, kSkStages - 2);
-        if (ahead >= 3)
-            wait_vmcnt<3 * kSkLoads>();
-        else if (ahead == 2)
-            wait_vmcnt<2 * kSkLoads>();
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+
+    const int n = kc1 - kc0;
+#pragma unroll
+    for (int c = 0; c < kPjStages - 1; ++c)
+        if (c < n) proj_dma<BKM>(a, row0, kc0 + c, lds + c * kPjStage, wave, lane);
+    for (int i = 0; i < n; ++i) {
+        // chunk i has landed once at most (stages - 2) later chunks are in flight
+        const int ahead = min(n - 1 - i, kPjStages - 2);
+        if (ahead >= 2)
+            wait_vmcnt<2 * kPjLoads>();
         else if (ahead == 1)
-            wait_vmcnt<kSkLoads>();
+            wait_vmcnt<kPjLoads>();
         else
             wait_vmcnt<0>();
         __syncthreads();
-        if (kc + kSkStages - 1 < nk)
-            branch_dma<BKM>(a, row0, kc + kSkStages - 1, lds + ((kc + kSkStages - 1) % kSkStages) * kSkStage, wave,
-                            lane);
-        const char* st = lds + (kc % kSkStages) * kSkStage;
-        const char* sb = st + kSkA;
+        if (i + kPjStages - 1 < n)
+            proj_dma<BKM>(a, row0, kc0 + i + kPjStages - 1, lds + ((i + kPjStages - 1) % kPjStages) * kPjStage,
+                          wave, lane);
+        const char* st = lds + (i % kPjStages) * kPjStage;
+        const char* sb = st + kPjA;
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
             const u32x4 av = *reinterpret_cast<const u32x4*>(st + (fa ^ ((uint32_t)s << 5)));
-            u32x4 bv;
-            if constexpr (BKM)
-                bv = *reinterpret_cast<const u32x4*>(sb + (fb ^ ((uint32_t)s << 5)));
-            else
-                bv = tr_read8(sb, fb, s);
-            mma32<uint16_t>(acc, av, bv);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                u32x4 bv;
+                if constexpr (BKM)
+                    bv = *reinterpret_cast<const u32x4*>(sb + (fb[j] ^ ((uint32_t)s << 5)));
+                else
+                    bv = tr_read8(sb, fb[j], s);
+                mma32<uint16_t>(acc[j], av, bv);
+            }
         }
+    }
+
+    // acc[j][v]: row 32 wr + 8(v/4) + 4h + v%4, column 64 wc + 32 j + r32;
+    // rows past T and columns past r are dropped by the buffer range check
+    const int r = a.r;
+    const __amdgpu_buffer_rsrc_t rp =
+        make_rsrc(reinterpret_cast<const char*>(a.P + piece * a.pstride) + (int64_t)row0 * r * 4,
+                  (int64_t)(a.T - row0) * r * 4);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int col = 64 * wc + 32 * j + r32;
+        const uint32_t vo = col < r ? (uint32_t)(((32 * wr + 4 * h) * r + col) * 4) : kOOB;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[j][v]), rp, vo,
+                                                  (uint32_t)((8 * (v >> 2) + (v & 3)) * r * 4), 0);
+    }
+}
+
+// acc[v] = sum over the S partials of token row0 + 8(v/4) + 4h + v%4, rank
+// column col (zero past T or r).
+__device__ __forceinline__ void sum_partials(const BranchArgs& a, int row0, int col, int h, f32x16& acc) {
+    const int r = a.r;
+    const uint32_t vo = col < r ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+    for (int s = 0; s < a.S; ++s) {
+        const __amdgpu_buffer_rsrc_t rp =
+            make_rsrc(reinterpret_cast<const char*>(a.P + s * a.pstride) + (int64_t)row0 * r * 4,
+                      (int64_t)(a.T - row0) * r * 4);
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            acc[v] += __uint_as_float(
+                __builtin_amdgcn_raw_buffer_load_b32(rp, vo, (uint32_t)((8 * (v >> 2) + (v & 3)) * r * 4), 0));
     }
 }
 
@@ -246,19 +307,19 @@ __device__ __forceinline__ float block_colsum(const float (&x)[16]) {
 
 __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds[kSkLds];
-    char* mt = lds + kSkStages * kSkStage;
+    char* mt = lds;
     char* ct = mt + kSkM;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
     const int row0 = blockIdx.x * kSkRows;
     const int r = a.r;
 
-    m_dma(a.M, r, mt, wave, lane);   // lands while the projection streams
-    f32x16 acc;
-    branch_mainloop<false>(a, row0, lds, wave, lane, acc);
-
+    m_dma(a.M, r, mt, wave, lane);   // lands while the partials are summed
     // acc[v]: token row0 + 8(v/4) + 4h + v%4, rank column 32 wave + r32
     const int col = 32 * wave + r32;
+    f32x16 acc;
+    sum_partials(a, row0, col, h, acc);
+
     const bool cv = col < r;
     const float w1 = cv ? a.w1[col] : 0.f, p1 = cv ? a.p1[col] : 0.f;
     const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
@@ -276,7 +337,8 @@ __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
         const float c1 = cv ? fast_cos(acc[v] * w1 + p1) : 0.f;
         *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = (uint16_t)f2bf(c1);
     }
-    __syncthreads();   // C1 tile complete; M landed (the main loop drained vmcnt)
+    wait_vmcnt<0>();   // this wave's part of M has landed
+    __syncthreads();   // C1 tile and M complete
 
     f32x16 h2;
 #pragma unroll
@@ -290,7 +352,7 @@ __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
 
 __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds[kSkLds];
-    char* mt = lds + kSkStages * kSkStage;
+    char* mt = lds;
     char* ct = mt + kSkM;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
@@ -298,10 +360,10 @@ __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
     const int r = a.r;
 
     m_dma(a.M, r, mt, wave, lane);
-    f32x16 dc2;
-    branch_mainloop<true>(a, row0, lds, wave, lane, dc2);   // dC2 = dy W_up^T
-
     const int col = 32 * wave + r32;
+    f32x16 dc2;
+    sum_partials(a, row0, col, h, dc2);   // dC2 = dy W_up^T
+
     const bool cv = col < r;
     const float w1 = cv ? a.w1[col] : 0.f, p1 = cv ? a.p1[col] : 0.f;
     const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
@@ -331,7 +393,8 @@ __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
         *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = c1;
         __builtin_amdgcn_raw_buffer_store_b16(c1, rc1, vo2, soff(v, 2), 0);
     }
-    __syncthreads();
+    wait_vmcnt<0>();   // this wave's part of M has landed
+    __syncthreads();   // C1 tile and M complete
 
     f32x16 h2;
 #pragma unroll

@@ -50,19 +50,75 @@ def _ws(T, di, do, r, dt):
     return st, a.value, b.value
 
 
+def _proj_split(T, K):
+    """K pieces of the bf16 rank projection: workgroups of 128 tokens until
+    256 are in flight, at least 4 chunks of 64 per piece, at most 8 pieces."""
+    blocks, nkc, s = -(-T // 128), -(-K // 64), 1
+    while blocks * s < 256 and 2 * s * 4 <= nkc and 2 * s <= 8:
+        s *= 2
+    return s
+
+
+def _align(n):
+    return -(-n // 256) * 256
+
+
+def _split_partials(tiles, nk, mn):
+    """K split of one weight-gradient product: waves of 256 workgroups x K
+    chunks of 64 (1.7 us each) plus (2S + 1) passes over the float32
+    partials at 5 TB/s; a split must beat the best so far by 3%."""
+    best, bs, s = 0.0, 1, 1
+    while s <= 16:
+        if s > 1 and s * 8 > nk:
+            break
+        waves = -(-(tiles * s) // 256)
+        cost = waves * (nk / s) * 1.7 + ((2.0 * s + 1) * mn * 4 / 5.0e6 if s > 1 else 0.0)
+        if s == 1 or cost < best * 0.97:
+            best, bs = cost, s
+        s *= 2
+    return bs
+
+
+def _wgrad_bytes(T, di, do, r, bk):
+    """dW partials: only dW stores partials (the rank gradients add
+    atomically)."""
+    nk = -(-T // bk) if T > 0 else 0
+    if nk == 0:
+        return 0
+    sp = _split_partials(-(-di // 256) * -(-do // 256), nk, di * do)
+    return _align(sp * di * do * 4) if sp > 1 else 0
+
+
 def test_workspace_sizes():
-    # four storage-type [T, r] regions
+    # four storage-type [T, r] regions, then (bf16) the float32 projection
+    # partials of the larger of the forward and backward splits, then the
+    # float32 split-K partials of the weight-gradient products
     st, res, scr = _ws(8192, 2048, 2048, 128, noble.NOBLE_BF16)
-    assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2
+    assert _proj_split(8192, 2048) == 4
+    # square 2048 projection: dW in 4 pieces
+    wg = 4 * 2048 * 2048 * 4
+    assert _wgrad_bytes(8192, 2048, 2048, 128, 64) == wg
+    assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + wg
+    st, res, scr = _ws(8192, 2048, 8192, 128, noble.NOBLE_BF16)
+    assert st == OK and scr == 4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + _wgrad_bytes(8192, 2048, 8192, 128, 64)
+    st, res, scr = _ws(300, 64, 1024, 40, noble.NOBLE_BF16)
+    S = max(_proj_split(300, 64), _proj_split(300, 1024))
+    assert _wgrad_bytes(300, 64, 1024, 40, 64) == 0   # 5 K chunks: no split
+    assert S == 4 and st == OK and scr == 4 * _align(300 * 40 * 2) + _align(S * 300 * 40 * 4)
     st, res, scr = _ws(256, 64, 64, 8, noble.NOBLE_F32)
     assert st == OK and res == 4 * 256 * 8 and scr == 4 * 256 * 8 * 4
     st, res, scr = _ws(1000, 64, 64, 0, noble.NOBLE_BF16)
+    assert st == OK and res == 0 and scr == _wgrad_bytes(1000, 64, 64, 0, 64) == 2 * 64 * 64 * 4
+    st, res, scr = _ws(200, 64, 64, 0, noble.NOBLE_BF16)
     assert st == OK and res == 0 and scr == 0
+    # a plain layer still needs the dW partials when it splits
+    st, res, scr = _ws(8192, 2048, 2048, 0, noble.NOBLE_BF16)
+    assert st == OK and res == 0 and scr == 4 * 2048 * 2048 * 4
     st, res, scr = _ws(0, 64, 64, 32, noble.NOBLE_BF16)
     assert st == OK and res == 0
     # each region of the scratch is 256-byte aligned
     st, res, scr = _ws(3, 64, 64, 8, noble.NOBLE_BF16)
-    assert st == OK and scr == 4 * 256
+    assert st == OK and scr == 4 * 256 + 256
     assert noble.lib().noble_linear_workspace_size(None, None, None) == NULL
 
 
@@ -144,3 +200,20 @@ def test_plain_linear_branch_pointers_unchecked():
         ptrs[FWD_ARGS.index(k)] = None
     ptrs[0] = None
     assert _fwd(d, ptrs, 0) == NULL
+
+
+def test_plain_backward_needs_scratch_when_dW_splits():
+    """r = 0 with 1000 tokens splits dW over K, so the backward needs the
+    partials scratch even without a branch: NULL or short scratch is rejected
+    before any HIP call."""
+    d = noble.make_desc(1000, 64, 64, 0, noble.NOBLE_BF16)
+    _, scr = noble.noble_linear_workspace_size(1000, 64, 64, 0, noble.NOBLE_BF16)
+    assert scr > 0
+    ptrs = list(FAKE[:22])
+    for k in ("W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up", "reserve", "dW_down", "dM", "dW_up",
+              "domega1", "dphi1", "domega2", "dphi2"):
+        ptrs[BWD_ARGS.index(k)] = None
+    ptrs[BWD_ARGS.index("scratch")] = None
+    assert _bwd(d, ptrs, scr) == NULL
+    ptrs[BWD_ARGS.index("scratch")] = FAKE[21]
+    assert _bwd(d, ptrs, scr - 256) == WS
