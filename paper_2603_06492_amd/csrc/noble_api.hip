@@ -191,31 +191,24 @@ int choose_split_atomic(int tiles, int nk) {
     return s;
 }
 
-// Weight-gradient batch plan over K = T: the split of dW (pieces store
-// float32 partials in the scratch, summed by reduce_kernel) and of dW_down,
-// dW_up, dM (atomic).
+// Split of dW over K = T: its pieces store float32 partials in the scratch
+// that reduce_kernel sums.
 struct WgradPlan {
-    int split[4];   // dW, dW_down, dW_up, dM
+    int split;      // K pieces of dW
     size_t bytes;   // dW partials
 };
 
-WgradPlan plan_wgrad(int64_t T, int64_t din, int64_t dout, int64_t r, int bk) {
-    WgradPlan w{};
+WgradPlan plan_wgrad(int64_t T, int64_t din, int64_t dout, int bk) {
+    WgradPlan w{1, 0};
     const int nkT = T > 0 ? cdiv(T, bk) : 0;
-    for (int i = 0; i < 4; ++i) w.split[i] = 1;
     if (nkT == 0) return w;
-    w.split[0] = choose_split_partials(cdiv(din, kBM) * cdiv(dout, kBN), nkT, din * dout);
-    w.bytes = w.split[0] > 1 ? align_up((size_t)w.split[0] * din * dout * 4) : 0;
-    if (r > 0) {
-        w.split[1] = choose_split_atomic(cdiv(din, kBM), nkT);
-        w.split[2] = choose_split_atomic(cdiv(dout, kBN), nkT);
-        w.split[3] = choose_split_atomic(1, nkT);
-    }
+    w.split = choose_split_partials(cdiv(din, kBM) * cdiv(dout, kBN), nkT, din * dout);
+    w.bytes = w.split > 1 ? align_up((size_t)w.split * din * dout * 4) : 0;
     return w;
 }
 
 size_t wgrad_need(const noble_linear_desc* d) {
-    return plan_wgrad(d->T, d->d_in, d->d_out, d->r, d->dtype == NOBLE_BF16 ? Elt<uint16_t>::BK : Elt<float>::BK).bytes;
+    return plan_wgrad(d->T, d->d_in, d->d_out, d->dtype == NOBLE_BF16 ? Elt<uint16_t>::BK : Elt<float>::BK).bytes;
 }
 
 // `plain`: the r = 0 forward, launched under its own kernel symbol so that
@@ -262,8 +255,10 @@ noble_status launch_chain(bool fwd, int RP, const ChainArgs& a, int T, hipStream
 
 // bf16 path, step 1: split-K rank projection of c.A against c.B into the
 // float32 partials P [S][T][r] (K = c.nk chunks of 64).
-noble_status launch_proj(bool fwd, const ChainArgs& c, float* P, int S, hipStream_t st) {
+noble_status launch_proj(bool fwd, const ChainArgs& c, float* P, int S, hipStream_t st,
+                         const ZeroList* zero = nullptr) {
     ProjArgs a{};
+    if (zero) a.z = *zero;
     a.A = c.A;
     a.B = c.B;
     a.P = P;
@@ -384,7 +379,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     // gradient.
     constexpr int GBK = gemm_bk<E>();
     const int nkT = cdiv(T, GBK);
-    const WgradPlan wp = plan_wgrad(T, din, dout, r, GBK);
+    const WgradPlan wp = plan_wgrad(T, din, dout, GBK);
     float* wpart = reinterpret_cast<float*>(base + (r > 0 ? 4 * reg + partial_need(d) : 0));
 
     ZeroList z{};
@@ -406,7 +401,9 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         zero(dw2, r);
         zero(dp2, r);
     }
-    if (z.count > 0) {
+    // On the bf16 path with a branch, the projection kernel does the zeroing.
+    const bool zero_in_proj = sizeof(E) == 2 && r > 0 && T > 0;
+    if (z.count > 0 && !zero_in_proj) {
         hipLaunchKernelGGL(zero_kernel, dim3(512), dim3(256), 0, st, z);
         NOBLE_TRY(last_launch());
     }
@@ -436,7 +433,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         if constexpr (sizeof(E) == 2) {
             float* P = reinterpret_cast<float*>(base + 4 * reg);
             const int S = proj_split(T, dout);
-            NOBLE_TRY(launch_proj(false, a, P, S, st));
+            NOBLE_TRY(launch_proj(false, a, P, S, st, &z));
             NOBLE_TRY(launch_branch(false, a, P, S, st));
         } else
             NOBLE_TRY(launch_chain<E>(false, chain_rp<E>(r), a, (int)T, st));
@@ -452,30 +449,34 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         NOBLE_TRY((launch_gemm<E, true, true>(bt, st)));
     }
 
-    // Weight gradients, reduced over tokens (K = T), A and B both MN-major; a
-    // split dW stores partials that reduce_kernel then sums into dW.
+    // Weight gradients, reduced over tokens (K = T), A and B both MN-major, in
+    // one grouped launch: the rank-r gradients (dW_down, dW_up, dM) add
+    // atomically and fill the CUs that dW leaves idle; a split dW stores
+    // partials that reduce_kernel then sums into dW.
     {
         Batch bt;
         const Operand xT = operand1(seg(x, din, T), din);
         const Operand dyN = operand1(seg(dy, dout, T), dout);
-        bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split[0],
-               wp.split[0] > 1 ? wpart : nullptr);
+        bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split,
+               wp.split > 1 ? wpart : nullptr);
         if (r > 0) {
             const Operand dHN = operand1(seg(dHs, r, T), r);
             const Operand C2T = operand1(seg(C2s, r, T), r);
             const Operand C1T = operand1(seg(C1s, r, T), r);
             const Operand dH2N = operand1(seg(dH2s, r, T), r);
-            bt.add(xT, dHN, (int)din, (int)r, nkT, dWd, r, true, nullptr, nullptr, wp.split[1]);
-            bt.add(C2T, dyN, (int)r, (int)dout, nkT, dWu, dout, true, nullptr, nullptr, wp.split[2]);
-            bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM, r, true, nullptr, nullptr, wp.split[3]);
+            bt.add(xT, dHN, (int)din, (int)r, nkT, dWd, r, true, nullptr, nullptr,
+                   choose_split_atomic(cdiv(din, kBM), nkT));
+            bt.add(C2T, dyN, (int)r, (int)dout, nkT, dWu, dout, true, nullptr, nullptr,
+                   choose_split_atomic(cdiv(dout, kBN), nkT));
+            bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM, r, true, nullptr, nullptr, choose_split_atomic(1, nkT));
         }
         NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
-        if (wp.split[0] > 1) {
+        if (wp.split > 1) {
             ReduceList red{};
             red.part[0] = wpart;
             red.out[0] = dW;
             red.n[0] = din * dout;
-            red.S[0] = wp.split[0];
+            red.S[0] = wp.split;
             red.count = 1;
             hipLaunchKernelGGL(reduce_kernel, dim3(1024), dim3(256), 0, st, red);
             NOBLE_TRY(last_launch());

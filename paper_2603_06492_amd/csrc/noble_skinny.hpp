@@ -26,6 +26,7 @@
 #pragma once
 
 #include "noble_gemm_dma.hpp"
+#include "noble_kernels.hpp"
 
 namespace noble {
 
@@ -51,6 +52,8 @@ struct ProjArgs {
     float* P;           // partials [S][T][r] float32
     int64_t pstride;    // T * r
     int T, r, nk, S;    // nk: 64-element K chunks
+    ZeroList z;         // float arrays to clear on the side (the backward's
+                        // atomically accumulated gradients)
 };
 
 struct BranchArgs {
@@ -231,6 +234,21 @@ __global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
 #pragma unroll
     for (int c = 0; c < kPjStages - 1; ++c)
         if (c < n) proj_dma<BKM>(a, row0, kc0 + c, lds + c * kPjStage, wave, lane);
+
+    // The zeroing rides on the projection: every workgroup clears a strided
+    // share while its first loads are in flight.
+    {
+        const int64_t stride = (int64_t)gridDim.x * kPjThreads;
+        const int64_t gid = (int64_t)blockIdx.x * kPjThreads + tid;
+        for (int s = 0; s < a.z.count; ++s) {
+            float* p = a.z.ptr[s];
+            const int64_t cnt = a.z.n[s];
+            const int64_t n4 = cnt >> 2;
+            for (int64_t i = gid; i < n4; i += stride)
+                reinterpret_cast<f32x4*>(p)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int64_t i = (n4 << 2) + gid; i < cnt; i += stride) p[i] = 0.f;
+        }
+    }
     for (int i = 0; i < n; ++i) {
         // chunk i has landed once at most (stages - 2) later chunks are in flight
         const int ahead = min(n - 1 - i, kPjStages - 2);
