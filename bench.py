@@ -70,8 +70,22 @@ def recorded_traffic(kernel: str, workgroups: int):
     return rec.get("traffic_bytes")
 
 
-def cpu_baseline(workload: str, budget_s: float = 12.0):
-    """fp64 oracle fwd+bwd on a prefix sample of tokens of the same workload."""
+def _row_err(gpu, ref):
+    """max over rows of max_j |gpu - ref| / (max_j |ref| + 1e-6)."""
+    import numpy as np
+    num = np.abs(gpu - ref).max(axis=1)
+    den = np.abs(ref).max(axis=1) + 1e-6
+    return float((num / den).max())
+
+
+def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0):
+    """fp64 oracle fwd+bwd on a prefix of the tokens of the bench's own
+    projections (the same arrays the GPU ran on).  `samples[i]` holds the
+    weights and the first rows of x and dy of projection i; `gpu_rows(i, n)`
+    returns the GPU's y and dx rows [0, n).  Besides the oracle's rate it
+    reports the row-wise parity error of y and dx on those rows (both depend
+    only on their own tokens; the weight gradients, sums over every token,
+    are checked by the tests)."""
     import oracle  # test infrastructure: only this leg of the bench uses it
     from paper_2603_06492_amd import inputs as inp
     try:
@@ -81,24 +95,42 @@ def cpu_baseline(workload: str, budget_s: float = 12.0):
         threads = 1
     shapes = inp.workload_shapes(workload)
     T_full = shapes[0][1]
+    T_max = min(T_full, samples[0]["x"].shape[0])
     Ts = 128
     while True:
-        projs = [inp.draw_workload_projection(workload, i, T=Ts) for i in range(len(shapes))]
+        outs = []
         t0 = time.perf_counter()
-        for p in projs:
-            a = p.arrays
-            oracle.forward(a["x"], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                           a["omega2"], a["phi2"], a["W_up"])
-            oracle.backward(a["dy"], a["x"], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                            a["omega2"], a["phi2"], a["W_up"])
+        for a in samples:
+            Y, _ = oracle.forward(a["x"][:Ts], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"],
+                                  a["omega2"], a["phi2"], a["W_up"])
+            g = oracle.backward(a["dy"][:Ts], a["x"][:Ts], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"],
+                                a["omega2"], a["phi2"], a["W_up"])
+            outs.append((Y, g["dx"]))
         dt = time.perf_counter() - t0
-        if dt >= budget_s / 4 or Ts * 2 > T_full:
+        if dt >= budget_s / 4 or Ts * 2 > T_max:
             break
         Ts *= 2
-    flops = sum(flop_alg(Ts, di, do, r) for (_, _, di, do, r) in shapes)
+    # repeat the pass on the chosen sample until about `budget_s` of CPU work
+    passes = 1
+    while dt < budget_s:
+        t0 = time.perf_counter()
+        for a in samples:
+            oracle.forward(a["x"][:Ts], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"],
+                           a["omega2"], a["phi2"], a["W_up"])
+            oracle.backward(a["dy"][:Ts], a["x"][:Ts], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"],
+                            a["omega2"], a["phi2"], a["W_up"])
+        dt += time.perf_counter() - t0
+        passes += 1
+    parity = {"rows": Ts, "tol": 2e-2, "y": 0.0, "dx": 0.0}
+    for i, (Y, dx) in enumerate(outs):
+        gy, gdx = gpu_rows(i, Ts)
+        parity["y"] = max(parity["y"], round(_row_err(gy, Y), 6))
+        parity["dx"] = max(parity["dx"], round(_row_err(gdx, dx), 6))
+    flops = passes * sum(flop_alg(Ts, di, do, r) for (_, _, di, do, r) in shapes)
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{Ts} of {T_full} tokens of every projection, numpy float64, one fwd+bwd pass",
-            "seconds": round(dt, 3)}
+            "sample": f"first {Ts} of {T_full} tokens of every projection (the bench's own arrays), "
+                      f"numpy float64, {passes} fwd+bwd passes",
+            "seconds": round(dt, 3), "parity_vs_gpu": parity}
 
 
 def main():
@@ -108,6 +140,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llm1p5b_block_r128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-blas", action="store_true",
+                    help="skip the hipBLASLt (torch.mm) context timings of the plain products")
+    ap.add_argument("--proj-reps", type=int, default=50,
+                    help="calls per per-projection median (fwd, bwd, plain fwd, plain bwd)")
     ap.add_argument("--roofline-launches", type=int, default=20,
                     help="timed launches of the plain main GEMM for the roofline entry")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -132,12 +168,15 @@ def main():
     shapes = inp.workload_shapes(args.workload)
     print(f"[bench] workload {args.workload}: {len(shapes)} projections, T={wl['T']}, r={wl['r']}",
           file=sys.stderr, flush=True)
-    probs, plain = [], []
+    probs, plain, samples = [], [], []
+    sample_rows = min(wl["T"], 8192)
     for i in range(len(shapes)):
         p = inp.draw_workload_projection(args.workload, i)
         dp = DeviceProblem(p)
         probs.append(dp)
         plain.append(DeviceProblem(p, branch=False, inputs_from=dp))
+        if not args.no_cpu_baseline:
+            samples.append({k: (v[:sample_rows] if k in ("x", "dy") else v) for k, v in p.arrays.items()})
         del p
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
@@ -167,36 +206,52 @@ def main():
     ms_plain, wall_plain = timed(plain, args.steps, args.warmup)
     print(f"[bench] plain step {ms_plain:.3f} ms", file=sys.stderr, flush=True)
 
-    # Per-projection fwd / bwd times (events between calls on the same stream).
+    # Per-projection fwd / bwd times: median over `--proj-reps` calls, each
+    # bracketed by HIP events on the launch stream, after warm-up calls.
+    def median_ms(fn, reps):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+        for i in range(reps):
+            evs[2 * i].record(stream)
+            fn()
+            evs[2 * i + 1].record(stream)
+        torch.cuda.synchronize()
+        d = sorted(evs[2 * i].elapsed_time(evs[2 * i + 1]) for i in range(reps))
+        return d[reps // 2]
+
     per = []
     for dp, d0 in zip(probs, plain):
         T, di, do, r = dp.p.T, dp.p.d_in, dp.p.d_out, dp.p.r
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
-        reps = max(3, args.steps // 2)
-        for _ in range(2):
+        for _ in range(10):
             dp.fwd(); dp.bwd(); d0.fwd(); d0.bwd()
         torch.cuda.synchronize()
-        evs[0].record(stream)
-        for _ in range(reps):
-            dp.fwd()
-        evs[1].record(stream)
-        for _ in range(reps):
-            dp.bwd()
-        evs[2].record(stream)
-        for _ in range(reps):
-            d0.fwd()
-        evs[3].record(stream)
-        for _ in range(reps):
-            d0.bwd()
-        evs[4].record(stream)
-        torch.cuda.synchronize()
-        tf, tb, pf, pb = (evs[i].elapsed_time(evs[i + 1]) / reps for i in range(4))
+        tf = median_ms(dp.fwd, args.proj_reps)
+        tb = median_ms(dp.bwd, args.proj_reps)
+        pf = median_ms(d0.fwd, args.proj_reps)
+        pb = median_ms(d0.bwd, args.proj_reps)
         fl = flop_alg(T, di, do, r)
-        per.append({"projection": dp.p.name.split("/")[-1], "T": T, "d_in": di, "d_out": do, "r": r,
-                    "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4), "plain_fwd_ms": round(pf, 4),
-                    "plain_bwd_ms": round(pb, 4), "tflops": round(fl / ((tf + tb) * 1e-3) / 1e12, 2),
-                    "overhead": round((tf + tb) / (pf + pb) - 1, 4),
-                    "overhead_floor": round((r * (di + do) + r * r) / (di * do), 4)})
+        entry = {"projection": dp.p.name.split("/")[-1], "T": T, "d_in": di, "d_out": do, "r": r,
+                 "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4), "plain_fwd_ms": round(pf, 4),
+                 "plain_bwd_ms": round(pb, 4), "tflops": round(fl / ((tf + tb) * 1e-3) / 1e12, 2),
+                 "pct_bf16_peak": round(100 * fl / ((tf + tb) * 1e-3) / PEAK_BF16, 2),
+                 "main_gemm_pct_peak": round(100 * 6.0 * T * di * do / ((pf + pb) * 1e-3) / PEAK_BF16, 2),
+                 "overhead": round((tf + tb) / (pf + pb) - 1, 4),
+                 "overhead_floor": round((r * (di + do) + r * r) / (di * do), 4)}
+        if not args.no_blas:
+            # Context only: hipBLASLt (through torch.mm) on the same plain
+            # products and operands, bf16 in and out: y = x W, dx = dy W^T,
+            # dW = x^T dy.  Operands are made contiguous first.
+            x, W, dy = dp.t["x"], dp.t["W"], dp.t["dy"]
+            WT, xT = W.t().contiguous(), x.t().contiguous()
+            for _ in range(3):
+                torch.mm(x, W); torch.mm(dy, WT); torch.mm(xT, dy)
+            bf = median_ms(lambda: torch.mm(x, W), args.proj_reps // 2)
+            bdx = median_ms(lambda: torch.mm(dy, WT), args.proj_reps // 2)
+            bdw = median_ms(lambda: torch.mm(xT, dy), args.proj_reps // 2)
+            del WT, xT
+            entry["hipblaslt_plain_ms"] = {"fwd": round(bf, 4), "dx": round(bdx, 4), "dW": round(bdw, 4),
+                                           "main_pct_peak": round(100 * 6.0 * T * di * do / ((bf + bdx + bdw) * 1e-3)
+                                                                  / PEAK_BF16, 2)}
+        per.append(entry)
 
     # Roofline entry: the main bf16 MFMA GEMM (x W, plain forward: exactly one
     # kernel launch per call), timed over its own launches with HIP events on
@@ -261,7 +316,11 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (fp64 oracle)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(args.workload)
+        def gpu_rows(i, n):
+            dp = probs[i]
+            return (dp.y[:n].float().cpu().numpy().astype("float64"),
+                    dp.g["dx"][:n].float().cpu().numpy().astype("float64"))
+        out["cpu_baseline"] = cpu_baseline(args.workload, samples, gpu_rows)
     print(json.dumps(out), flush=True)
 
 
