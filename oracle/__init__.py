@@ -8,7 +8,13 @@ unpinned".
 """
 
 from .noble_oracle import (  # noqa: F401
+    ACTIVATIONS,
+    LEAKY_SLOPE,
+    activation_slope,
+    activation_value,
     backward,
+    branch_backward,
+    branch_forward,
     branch_param_shapes,
     cosnet_backward,
     cosnet_forward,

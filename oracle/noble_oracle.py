@@ -39,6 +39,12 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = [
+    "ACTIVATIONS",
+    "LEAKY_SLOPE",
+    "activation_value",
+    "activation_slope",
+    "branch_forward",
+    "branch_backward",
     "cosnet_forward",
     "cosnet_backward",
     "forward",
@@ -46,9 +52,83 @@ __all__ = [
     "branch_param_shapes",
 ]
 
+# The bottleneck activations of the ablation in §5 (Table 5): each nonlinearity
+# as a single activation and as the 2-layer sandwich with the mixing matrix M
+# between two applications (the CosNet form of Eq. (2)).  name -> (f, layers).
+# Readings (the paper names the activations but not their parameters): every
+# layer keeps the per-dimension affine w (.) h + p of Eq. (2) before f, so
+# w = 1, p = 0 gives the bare activation; LeakyReLU has negative slope 0.01 and
+# GELU is the exact form x Phi(x) (the common library defaults).
+ACTIVATIONS = {
+    "cosnet": ("cos", 2),
+    "cos": ("cos", 1),
+    "tanh": ("tanh", 1),
+    "tanh_m": ("tanh", 2),
+    "leaky_relu": ("leaky_relu", 1),
+    "leaky_relu_m": ("leaky_relu", 2),
+    "gelu": ("gelu", 1),
+    "gelu_m": ("gelu", 2),
+}
+LEAKY_SLOPE = 0.01
+
 
 def _f64(a):
     return None if a is None else np.asarray(a, dtype=np.float64)
+
+
+def _phi_cdf(a):
+    """Standard normal CDF, 0.5 (1 + erf(a / sqrt 2))."""
+    from scipy.special import erf
+    return 0.5 * (1.0 + erf(a / np.sqrt(2.0)))
+
+
+def activation_value(f, a):
+    """f(a) elementwise for f in cos, tanh, leaky_relu, gelu."""
+    a = _f64(a)
+    if f == "cos":
+        return np.cos(a)
+    if f == "tanh":
+        return np.tanh(a)
+    if f == "leaky_relu":
+        return np.where(a > 0, a, LEAKY_SLOPE * a)
+    if f == "gelu":
+        return a * _phi_cdf(a)
+    raise ValueError(f"unknown activation {f!r}")
+
+
+def activation_slope(f, a):
+    """f'(a) elementwise.  d cos = -sin; d tanh = 1 - tanh^2; LeakyReLU's slope
+    is 1 for a > 0 and LEAKY_SLOPE otherwise; d (a Phi(a)) = Phi(a) + a phi(a)
+    with phi the standard normal density."""
+    a = _f64(a)
+    if f == "cos":
+        return -np.sin(a)
+    if f == "tanh":
+        return 1.0 - np.tanh(a) ** 2
+    if f == "leaky_relu":
+        return np.where(a > 0, 1.0, LEAKY_SLOPE)
+    if f == "gelu":
+        return _phi_cdf(a) + a * np.exp(-0.5 * a * a) / np.sqrt(2.0 * np.pi)
+    raise ValueError(f"unknown activation {f!r}")
+
+
+def branch_forward(H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
+    """The bottleneck nonlinearity sigma applied to every row of ``H: [T, r]``.
+
+    2-layer forms (Eq. (2) for cosine):  A1 = w1 (.) H + p1, C1 = f(A1),
+    H2 = C1 M, A2 = w2 (.) H2 + p2, C2 = f(A2).  1-layer forms stop at
+    C2 = C1 = f(A1) and ignore M, w2, p2.  Returns the intermediates by name.
+    """
+    f, layers = ACTIVATIONS[activation]
+    H = _f64(H)
+    A1 = H * _f64(omega1) + _f64(phi1)          # w1 (.) h + p1
+    C1 = activation_value(f, A1)                 # h1 = f(.)
+    if layers == 1:
+        return {"A1": A1, "C1": C1, "C2": C1}
+    H2 = C1 @ _f64(M)                            # h2 = h1 mixed by M (row form)
+    A2 = H2 * _f64(omega2) + _f64(phi2)          # w2 (.) h2 + p2
+    C2 = activation_value(f, A2)                 # sigma(h) = f(.)
+    return {"A1": A1, "C1": C1, "H2": H2, "A2": A2, "C2": C2}
 
 
 def cosnet_forward(H, omega1, phi1, M, omega2, phi2):
@@ -56,28 +136,51 @@ def cosnet_forward(H, omega1, phi1, M, omega2, phi2):
 
     Returns the intermediates by name: A1, C1, H2, A2, C2 (all ``[T, r]``).
     """
-    H = _f64(H)
-    A1 = H * _f64(omega1) + _f64(phi1)          # w1 (.) h + p1
-    C1 = np.cos(A1)                              # h1 = cos(.)
-    H2 = C1 @ _f64(M)                            # h2 = h1 mixed by M (row form)
-    A2 = H2 * _f64(omega2) + _f64(phi2)          # w2 (.) h2 + p2
-    C2 = np.cos(A2)                              # sigma(h) = cos(.)
-    return {"A1": A1, "C1": C1, "H2": H2, "A2": A2, "C2": C2}
+    return branch_forward(H, "cosnet", omega1, phi1, M, omega2, phi2)
 
 
-def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up):
-    """Eq. (1) with sigma = CosNet.  Rows of ``x`` are independent tokens, so
-    passing a subset of rows of ``x`` yields exactly those rows of ``Y``.
+def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="cosnet"):
+    """Eq. (1) with sigma = the named bottleneck activation (CosNet by
+    default).  Rows of ``x`` are independent tokens, so passing a subset of
+    rows of ``x`` yields exactly those rows of ``Y``.
 
     Returns ``(Y, H)`` where ``H = x @ W_down`` is the bottleneck input.
     """
     x = _f64(x)
     H = x @ _f64(W_down)
-    C2 = cosnet_forward(H, omega1, phi1, M, omega2, phi2)["C2"]
+    C2 = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)["C2"]
     Y = x @ _f64(W) + C2 @ _f64(W_up)
     if b is not None:
         Y = Y + _f64(b)
     return Y, H
+
+
+def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
+    """Chain rule through sigma for ``L`` with ``dL/dC2 = dC2`` (rows = tokens).
+
+    Recomputes the forward chain from ``H``.  Returns dH, domega1, dphi1, the
+    recomputed C2 and, for 2-layer forms, dM, domega2, dphi2 (None otherwise).
+    """
+    f, layers = ACTIVATIONS[activation]
+    dC2 = _f64(dC2)
+    H = _f64(H)
+    w1 = _f64(omega1)
+    fw = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)
+    out = {"dM": None, "domega2": None, "dphi2": None, "C2": fw["C2"]}
+    if layers == 2:
+        dA2 = activation_slope(f, fw["A2"]) * dC2    # C2 = f(A2)
+        out["domega2"] = np.sum(dA2 * fw["H2"], axis=0)   # A2 = w2 (.) H2 + p2
+        out["dphi2"] = np.sum(dA2, axis=0)
+        dH2 = dA2 * _f64(omega2)
+        out["dM"] = fw["C1"].T @ dH2                 # H2 = C1 @ M
+        dC1 = dH2 @ _f64(M).T
+    else:
+        dC1 = dC2                                    # C2 = C1
+    dA1 = activation_slope(f, fw["A1"]) * dC1        # C1 = f(A1)
+    out["domega1"] = np.sum(dA1 * H, axis=0)         # A1 = w1 (.) H + p1
+    out["dphi1"] = np.sum(dA1, axis=0)
+    out["dH"] = dA1 * w1
+    return out
 
 
 def cosnet_backward(dC2, H, omega1, phi1, M, omega2, phi2):
@@ -86,39 +189,18 @@ def cosnet_backward(dC2, H, omega1, phi1, M, omega2, phi2):
     Recomputes the forward chain from ``H``.  Returns dH, dM, domega1, dphi1,
     domega2, dphi2 and the recomputed C2.
     """
-    dC2 = _f64(dC2)
-    H = _f64(H)
-    w1, w2 = _f64(omega1), _f64(omega2)
-    f = cosnet_forward(H, omega1, phi1, M, omega2, phi2)
-    dA2 = -np.sin(f["A2"]) * dC2                 # d cos(A2) = -sin(A2) dA2
-    domega2 = np.sum(dA2 * f["H2"], axis=0)      # A2 = w2 (.) H2 + p2
-    dphi2 = np.sum(dA2, axis=0)
-    dH2 = dA2 * w2
-    dM = f["C1"].T @ dH2                         # H2 = C1 @ M
-    dC1 = dH2 @ _f64(M).T
-    dA1 = -np.sin(f["A1"]) * dC1                 # C1 = cos(A1)
-    domega1 = np.sum(dA1 * H, axis=0)            # A1 = w1 (.) H + p1
-    dphi1 = np.sum(dA1, axis=0)
-    dH = dA1 * w1
-    return {
-        "dH": dH,
-        "dM": dM,
-        "domega1": domega1,
-        "dphi1": dphi1,
-        "domega2": domega2,
-        "dphi2": dphi2,
-        "C2": f["C2"],
-    }
+    return branch_backward(dC2, H, "cosnet", omega1, phi1, M, omega2, phi2)
 
 
 def backward(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up,
-             dx_rows=None, dW_rows=None):
+             dx_rows=None, dW_rows=None, activation="cosnet"):
     """Gradients of ``L = sum(dy * Y)`` with respect to every input of Eq. (1).
 
     Returns a dict with dx, dW, db, dW_down, dM, dW_up, domega1, dphi1,
-    domega2, dphi2.  ``dx_rows`` / ``dW_rows`` (index arrays) restrict the two
-    large products to the listed rows of dx and dW; every other gradient is
-    always complete.  Row selection does not change any value.
+    domega2, dphi2 (dM, domega2, dphi2 are None for 1-layer activations).
+    ``dx_rows`` / ``dW_rows`` (index arrays) restrict the two large products
+    to the listed rows of dx and dW; every other gradient is always complete.
+    Row selection does not change any value.
     """
     dy = _f64(dy)
     x = _f64(x)
@@ -127,7 +209,7 @@ def backward(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up,
     U = _f64(W_up)
     H = x @ D
     dC2 = dy @ U.T                               # Y = ... + C2 @ W_up
-    cb = cosnet_backward(dC2, H, omega1, phi1, M, omega2, phi2)
+    cb = branch_backward(dC2, H, activation, omega1, phi1, M, omega2, phi2)
     dH = cb["dH"]
     out = {
         "dW_up": cb["C2"].T @ dy,

@@ -1,6 +1,7 @@
 """Strength of the oracle pins: plausible mistakes planted in a copy of the
 oracle (on the CPU, never on a device) must each be caught by the pin battery
-(hand-worked closed-form examples plus finite differences)."""
+(hand-worked closed-form examples of the CosNet layer and of every bottleneck
+activation, plus finite differences of every activation variant)."""
 
 import importlib.util
 import json
@@ -20,17 +21,30 @@ MUTATIONS = {
     "forward_mixing_transposed": ("H2 = C1 @ _f64(M)", "H2 = C1 @ _f64(M).T"),
     "phase2_dropped": ("A2 = H2 * _f64(omega2) + _f64(phi2)", "A2 = H2 * _f64(omega2)"),
     "bias_dropped": ("Y = Y + _f64(b)", "Y = Y"),
-    "sin_sign_outer": ("dA2 = -np.sin(f[\"A2\"]) * dC2", "dA2 = np.sin(f[\"A2\"]) * dC2"),
-    "sin_sign_inner": ("dA1 = -np.sin(f[\"A1\"]) * dC1", "dA1 = np.sin(f[\"A1\"]) * dC1"),
+    "cos_slope_sign": ("return -np.sin(a)", "return np.sin(a)"),
+    "outer_slope_sign": ("dA2 = activation_slope(f, fw[\"A2\"]) * dC2", "dA2 = -activation_slope(f, fw[\"A2\"]) * dC2"),
+    "inner_slope_sign": ("dA1 = activation_slope(f, fw[\"A1\"]) * dC1", "dA1 = -activation_slope(f, fw[\"A1\"]) * dC1"),
     "dC1_not_transposed": ("dC1 = dH2 @ _f64(M).T", "dC1 = dH2 @ _f64(M)"),
-    "dM_transposed": ("dM = f[\"C1\"].T @ dH2", "dM = dH2.T @ f[\"C1\"]"),
-    "domega1_dropped_H": ("domega1 = np.sum(dA1 * H, axis=0)", "domega1 = np.sum(dA1, axis=0)"),
-    "domega2_wrong_factor": ("domega2 = np.sum(dA2 * f[\"H2\"], axis=0)",
-                             "domega2 = np.sum(dA2 * f[\"C1\"], axis=0)"),
-    "dH_missing_omega1": ("dH = dA1 * w1", "dH = dA1"),
-    "dH2_missing_omega2": ("dH2 = dA2 * w2", "dH2 = dA2"),
+    "dM_transposed": ("out[\"dM\"] = fw[\"C1\"].T @ dH2", "out[\"dM\"] = dH2.T @ fw[\"C1\"]"),
+    "domega1_dropped_H": ("out[\"domega1\"] = np.sum(dA1 * H, axis=0)", "out[\"domega1\"] = np.sum(dA1, axis=0)"),
+    "domega2_wrong_factor": ("out[\"domega2\"] = np.sum(dA2 * fw[\"H2\"], axis=0)",
+                             "out[\"domega2\"] = np.sum(dA2 * fw[\"C1\"], axis=0)"),
+    "dH_missing_omega1": ("out[\"dH\"] = dA1 * w1", "out[\"dH\"] = dA1"),
+    "dH2_missing_omega2": ("dH2 = dA2 * _f64(omega2)", "dH2 = dA2"),
     "dx_missing_branch": ("out[\"dx\"] = dy @ W.T + dH @ D.T", "out[\"dx\"] = dy @ W.T"),
     "dW_up_uses_cos_argument": ("\"dW_up\": cb[\"C2\"].T @ dy", "\"dW_up\": np.cos(cb[\"C2\"]).T @ dy"),
+    # activation variants
+    "tanh_slope_not_squared": ("return 1.0 - np.tanh(a) ** 2", "return 1.0 - np.tanh(a)"),
+    "tanh_value_is_sin": ("return np.tanh(a)\n", "return np.sin(a)\n"),
+    "leaky_value_is_relu": ("return np.where(a > 0, a, LEAKY_SLOPE * a)", "return np.where(a > 0, a, 0.0 * a)"),
+    "leaky_slope_swapped": ("return np.where(a > 0, 1.0, LEAKY_SLOPE)", "return np.where(a > 0, LEAKY_SLOPE, 1.0)"),
+    "leaky_slope_value": ("LEAKY_SLOPE = 0.01", "LEAKY_SLOPE = 0.02"),
+    "gelu_slope_missing_density": ("return _phi_cdf(a) + a * np.exp(-0.5 * a * a) / np.sqrt(2.0 * np.pi)",
+                                   "return _phi_cdf(a)"),
+    "gelu_value_is_cdf": ("return a * _phi_cdf(a)", "return _phi_cdf(a)"),
+    "gelu_cdf_unscaled": ("return 0.5 * (1.0 + erf(a / np.sqrt(2.0)))", "return 0.5 * (1.0 + erf(a))"),
+    "one_layer_chain_mixes": ("        dC1 = dC2                                    # C2 = C1",
+                              "        dC1 = 2.0 * dC2"),
 }
 
 
@@ -47,7 +61,7 @@ def _eval(v):
     if isinstance(v, list):
         return np.array([_eval(e) for e in v], dtype=np.float64)
     if isinstance(v, str):
-        return float(eval(v, {"__builtins__": {}}, {"pi": math.pi, "sqrt": math.sqrt}))
+        return float(eval(v, {"__builtins__": {}}, {"pi": math.pi, "sqrt": math.sqrt, "atanh": math.atanh}))
     return float(v)
 
 
@@ -72,25 +86,43 @@ def _battery_passes(mod):
             for k in e:
                 if k in g and not np.allclose(g[k], e[k], rtol=0, atol=1e-11):
                     return False
+    with open(os.path.join(GOLDEN, "activation_examples.json")) as f:
+        for ex in json.load(f)["examples"]:
+            act = ex["activation"]
+            p = {k: _eval(v) for k, v in ex["inputs"].items()}
+            Y, _ = mod.forward(p["x"], p["W"], p["b"], p["W_down"], p["omega1"], p["phi1"], p["M"],
+                               p["omega2"], p["phi2"], p["W_up"], activation=act)
+            g = mod.backward(p["dy"], p["x"], p["W"], p["W_down"], p["omega1"], p["phi1"], p["M"],
+                             p["omega2"], p["phi2"], p["W_up"], activation=act)
+            for k, v in ex["expected"].items():
+                got = Y if k == "y" else g[k]
+                if not np.allclose(got, _eval(v), rtol=0, atol=1e-12):
+                    return False
     p = {k: v.astype(np.float64) for k, v in
          inp.draw_projection("t", 4, 5, 6, 3, "f32", 21, bias_std=0.5).arrays.items()}
-    g = bwd(p)
+    for act, (_, layers) in sorted(good.ACTIVATIONS.items()):
+        g = mod.backward(p["dy"], p["x"], p["W"], p["W_down"], p["omega1"], p["phi1"], p["M"],
+                         p["omega2"], p["phi2"], p["W_up"], activation=act)
 
-    def loss(q):
-        return float(np.sum(q["dy"] * fwd(q)[0]))
+        def loss(q):
+            Y, _ = mod.forward(q["x"], q["W"], q["b"], q["W_down"], q["omega1"], q["phi1"], q["M"],
+                               q["omega2"], q["phi2"], q["W_up"], activation=act)
+            return float(np.sum(q["dy"] * Y))
 
-    pairs = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "M": "dM", "W_up": "dW_up",
-             "omega1": "domega1", "phi1": "dphi1", "omega2": "domega2", "phi2": "dphi2"}
-    for pn, gn in pairs.items():
-        for idx in np.ndindex(p[pn].shape):
-            qp, qm = dict(p), dict(p)
-            qp[pn] = p[pn].copy()
-            qm[pn] = p[pn].copy()
-            qp[pn][idx] += 1e-6
-            qm[pn][idx] -= 1e-6
-            fd = (loss(qp) - loss(qm)) / 2e-6
-            if abs(fd - g[gn][idx]) > 1e-6 * max(1.0, abs(g[gn][idx])):
-                return False
+        pairs = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "W_up": "dW_up",
+                 "omega1": "domega1", "phi1": "dphi1"}
+        if layers == 2:
+            pairs.update({"M": "dM", "omega2": "domega2", "phi2": "dphi2"})
+        for pn, gn in pairs.items():
+            for idx in np.ndindex(p[pn].shape):
+                qp, qm = dict(p), dict(p)
+                qp[pn] = p[pn].copy()
+                qm[pn] = p[pn].copy()
+                qp[pn][idx] += 1e-6
+                qm[pn][idx] -= 1e-6
+                fd = (loss(qp) - loss(qm)) / 2e-6
+                if abs(fd - g[gn][idx]) > 1e-6 * max(1.0, abs(g[gn][idx])):
+                    return False
     return True
 
 

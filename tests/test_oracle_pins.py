@@ -301,3 +301,163 @@ def test_input_recipe_is_seeded_and_shaped():
         np.testing.assert_array_equal(inp.round_bf16(p[k]), p[k])
     assert np.all(p["b"] == 0)
     assert 0 <= p["phi1"].min() and p["phi1"].max() < 2 * np.pi
+
+
+# ------------------------------------------------- activation variants -----
+# The ablation of §5 (Table 5): cos, tanh, LeakyReLU and GELU, as a single
+# activation and as the 2-layer sandwich with M.
+
+ACTS = sorted(oracle.ACTIVATIONS)
+ONE_LAYER = [a for a in ACTS if oracle.ACTIVATIONS[a][1] == 1]
+
+
+def _eval_act(v):
+    if isinstance(v, list):
+        return np.array([_eval_act(e) for e in v], dtype=np.float64)
+    if isinstance(v, str):
+        return float(eval(v, {"__builtins__": {}}, {"pi": math.pi, "sqrt": math.sqrt, "atanh": math.atanh}))
+    return float(v)
+
+
+def _activation_examples():
+    with open(os.path.join(GOLDEN, "activation_examples.json")) as f:
+        return json.load(f)["examples"]
+
+
+def _fwd_a(p, act):
+    return oracle.forward(p["x"], p["W"], p["b"], p["W_down"], p["omega1"], p["phi1"],
+                          p["M"], p["omega2"], p["phi2"], p["W_up"], activation=act)
+
+
+def _bwd_a(p, act):
+    return oracle.backward(p["dy"], p["x"], p["W"], p["W_down"], p["omega1"], p["phi1"],
+                           p["M"], p["omega2"], p["phi2"], p["W_up"], activation=act)
+
+
+@pytest.mark.parametrize("ex", _activation_examples(), ids=lambda e: e["name"])
+def test_activation_hand_examples(ex):
+    """r = 1 cases whose pre-activations are chosen so that each activation's
+    value and slope are known exactly (tanh(atanh t) = t, cos(pi/3) = 1/2,
+    LeakyReLU(-2) = -0.02, GELU(1) = Phi(1) from a normal table)."""
+    p = {k: _eval_act(v) for k, v in ex["inputs"].items()}
+    Y, _ = _fwd_a(p, ex["activation"])
+    g = _bwd_a(p, ex["activation"])
+    for k, v in ex["expected"].items():
+        got = Y if k == "y" else g[k]
+        np.testing.assert_allclose(got, _eval_act(v), rtol=0, atol=1e-12, err_msg=f"{ex['name']} {k}")
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_activation_gradients_match_central_differences(act):
+    p = _tiny(seed=17)
+    g = _bwd_a(p, act)
+    two = oracle.ACTIVATIONS[act][1] == 2
+
+    def loss(q):
+        return float(np.sum(q["dy"] * _fwd_a(q, act)[0]))
+
+    names = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "W_up": "dW_up",
+             "omega1": "domega1", "phi1": "dphi1"}
+    if two:
+        names.update({"M": "dM", "omega2": "domega2", "phi2": "dphi2"})
+    else:
+        assert g["dM"] is None and g["domega2"] is None and g["dphi2"] is None
+    for pname, gname in names.items():
+        base = p[pname]
+        fd = np.zeros_like(base)
+        for idx in np.ndindex(base.shape):
+            h = 1e-6 * max(1.0, abs(base[idx]))
+            qp, qm = dict(p), dict(p)
+            qp[pname] = base.copy()
+            qm[pname] = base.copy()
+            qp[pname][idx] += h
+            qm[pname][idx] -= h
+            fd[idx] = (loss(qp) - loss(qm)) / (2 * h)
+        scale = max(1.0, float(np.max(np.abs(g[gname]))))
+        assert np.max(np.abs(fd - g[gname])) <= 1e-6 * scale, (act, gname)
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_activation_gradients_match_torch_autograd(act):
+    """An independent torch formulation (torch's own tanh, leaky_relu with
+    slope 0.01, exact gelu, cos), differentiated by autograd in float64."""
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    fn = {"cos": torch.cos, "tanh": torch.tanh, "leaky_relu": lambda a: F.leaky_relu(a, 0.01),
+          "gelu": lambda a: F.gelu(a)}[oracle.ACTIVATIONS[act][0]]
+    two = oracle.ACTIVATIONS[act][1] == 2
+    p = _tiny(seed=23, T=9, d_in=16, d_out=24, r=8)
+    t = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True) for k, v in p.items()}
+    h = t["x"] @ t["W_down"]
+    c = fn(t["omega1"] * h + t["phi1"])
+    if two:
+        h2 = (c[:, :, None] * t["M"][None, :, :]).sum(dim=1)
+        c = fn(t["omega2"] * h2 + t["phi2"])
+    y = t["x"] @ t["W"] + t["b"] + c @ t["W_up"]
+    (y * t["dy"]).sum().backward()
+    Y, _ = _fwd_a(p, act)
+    np.testing.assert_allclose(Y, y.detach().numpy(), rtol=0, atol=1e-12)
+    g = _bwd_a(p, act)
+    names = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "W_up": "dW_up",
+             "omega1": "domega1", "phi1": "dphi1"}
+    if two:
+        names.update({"M": "dM", "omega2": "domega2", "phi2": "dphi2"})
+    for pname, gname in names.items():
+        np.testing.assert_allclose(g[gname], t[pname].grad.numpy(), rtol=1e-10, atol=1e-10,
+                                   err_msg=f"{act} {gname}")
+
+
+def test_one_layer_ignores_the_second_layer_parameters():
+    p = _tiny(seed=29)
+    for act in ONE_LAYER:
+        Y1, _ = _fwd_a(p, act)
+        q = dict(p, M=None, omega2=None, phi2=None)
+        Y2, _ = _fwd_a(q, act)
+        np.testing.assert_array_equal(Y1, Y2)
+
+
+def test_odd_and_even_single_activations():
+    """With p1 = 0: tanh is odd, cos even; flipping the sign of W_down flips
+    or keeps the branch accordingly."""
+    p = _tiny(seed=31)
+    p["phi1"] = np.zeros_like(p["phi1"])
+    q = dict(p, W_down=-p["W_down"])
+    W0 = dict(p, W_up=np.zeros_like(p["W_up"]))
+    base = _fwd_a(W0, "tanh")[0]
+    bt_p = _fwd_a(p, "tanh")[0] - base
+    bt_q = _fwd_a(q, "tanh")[0] - base
+    np.testing.assert_allclose(bt_q, -bt_p, rtol=0, atol=1e-13)
+    bc_p = _fwd_a(p, "cos")[0] - base
+    bc_q = _fwd_a(q, "cos")[0] - base
+    np.testing.assert_allclose(bc_q, bc_p, rtol=0, atol=1e-13)
+
+
+def test_leaky_relu_positive_homogeneity_and_linear_regime():
+    """LeakyReLU is positively homogeneous (with p1 = 0, scaling W_down by
+    c > 0 scales the 1-layer branch by c), and on positive pre-activations the
+    1-layer branch is the linear map (w1 (.) H + p1) W_up."""
+    p = _tiny(seed=37)
+    p["phi1"] = np.zeros_like(p["phi1"])
+    W0 = dict(p, W_up=np.zeros_like(p["W_up"]))
+    base = _fwd_a(W0, "leaky_relu")[0]
+    b1 = _fwd_a(p, "leaky_relu")[0] - base
+    b3 = _fwd_a(dict(p, W_down=2.5 * p["W_down"]), "leaky_relu")[0] - base
+    np.testing.assert_allclose(b3, 2.5 * b1, rtol=0, atol=1e-12)
+    q = dict(p, phi1=np.full_like(p["phi1"], 50.0))   # every A1 > 0
+    H = q["x"] @ q["W_down"]
+    lin = (H * q["omega1"] + q["phi1"]) @ q["W_up"]
+    np.testing.assert_allclose(_fwd_a(q, "leaky_relu")[0] - base, lin, rtol=0, atol=1e-10)
+
+
+def test_gelu_tends_to_identity_and_zero():
+    """GELU(a) -> a for large a and -> 0 for very negative a (the 1-layer
+    branch becomes linear, then vanishes)."""
+    p = _tiny(seed=41)
+    W0 = dict(p, W_up=np.zeros_like(p["W_up"]))
+    base = _fwd_a(W0, "gelu")[0]
+    H = p["x"] @ p["W_down"]
+    q = dict(p, phi1=np.full_like(p["phi1"], 40.0))
+    np.testing.assert_allclose(_fwd_a(q, "gelu")[0] - base, (H * q["omega1"] + 40.0) @ q["W_up"],
+                               rtol=0, atol=1e-10)
+    q = dict(p, phi1=np.full_like(p["phi1"], -40.0))
+    np.testing.assert_allclose(_fwd_a(q, "gelu")[0] - base, 0.0, rtol=0, atol=1e-12)
