@@ -15,7 +15,7 @@ What it computes (the paper, arXiv 2603.06492):
   §3.2) and an r x r mixing matrix ``M``.
 * Backward: the paper prints no gradient formulas.  They follow from the
   forward by the chain rule, using d cos(u)/du = -sin(u) (the derivative the
-  paper names in §6, "Why Cosine Activations?").
+  paper names in §5, "Why Cosine Activations?").
 
 Readings where the paper is silent or ambiguous:
 
@@ -32,6 +32,14 @@ Readings where the paper is silent or ambiguous:
 Everything is evaluated in float64 on whatever values it is handed; callers pass
 the exact values the device sees (bf16-rounded storage tensors upcast to
 float64).  There is no blocking, fusion or reordering beyond the equations.
+
+``mix_round`` (optional, default exact): an elementwise map applied to C1
+where it enters the mixing product, H2 = mix_round(C1) M, with its derivative
+taken as the identity (so dM = mix_round(C1)^T dH2 and dC1 = dH2 M^T).  With
+bf16 rounding this is the operand rounding of the bf16 mixed precision the
+paper trains in (§3.4); callers use it where a later decision (the sign that
+picks LeakyReLU's slope) must be taken from the same operand values a bf16
+implementation sees.
 """
 
 from __future__ import annotations
@@ -52,7 +60,7 @@ __all__ = [
     "branch_param_shapes",
 ]
 
-# The bottleneck activations of the ablation in §5 (Table 5): each nonlinearity
+# The bottleneck activations of the ablation in §4.4 (Table 5): each nonlinearity
 # as a single activation and as the 2-layer sandwich with the mixing matrix M
 # between two applications (the CosNet form of Eq. (2)).  name -> (f, layers).
 # Readings (the paper names the activations but not their parameters): every
@@ -112,12 +120,13 @@ def activation_slope(f, a):
     raise ValueError(f"unknown activation {f!r}")
 
 
-def branch_forward(H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
+def branch_forward(H, activation, omega1, phi1, M=None, omega2=None, phi2=None, mix_round=None):
     """The bottleneck nonlinearity sigma applied to every row of ``H: [T, r]``.
 
     2-layer forms (Eq. (2) for cosine):  A1 = w1 (.) H + p1, C1 = f(A1),
     H2 = C1 M, A2 = w2 (.) H2 + p2, C2 = f(A2).  1-layer forms stop at
-    C2 = C1 = f(A1) and ignore M, w2, p2.  Returns the intermediates by name.
+    C2 = C1 = f(A1) and ignore M, w2, p2.  Returns the intermediates by name
+    (C1m: the mixing operand, C1 or mix_round(C1)).
     """
     f, layers = ACTIVATIONS[activation]
     H = _f64(H)
@@ -125,10 +134,11 @@ def branch_forward(H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
     C1 = activation_value(f, A1)                 # h1 = f(.)
     if layers == 1:
         return {"A1": A1, "C1": C1, "C2": C1}
-    H2 = C1 @ _f64(M)                            # h2 = h1 mixed by M (row form)
+    C1m = C1 if mix_round is None else _f64(mix_round(C1))
+    H2 = C1m @ _f64(M)                           # h2 = h1 mixed by M (row form)
     A2 = H2 * _f64(omega2) + _f64(phi2)          # w2 (.) h2 + p2
     C2 = activation_value(f, A2)                 # sigma(h) = f(.)
-    return {"A1": A1, "C1": C1, "H2": H2, "A2": A2, "C2": C2}
+    return {"A1": A1, "C1": C1, "C1m": C1m, "H2": H2, "A2": A2, "C2": C2}
 
 
 def cosnet_forward(H, omega1, phi1, M, omega2, phi2):
@@ -139,7 +149,7 @@ def cosnet_forward(H, omega1, phi1, M, omega2, phi2):
     return branch_forward(H, "cosnet", omega1, phi1, M, omega2, phi2)
 
 
-def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="cosnet"):
+def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="cosnet", mix_round=None):
     """Eq. (1) with sigma = the named bottleneck activation (CosNet by
     default).  Rows of ``x`` are independent tokens, so passing a subset of
     rows of ``x`` yields exactly those rows of ``Y``.
@@ -148,14 +158,14 @@ def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="co
     """
     x = _f64(x)
     H = x @ _f64(W_down)
-    C2 = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)["C2"]
+    C2 = branch_forward(H, activation, omega1, phi1, M, omega2, phi2, mix_round)["C2"]
     Y = x @ _f64(W) + C2 @ _f64(W_up)
     if b is not None:
         Y = Y + _f64(b)
     return Y, H
 
 
-def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
+def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=None, mix_round=None):
     """Chain rule through sigma for ``L`` with ``dL/dC2 = dC2`` (rows = tokens).
 
     Recomputes the forward chain from ``H``.  Returns dH, domega1, dphi1, the
@@ -165,14 +175,14 @@ def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=
     dC2 = _f64(dC2)
     H = _f64(H)
     w1 = _f64(omega1)
-    fw = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)
+    fw = branch_forward(H, activation, omega1, phi1, M, omega2, phi2, mix_round)
     out = {"dM": None, "domega2": None, "dphi2": None, "C2": fw["C2"]}
     if layers == 2:
         dA2 = activation_slope(f, fw["A2"]) * dC2    # C2 = f(A2)
         out["domega2"] = np.sum(dA2 * fw["H2"], axis=0)   # A2 = w2 (.) H2 + p2
         out["dphi2"] = np.sum(dA2, axis=0)
         dH2 = dA2 * _f64(omega2)
-        out["dM"] = fw["C1"].T @ dH2                 # H2 = C1 @ M
+        out["dM"] = fw["C1m"].T @ dH2                # H2 = C1m @ M
         dC1 = dH2 @ _f64(M).T
     else:
         dC1 = dC2                                    # C2 = C1
@@ -193,7 +203,7 @@ def cosnet_backward(dC2, H, omega1, phi1, M, omega2, phi2):
 
 
 def backward(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up,
-             dx_rows=None, dW_rows=None, activation="cosnet"):
+             dx_rows=None, dW_rows=None, activation="cosnet", mix_round=None):
     """Gradients of ``L = sum(dy * Y)`` with respect to every input of Eq. (1).
 
     Returns a dict with dx, dW, db, dW_down, dM, dW_up, domega1, dphi1,
@@ -209,7 +219,7 @@ def backward(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up,
     U = _f64(W_up)
     H = x @ D
     dC2 = dy @ U.T                               # Y = ... + C2 @ W_up
-    cb = branch_backward(dC2, H, activation, omega1, phi1, M, omega2, phi2)
+    cb = branch_backward(dC2, H, activation, omega1, phi1, M, omega2, phi2, mix_round)
     dH = cb["dH"]
     out = {
         "dW_up": cb["C2"].T @ dy,
