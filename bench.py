@@ -8,11 +8,13 @@ tokens, d = 2048, r = 128, projections QKV 2048->6144, O 2048->2048, FFN up
 2048->8192, FFN down 8192->2048.
 
 Reported: algorithmic TFLOP/s, 6 T [d_in d_out + r (d_in + d_out) + r^2] per
-projection over the step time; the same step with r = 0 (plain linear, same
+projection over the step time (no r^2 term for the one-application
+activations, which have no M); the same step with r = 0 (plain linear, same
 kernels) and the overhead over it; the roofline of the main MFMA GEMM; and the
 fp64 oracle's throughput on a bounded sample on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                      [--activation NAME]   (CosNet by default)
 """
 
 from __future__ import annotations
@@ -36,17 +38,24 @@ PEAK_F32 = 157.3e12  # dense fp32 MFMA, MI355X
 METRIC = "NOBLE linear fwd+bwd TFLOP/s, % bf16 MFMA peak, overhead vs plain GEMM"
 
 
-def flop_alg(T, d_in, d_out, r):
-    return 6.0 * T * (d_in * d_out + r * (d_in + d_out) + r * r)
+def flop_alg(T, d_in, d_out, r, mixing=True):
+    return 6.0 * T * (d_in * d_out + r * (d_in + d_out) + (r * r if mixing else 0))
 
 
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "gemm_fwd_plain_ffn_up_T8192_traffic.md")
 
 
+# Sources of the roofline kernel (gemm_bf16_kernel): a traffic record stays
+# valid while these files and the compiler flags are unchanged.
+ROOFLINE_SOURCES = ("noble_tiles.hpp", "noble_gemm.hpp", "noble_gemm_dma.hpp")
+
+
 def kernel_source_hash() -> str:
+    from paper_2603_06492_amd import _build
     h = hashlib.sha256()
+    h.update(" ".join(_build.HIP_FLAGS).encode())
     d = os.path.join(ROOT, "paper_2603_06492_amd", "csrc")
-    for f in sorted(os.listdir(d)):
+    for f in ROOFLINE_SOURCES:
         h.update(f.encode())
         with open(os.path.join(d, f), "rb") as fh:
             h.update(fh.read())
@@ -78,7 +87,7 @@ def _row_err(gpu, ref):
     return float((num / den).max())
 
 
-def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0):
+def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0, activation: str = "cosnet"):
     """fp64 oracle fwd+bwd on a prefix of the tokens of the bench's own
     projections (the same arrays the GPU ran on).  `samples[i]` holds the
     weights and the first rows of x and dy of projection i; `gpu_rows(i, n)`
@@ -88,6 +97,15 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0):
     are checked by the tests)."""
     import oracle  # test infrastructure: only this leg of the bench uses it
     from paper_2603_06492_amd import inputs as inp
+    from paper_2603_06492_amd import noble
+    mixing = noble.two_layers(activation)
+    # the variants' two-application forms are compared with the mixing
+    # operand C1 rounded to bf16 as the kernels round it (a sign decision of
+    # LeakyReLU and GELU's conditioning depend on it)
+    mix = None
+    if mixing and activation != "cosnet":
+        mix = lambda a: inp.round_bf16(np.asarray(a, dtype=np.float32)).astype(np.float64)
+    kw = dict(activation=activation, mix_round=mix)
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
@@ -102,9 +120,9 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0):
         t0 = time.perf_counter()
         for a in samples:
             Y, _ = oracle.forward(a["x"][:Ts], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                                  a["omega2"], a["phi2"], a["W_up"])
+                                  a["omega2"], a["phi2"], a["W_up"], **kw)
             g = oracle.backward(a["dy"][:Ts], a["x"][:Ts], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                                a["omega2"], a["phi2"], a["W_up"])
+                                a["omega2"], a["phi2"], a["W_up"], **kw)
             outs.append((Y, g["dx"]))
         dt = time.perf_counter() - t0
         if dt >= budget_s / 4 or Ts * 2 > T_max:
@@ -116,9 +134,9 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0):
         t0 = time.perf_counter()
         for a in samples:
             oracle.forward(a["x"][:Ts], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                           a["omega2"], a["phi2"], a["W_up"])
+                           a["omega2"], a["phi2"], a["W_up"], **kw)
             oracle.backward(a["dy"][:Ts], a["x"][:Ts], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                            a["omega2"], a["phi2"], a["W_up"])
+                            a["omega2"], a["phi2"], a["W_up"], **kw)
         dt += time.perf_counter() - t0
         passes += 1
     parity = {"rows": Ts, "tol": 2e-2, "y": 0.0, "dx": 0.0}
@@ -126,7 +144,7 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0):
         gy, gdx = gpu_rows(i, Ts)
         parity["y"] = max(parity["y"], round(_row_err(gy, Y), 6))
         parity["dx"] = max(parity["dx"], round(_row_err(gdx, dx), 6))
-    flops = passes * sum(flop_alg(Ts, di, do, r) for (_, _, di, do, r) in shapes)
+    flops = passes * sum(flop_alg(Ts, di, do, r, mixing) for (_, _, di, do, r) in shapes)
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"first {Ts} of {T_full} tokens of every projection (the bench's own arrays), "
                       f"numpy float64, {passes} fwd+bwd passes",
@@ -139,6 +157,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llm1p5b_block_r128")
+    ap.add_argument("--activation", default="cosnet",
+                    help="bottleneck activation: cosnet (default), cos, tanh, tanh_m, leaky_relu, "
+                         "leaky_relu_m, gelu, gelu_m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-blas", action="store_true",
                     help="skip the hipBLASLt (torch.mm) context timings of the plain products")
@@ -158,8 +179,10 @@ def main():
 
     import torch
     from paper_2603_06492_amd import inputs as inp
+    from paper_2603_06492_amd import noble
     from paper_2603_06492_amd.runner import DeviceProblem
 
+    mixing = noble.two_layers(args.activation)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
@@ -172,7 +195,7 @@ def main():
     sample_rows = min(wl["T"], 8192)
     for i in range(len(shapes)):
         p = inp.draw_workload_projection(args.workload, i)
-        dp = DeviceProblem(p)
+        dp = DeviceProblem(p, activation=args.activation)
         probs.append(dp)
         plain.append(DeviceProblem(p, branch=False, inputs_from=dp))
         if not args.no_cpu_baseline:
@@ -228,14 +251,14 @@ def main():
         tb = median_ms(dp.bwd, args.proj_reps)
         pf = median_ms(d0.fwd, args.proj_reps)
         pb = median_ms(d0.bwd, args.proj_reps)
-        fl = flop_alg(T, di, do, r)
+        fl = flop_alg(T, di, do, r, mixing)
         entry = {"projection": dp.p.name.split("/")[-1], "T": T, "d_in": di, "d_out": do, "r": r,
                  "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4), "plain_fwd_ms": round(pf, 4),
                  "plain_bwd_ms": round(pb, 4), "tflops": round(fl / ((tf + tb) * 1e-3) / 1e12, 2),
                  "pct_bf16_peak": round(100 * fl / ((tf + tb) * 1e-3) / PEAK_BF16, 2),
                  "main_gemm_pct_peak": round(100 * 6.0 * T * di * do / ((pf + pb) * 1e-3) / PEAK_BF16, 2),
                  "overhead": round((tf + tb) / (pf + pb) - 1, 4),
-                 "overhead_floor": round((r * (di + do) + r * r) / (di * do), 4)}
+                 "overhead_floor": round((r * (di + do) + (r * r if mixing else 0)) / (di * do), 4)}
         if not args.no_blas:
             # Context only: hipBLASLt (through torch.mm) on the same plain
             # products and operands, bf16 in and out: y = x W, dx = dy W^T,
@@ -285,10 +308,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    flops_step = sum(flop_alg(T, di, do, r) for (_, T, di, do, r) in shapes)
+    flops_step = sum(flop_alg(T, di, do, r, mixing) for (_, T, di, do, r) in shapes)
     main_flops = sum(6.0 * T * di * do for (_, T, di, do, r) in shapes)
     value = flops_step / (ms_noble * 1e-3) / 1e12
-    floor = sum(T * (r * (di + do) + r * r) for (_, T, di, do, r) in shapes) / \
+    floor = sum(T * (r * (di + do) + (r * r if mixing else 0)) for (_, T, di, do, r) in shapes) / \
         sum(T * di * do for (_, T, di, do, r) in shapes)
     out = {
         "metric": METRIC,
@@ -303,7 +326,7 @@ def main():
         "vs_baseline": None,
         "dtype": wl["dtype"],
         "data": "synthetic",
-        "config": {"workload": args.workload, "T": wl["T"], "r": wl["r"],
+        "config": {"workload": args.workload, "T": wl["T"], "r": wl["r"], "activation": args.activation,
                    "projections": [f"{n} {di}->{do}" for (n, _, di, do, _) in shapes]},
         "pct_bf16_peak": round(100 * value / (PEAK_BF16 / 1e12), 2),
         "plain_ms_per_step": round(ms_plain, 4),
@@ -320,7 +343,7 @@ def main():
             dp = probs[i]
             return (dp.y[:n].float().cpu().numpy().astype("float64"),
                     dp.g["dx"][:n].float().cpu().numpy().astype("float64"))
-        out["cpu_baseline"] = cpu_baseline(args.workload, samples, gpu_rows)
+        out["cpu_baseline"] = cpu_baseline(args.workload, samples, gpu_rows, activation=args.activation)
     print(json.dumps(out), flush=True)
 
 

@@ -15,6 +15,12 @@
  * (the paper prints none; d cos(u)/du = -sin(u)), recomputing the cosines from
  * the saved H instead of storing them.
  *
+ * desc->activation selects the bottleneck nonlinearity among the variants of
+ * the activation ablation (Sec. 4.4, Table 5): cos (the CosNet above), tanh,
+ * LeakyReLU (negative slope 0.01) or GELU (exact, a Phi(a)), each either in
+ * the two-application form above (f in place of cos, with M between) or as
+ * one application C2 = f(H (.) omega1 + phi1), which has no M, omega2, phi2.
+ *
  * Conventions shared by every call
  * --------------------------------
  *  - All tensors are dense, row-major and contiguous, in device memory owned
@@ -61,17 +67,33 @@ typedef enum noble_status {
     NOBLE_ERR_MISALIGNED = 4,        /* a pointer is not 16-byte aligned */
     NOBLE_ERR_WORKSPACE_TOO_SMALL = 5, /* scratch_bytes below the required size */
     NOBLE_ERR_UNSUPPORTED_DEVICE = 6,  /* current device is not gfx950 */
-    NOBLE_ERR_HIP = 7                /* a HIP runtime call or launch failed */
+    NOBLE_ERR_HIP = 7,               /* a HIP runtime call or launch failed */
+    NOBLE_ERR_BAD_ACTIVATION = 8     /* desc->activation is not a noble_activation */
 } noble_status;
 
-/* Problem description.  `dtype` holds a noble_dtype value. */
+/* Bottleneck nonlinearity (Sec. 3.2 Eq. 2; variants of Sec. 4.4, Table 5).
+ * The _M forms and COSNET apply f twice with M between them; the others
+ * apply f once. */
+typedef enum noble_activation {
+    NOBLE_ACT_COSNET = 0,       /* cos(w2 (.) (cos(w1 (.) H + p1) M) + p2) */
+    NOBLE_ACT_COS = 1,          /* cos(w1 (.) H + p1) */
+    NOBLE_ACT_TANH = 2,
+    NOBLE_ACT_TANH_M = 3,
+    NOBLE_ACT_LEAKY_RELU = 4,
+    NOBLE_ACT_LEAKY_RELU_M = 5,
+    NOBLE_ACT_GELU = 6,
+    NOBLE_ACT_GELU_M = 7
+} noble_activation;
+
+/* Problem description.  `dtype` holds a noble_dtype value and `activation`
+ * a noble_activation (0, the CosNet, for a zero-initialised desc). */
 typedef struct noble_linear_desc {
     int64_t T;      /* tokens (rows of x, y, dy, dx) */
     int64_t d_in;   /* input features */
     int64_t d_out;  /* output features */
     int64_t r;      /* bottleneck rank; 0 = plain linear */
     int32_t dtype;  /* noble_dtype */
-    int32_t reserved; /* must be 0 */
+    int32_t activation; /* noble_activation */
 } noble_linear_desc;
 
 /* Sizes of the two caller-owned work buffers for `desc`.
@@ -83,7 +105,8 @@ typedef struct noble_linear_desc {
  *                  only when r > 0; the backward may use it also when r = 0
  *                  (split-K partial sums of dW), whenever scratch_bytes > 0.
  * Either output pointer may be NULL.  Returns NOBLE_ERR_NULL_ARG (desc NULL),
- * NOBLE_ERR_BAD_SHAPE or NOBLE_ERR_BAD_DTYPE; makes no HIP call. */
+ * NOBLE_ERR_BAD_SHAPE, NOBLE_ERR_BAD_DTYPE or NOBLE_ERR_BAD_ACTIVATION;
+ * makes no HIP call.  The sizes do not depend on the activation. */
 noble_status noble_linear_workspace_size(const noble_linear_desc* desc,
                                          size_t* reserve_bytes,
                                          size_t* scratch_bytes);
@@ -94,7 +117,9 @@ noble_status noble_linear_workspace_size(const noble_linear_desc* desc,
  *          W_down [d_in, r], omega1/phi1/omega2/phi2 [r] f32, M [r, r],
  *          W_up [r, d_out].
  * Outputs: y [T, d_out]; reserve (>= reserve_bytes) receives H for the
- *          backward.  scratch must hold scratch_bytes. */
+ *          backward.  scratch must hold scratch_bytes.
+ * With a one-application activation, M, omega2 and phi2 are not read and
+ * may be NULL. */
 noble_status noble_linear_fwd(const noble_linear_desc* desc,
                               const void* x, const void* W, const float* b,
                               const void* W_down,
@@ -116,7 +141,9 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc,
  * omega / phi gradients are summed over tokens with float atomics, so they
  * may differ in the last bits between runs; the matrix gradients are
  * reproducible.  scratch (>= scratch_bytes) may be NULL only when
- * scratch_bytes is 0 or T is 0. */
+ * scratch_bytes is 0 or T is 0.  With a one-application activation, M,
+ * omega2 and phi2 are not read, and dM, domega2, dphi2 may be NULL; when
+ * given they are set to zero (the function does not depend on them). */
 noble_status noble_linear_bwd(const noble_linear_desc* desc,
                               const void* dy, const void* x, const void* W,
                               const void* W_down,
@@ -138,7 +165,7 @@ const char* noble_status_string(int status);
 /* ABI version of this header (bumped on incompatible changes). */
 int noble_abi_version(void);
 
-#define NOBLE_ABI_VERSION 1
+#define NOBLE_ABI_VERSION 2
 
 #ifdef __cplusplus
 }

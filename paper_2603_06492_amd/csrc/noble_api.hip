@@ -29,6 +29,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 noble_status check_desc(const noble_linear_desc* d) {
     if (!d) return NOBLE_ERR_NULL_ARG;
     if (d->dtype != NOBLE_BF16 && d->dtype != NOBLE_F32) return NOBLE_ERR_BAD_DTYPE;
+    if (d->activation < NOBLE_ACT_COSNET || d->activation > NOBLE_ACT_GELU_M) return NOBLE_ERR_BAD_ACTIVATION;
     if (d->T < 0 || d->T > kMaxTokens) return NOBLE_ERR_BAD_SHAPE;
     if (d->d_in < 8 || d->d_in % 8 || d->d_in > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
     if (d->d_out < 8 || d->d_out % 8 || d->d_out > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
@@ -37,6 +38,38 @@ noble_status check_desc(const noble_linear_desc* d) {
 }
 
 size_t elt_size(const noble_linear_desc* d) { return d->dtype == NOBLE_BF16 ? 2 : 4; }
+
+// Function and number of applications of a noble_activation.
+Act act_fn(int a) {
+    switch (a) {
+        case NOBLE_ACT_TANH:
+        case NOBLE_ACT_TANH_M: return Act::Tanh;
+        case NOBLE_ACT_LEAKY_RELU:
+        case NOBLE_ACT_LEAKY_RELU_M: return Act::Leaky;
+        case NOBLE_ACT_GELU:
+        case NOBLE_ACT_GELU_M: return Act::Gelu;
+        default: return Act::Cos;
+    }
+}
+bool act_two_layers(int a) {
+    return a == NOBLE_ACT_COSNET || a == NOBLE_ACT_TANH_M || a == NOBLE_ACT_LEAKY_RELU_M || a == NOBLE_ACT_GELU_M;
+}
+
+// Calls fn.template operator()<F, L2>() for the activation `a`.
+template <typename Fn>
+noble_status with_act(int a, Fn&& fn) {
+    const bool l2 = act_two_layers(a);
+    switch (act_fn(a)) {
+        case Act::Cos: return l2 ? fn.template operator()<Act::Cos, true>() : fn.template operator()<Act::Cos, false>();
+        case Act::Tanh:
+            return l2 ? fn.template operator()<Act::Tanh, true>() : fn.template operator()<Act::Tanh, false>();
+        case Act::Leaky:
+            return l2 ? fn.template operator()<Act::Leaky, true>() : fn.template operator()<Act::Leaky, false>();
+        case Act::Gelu:
+            return l2 ? fn.template operator()<Act::Gelu, true>() : fn.template operator()<Act::Gelu, false>();
+    }
+    return NOBLE_ERR_BAD_ACTIVATION;
+}
 
 // Pieces of K for the bf16 rank projection [T, K] x [K, r]: enough
 // workgroups of 128 tokens to cover the CUs, at least kPjMinChunks K chunks
@@ -230,27 +263,23 @@ noble_status launch_gemm(const Batch& bt, hipStream_t st, bool plain = false) {
 }
 
 // float32 path: chain kernels with their own rank projection.
-template <typename E>
-noble_status launch_chain(bool fwd, int RP, const ChainArgs& a, int T, hipStream_t st) {
+noble_status launch_chain(bool fwd, int RP, int act, const ChainArgs& a, int T, hipStream_t st) {
     const dim3 grid(cdiv(T, kChainRows)), block(kThreads);
-#define NOBLE_CHAIN(RPV)                                                          \
-    if (RP == RPV) {                                                              \
-        if (fwd)                                                                  \
-            hipLaunchKernelGGL((fwd_chain_kernel<E, RPV>), grid, block, 0, st, a); \
-        else                                                                      \
-            hipLaunchKernelGGL((bwd_chain_kernel<E, RPV>), grid, block, 0, st, a); \
-        return last_launch();                                                     \
+    return with_act(act, [&]<Act F, bool L2>() -> noble_status {
+#define NOBLE_CHAIN(RPV)                                                                    \
+    if (RP == RPV) {                                                                        \
+        if (fwd)                                                                            \
+            hipLaunchKernelGGL((fwd_chain_kernel<float, RPV, F, L2>), grid, block, 0, st, a); \
+        else                                                                                \
+            hipLaunchKernelGGL((bwd_chain_kernel<float, RPV, F, L2>), grid, block, 0, st, a); \
+        return last_launch();                                                               \
     }
-    if constexpr (sizeof(E) == 4) {
         NOBLE_CHAIN(32)
         NOBLE_CHAIN(64)
         NOBLE_CHAIN(128)
-    } else {
-        NOBLE_CHAIN(64)
-        NOBLE_CHAIN(128)
-    }
 #undef NOBLE_CHAIN
-    return NOBLE_ERR_BAD_SHAPE;
+        return NOBLE_ERR_BAD_SHAPE;
+    });
 }
 
 // bf16 path, step 1: split-K rank projection of c.A against c.B into the
@@ -275,9 +304,9 @@ noble_status launch_proj(bool fwd, const ChainArgs& c, float* P, int S, hipStrea
     return last_launch();
 }
 
-// bf16 path, step 2: CosNet chain (forward or backward) from the summed
-// partials.
-noble_status launch_branch(bool fwd, const ChainArgs& c, const float* P, int S, hipStream_t st) {
+// bf16 path, step 2: the branch nonlinearity (forward or backward) from the
+// summed partials.
+noble_status launch_branch(bool fwd, int act, const ChainArgs& c, const float* P, int S, hipStream_t st) {
     BranchArgs a{};
     a.P = P;
     a.pstride = (int64_t)c.T * c.r;
@@ -299,11 +328,13 @@ noble_status launch_branch(bool fwd, const ChainArgs& c, const float* P, int S, 
     a.T = c.T;
     a.r = c.r;
     const dim3 grid(cdiv(c.T, kSkRows)), block(kThreads);
-    if (fwd)
-        hipLaunchKernelGGL(branch_fwd_kernel, grid, block, 0, st, a);
-    else
-        hipLaunchKernelGGL(branch_bwd_kernel, grid, block, 0, st, a);
-    return last_launch();
+    return with_act(act, [&]<Act F, bool L2>() -> noble_status {
+        if (fwd)
+            hipLaunchKernelGGL((branch_fwd_kernel<F, L2>), grid, block, 0, st, a);
+        else
+            hipLaunchKernelGGL((branch_bwd_kernel<F, L2>), grid, block, 0, st, a);
+        return last_launch();
+    });
 }
 
 // K chunk of the large products (128 bytes of a row: 64 bf16 or 32 f32).
@@ -312,11 +343,11 @@ constexpr int gemm_bk() {
     return Elt<E>::BK;
 }
 
-// Padded rank of the chain kernels: a multiple of the K chunk, instantiated
-// for 64 and 128 (bf16) and 32, 64 and 128 (f32).
+// Padded rank of the float32 chain kernels: a multiple of the K chunk,
+// instantiated for 32, 64 and 128.
 template <typename E>
 int chain_rp(int64_t r) {
-    if (sizeof(E) == 4 && r <= 32) return 32;
+    if (r <= 32) return 32;
     return r <= 64 ? 64 : 128;
 }
 
@@ -345,9 +376,9 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
             float* P = reinterpret_cast<float*>(static_cast<char*>(scratch) + 4 * scratch_region(d));
             const int S = proj_split(T, din);
             NOBLE_TRY(launch_proj(true, a, P, S, st));
-            NOBLE_TRY(launch_branch(true, a, P, S, st));
+            NOBLE_TRY(launch_branch(true, d->activation, a, P, S, st));
         } else
-            NOBLE_TRY(launch_chain<E>(true, chain_rp<E>(r), a, (int)T, st));
+            NOBLE_TRY(launch_chain(true, chain_rp<E>(r), d->activation, a, (int)T, st));
     }
     // y = [x | C2] [W ; W_up] + b
     constexpr int GBK = gemm_bk<E>();
@@ -376,7 +407,8 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     // dW is overwritten by its product (or by the sum of its split-K
     // partials); db, dW_down, dW_up, dM and the dw / dp vectors are
     // accumulated atomically and start from zero.  T = 0 zeroes every
-    // gradient.
+    // gradient; so does a one-application activation for the unused dM, dw2
+    // and dp2 (when given).
     constexpr int GBK = gemm_bk<E>();
     const int nkT = cdiv(T, GBK);
     const WgradPlan wp = plan_wgrad(T, din, dout, GBK);
@@ -434,9 +466,9 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             float* P = reinterpret_cast<float*>(base + 4 * reg);
             const int S = proj_split(T, dout);
             NOBLE_TRY(launch_proj(false, a, P, S, st, &z));
-            NOBLE_TRY(launch_branch(false, a, P, S, st));
+            NOBLE_TRY(launch_branch(false, d->activation, a, P, S, st));
         } else
-            NOBLE_TRY(launch_chain<E>(false, chain_rp<E>(r), a, (int)T, st));
+            NOBLE_TRY(launch_chain(false, chain_rp<E>(r), d->activation, a, (int)T, st));
     }
 
     // dx = [dy | dH] [W^T ; W_down^T]   (B(k, n) stored [n][k]: K-major)
@@ -468,7 +500,8 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
                    choose_split_atomic(cdiv(din, kBM), nkT));
             bt.add(C2T, dyN, (int)r, (int)dout, nkT, dWu, dout, true, nullptr, nullptr,
                    choose_split_atomic(cdiv(dout, kBN), nkT));
-            bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM, r, true, nullptr, nullptr, choose_split_atomic(1, nkT));
+            if (act_two_layers(d->activation))
+                bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM, r, true, nullptr, nullptr, choose_split_atomic(1, nkT));
         }
         NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
         if (wp.split > 1) {
@@ -501,6 +534,7 @@ const char* noble_status_string(int status) {
         case NOBLE_ERR_WORKSPACE_TOO_SMALL: return "NOBLE_ERR_WORKSPACE_TOO_SMALL: scratch buffer too small";
         case NOBLE_ERR_UNSUPPORTED_DEVICE: return "NOBLE_ERR_UNSUPPORTED_DEVICE: current device is not gfx950";
         case NOBLE_ERR_HIP: return "NOBLE_ERR_HIP: a HIP runtime call or kernel launch failed";
+        case NOBLE_ERR_BAD_ACTIVATION: return "NOBLE_ERR_BAD_ACTIVATION: activation is not a noble_activation";
         default: return "NOBLE_ERR_UNKNOWN: not a noble_status value";
     }
 }
@@ -524,12 +558,13 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, cons
     NOBLE_TRY(optional(b));
     NOBLE_TRY(need(y, rows));
     if (br) {
+        const bool l2 = act_two_layers(desc->activation);
         NOBLE_TRY(need(W_down, true));
         NOBLE_TRY(need(omega1, true));
         NOBLE_TRY(need(phi1, true));
-        NOBLE_TRY(need(M, true));
-        NOBLE_TRY(need(omega2, true));
-        NOBLE_TRY(need(phi2, true));
+        NOBLE_TRY(l2 ? need(M, true) : optional(M));
+        NOBLE_TRY(l2 ? need(omega2, true) : optional(omega2));
+        NOBLE_TRY(l2 ? need(phi2, true) : optional(phi2));
         NOBLE_TRY(need(W_up, true));
         NOBLE_TRY(need(reserve, rows));
         NOBLE_TRY(need(scratch, rows));
@@ -558,21 +593,22 @@ noble_status noble_linear_bwd(const noble_linear_desc* desc, const void* dy, con
     NOBLE_TRY(need(dW, true));
     NOBLE_TRY(optional(db));
     if (br) {
+        const bool l2 = act_two_layers(desc->activation);
         NOBLE_TRY(need(W_down, true));
         NOBLE_TRY(need(omega1, true));
         NOBLE_TRY(need(phi1, true));
-        NOBLE_TRY(need(M, true));
-        NOBLE_TRY(need(omega2, true));
-        NOBLE_TRY(need(phi2, true));
+        NOBLE_TRY(l2 ? need(M, true) : optional(M));
+        NOBLE_TRY(l2 ? need(omega2, true) : optional(omega2));
+        NOBLE_TRY(l2 ? need(phi2, true) : optional(phi2));
         NOBLE_TRY(need(W_up, true));
         NOBLE_TRY(need(reserve, rows));
         NOBLE_TRY(need(dW_down, true));
-        NOBLE_TRY(need(dM, true));
+        NOBLE_TRY(l2 ? need(dM, true) : optional(dM));
         NOBLE_TRY(need(dW_up, true));
         NOBLE_TRY(need(domega1, true));
         NOBLE_TRY(need(dphi1, true));
-        NOBLE_TRY(need(domega2, true));
-        NOBLE_TRY(need(dphi2, true));
+        NOBLE_TRY(l2 ? need(domega2, true) : optional(domega2));
+        NOBLE_TRY(l2 ? need(dphi2, true) : optional(dphi2));
     }
     if (scratch_need(desc) > 0) {
         NOBLE_TRY(need(scratch, rows));

@@ -18,8 +18,12 @@
 //                      dM = C1^T dH2 as one grouped launch with split-K over
 //                      tokens; db = column sums of dy, taken from the dy tiles
 //                      the dW problem already stages.
+// The chain kernels are instantiated per bottleneck activation (cos, tanh,
+// LeakyReLU, GELU) and for the one-application form C2 = f(H w1 + p1), which
+// has no M and therefore no mixing products and no dM.
 #pragma once
 
+#include "noble_act.hpp"
 #include "noble_gemm.hpp"
 #include "noble_tiles.hpp"
 
@@ -148,7 +152,9 @@ __device__ __forceinline__ float wave_colsum(float x) {
     return x;
 }
 
-template <typename E, int RP>
+// Forward chain for activation F; L2 = two applications with M between them
+// (CosNet for F = Cos), otherwise C2 = f(H w1 + p1) and M, w2, p2 are unused.
+template <typename E, int RP, Act F, bool L2>
 __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
     using S = ChainShape<E, RP>;
     constexpr int TN = S::TN;
@@ -166,9 +172,10 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
 
     char* Cb = lds;
     char* Mb = lds + S::NKB * kChainRows * kRowBytes;
-    stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
+    if constexpr (L2) stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
 
-    // H -> reserve; C1 = cos(H w1 + p1) -> LDS (A operand of the mixing)
+    // H -> reserve; C1 = f(H w1 + p1) -> LDS (A operand of the mixing), or
+    // straight to C2 for one application
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int col = wn0 + 16 * j + r16;
@@ -179,10 +186,14 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
             const int row = wm0 + 4 * g + v, grow = m0 + row;
             const float h = acc[0][j][v];
             if (cv && grow < a.T) a.H[(int64_t)grow * r + col] = h;
-            const float c1 = cv ? cosf(h * w + p) : 0.f;
-            *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = to_elt<E>(c1);
+            const float c1 = cv ? act_value<F, false>(h * w + p) : 0.f;
+            if constexpr (L2)
+                *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = to_elt<E>(c1);
+            else if (cv && grow < a.T)
+                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = to_elt<E>(c1);
         }
     }
+    if constexpr (!L2) return;
     __syncthreads();
 
     f32x4 mix[1][TN];
@@ -192,7 +203,7 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
     for (int kb = 0; kb < S::NKB; ++kb)
         mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, mix);
 
-    // C2 = cos(H2 w2 + p2) -> scratch
+    // C2 = f(H2 w2 + p2) -> scratch
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int col = wn0 + 16 * j + r16;
@@ -202,12 +213,15 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
         for (int v = 0; v < 4; ++v) {
             const int grow = m0 + wm0 + 4 * g + v;
             if (grow < a.T)
-                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = to_elt<E>(cosf(mix[0][j][v] * w + p));
+                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] =
+                    to_elt<E>(act_value<F, false>(mix[0][j][v] * w + p));
         }
     }
 }
 
-template <typename E, int RP>
+// Backward chain, same forms as fwd_chain_kernel.  The one-application form
+// writes C2 and dH only.
+template <typename E, int RP, Act F, bool L2>
 __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
     using S = ChainShape<E, RP>;
     constexpr int TN = S::TN;
@@ -226,10 +240,11 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
 
     char* Cb = lds;
     char* Mb = lds + S::NKB * kChainRows * kRowBytes;
-    stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
+    if constexpr (L2) stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
 
-    // Recompute A1 = H w1 + p1, C1 = cos A1 (-> LDS and scratch), keep H, sin A1.
-    float hr[TN][4], s1[TN][4];
+    // Recompute A1 = H w1 + p1 and C1 = f(A1) (-> LDS and scratch, or to C2
+    // for one application); keep H and f'(A1).
+    float hr[TN][4], d1[TN][4];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int col = wn0 + 16 * j + r16;
@@ -240,70 +255,80 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
             const int row = wm0 + 4 * g + v, grow = m0 + row;
             const bool ok = cv && grow < a.T;
             const float h = ok ? a.H[(int64_t)grow * r + col] : 0.f;
-            float sn = 0.f, cs = 0.f;
-            if (cv) sincosf(h * w + p, &sn, &cs);
+            float f = 0.f, d = 0.f;
+            if (cv) act_value_slope<F, false>(h * w + p, f, d);
             hr[j][v] = h;
-            s1[j][v] = sn;
-            const E c1 = to_elt<E>(cs);
-            *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = c1;
-            if (ok) reinterpret_cast<E*>(a.C1s)[(int64_t)grow * r + col] = c1;
-        }
-    }
-    __syncthreads();
-
-    // H2 = C1 M
-    f32x4 h2[1][TN];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) h2[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < S::NKB; ++kb)
-        mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, h2);
-    __syncthreads();  // every wave is done with C1 and M in LDS
-
-    stage_mix_matrix<E, RP, true>(a.M, r, Mb, tid);
-
-    // A2 = H2 w2 + p2; C2 = cos A2 -> scratch; dA2 = -sin(A2) dC2;
-    // dw2 += dA2 H2, dp2 += dA2; dH2 = dA2 w2 -> LDS and scratch.
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int col = wn0 + 16 * j + r16;
-        const bool cv = col < r;
-        const float w = cv ? a.w2[col] : 0.f, p = cv ? a.p2[col] : 0.f;
-        float sw = 0.f, sp = 0.f;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int row = wm0 + 4 * g + v, grow = m0 + row;
-            const bool ok = cv && grow < a.T;
-            float sn = 0.f, cs = 0.f;
-            if (cv) sincosf(h2[0][j][v] * w + p, &sn, &cs);
-            const float da2 = ok ? -sn * dc2[0][j][v] : 0.f;
-            sw += da2 * h2[0][j][v];
-            sp += da2;
-            const E dh2 = to_elt<E>(da2 * w);
-            *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = dh2;
-            if (ok) {
-                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = to_elt<E>(cs);
-                reinterpret_cast<E*>(a.dH2s)[(int64_t)grow * r + col] = dh2;
+            d1[j][v] = d;
+            const E c1 = to_elt<E>(f);
+            if constexpr (L2) {
+                *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = c1;
+                if (ok) reinterpret_cast<E*>(a.C1s)[(int64_t)grow * r + col] = c1;
+            } else if (ok) {
+                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = c1;
             }
         }
-        sw = wave_colsum(sw);
-        sp = wave_colsum(sp);
-        if (g == 0 && cv) {
-            unsafeAtomicAdd(a.dw2 + col, sw);
-            unsafeAtomicAdd(a.dp2 + col, sp);
-        }
     }
-    __syncthreads();
 
-    // dC1 = dH2 M^T
+    // dC1: dC2 itself (one application) or dH2 M^T (two)
     f32x4 dc1[1][TN];
+    if constexpr (!L2) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) dc1[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < S::NKB; ++kb)
-        mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, dc1);
+        for (int j = 0; j < TN; ++j) dc1[0][j] = dc2[0][j];
+    } else {
+        __syncthreads();
 
-    // dA1 = -sin(A1) dC1; dw1 += dA1 H, dp1 += dA1; dH = dA1 w1 -> scratch
+        // H2 = C1 M
+        f32x4 h2[1][TN];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) h2[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < S::NKB; ++kb)
+            mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, h2);
+        __syncthreads();  // every wave is done with C1 and M in LDS
+
+        stage_mix_matrix<E, RP, true>(a.M, r, Mb, tid);
+
+        // A2 = H2 w2 + p2; C2 = f(A2) -> scratch; dA2 = f'(A2) dC2;
+        // dw2 += dA2 H2, dp2 += dA2; dH2 = dA2 w2 -> LDS and scratch.
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = wn0 + 16 * j + r16;
+            const bool cv = col < r;
+            const float w = cv ? a.w2[col] : 0.f, p = cv ? a.p2[col] : 0.f;
+            float sw = 0.f, sp = 0.f;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = wm0 + 4 * g + v, grow = m0 + row;
+                const bool ok = cv && grow < a.T;
+                float f = 0.f, d = 0.f;
+                if (cv) act_value_slope<F, false>(h2[0][j][v] * w + p, f, d);
+                const float da2 = ok ? d * dc2[0][j][v] : 0.f;
+                sw += da2 * h2[0][j][v];
+                sp += da2;
+                const E dh2 = to_elt<E>(da2 * w);
+                *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = dh2;
+                if (ok) {
+                    reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = to_elt<E>(f);
+                    reinterpret_cast<E*>(a.dH2s)[(int64_t)grow * r + col] = dh2;
+                }
+            }
+            sw = wave_colsum(sw);
+            sp = wave_colsum(sp);
+            if (g == 0 && cv) {
+                unsafeAtomicAdd(a.dw2 + col, sw);
+                unsafeAtomicAdd(a.dp2 + col, sp);
+            }
+        }
+        __syncthreads();
+
+#pragma unroll
+        for (int j = 0; j < TN; ++j) dc1[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < S::NKB; ++kb)
+            mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, dc1);
+    }
+
+    // dA1 = f'(A1) dC1; dw1 += dA1 H, dp1 += dA1; dH = dA1 w1 -> scratch
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int col = wn0 + 16 * j + r16;
@@ -314,7 +339,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
         for (int v = 0; v < 4; ++v) {
             const int grow = m0 + wm0 + 4 * g + v;
             const bool ok = cv && grow < a.T;
-            const float da1 = ok ? -s1[j][v] * dc1[0][j][v] : 0.f;
+            const float da1 = ok ? d1[j][v] * dc1[0][j][v] : 0.f;
             sw += da1 * hr[j][v];
             sp += da1;
             if (ok) reinterpret_cast<E*>(a.dHs)[(int64_t)grow * r + col] = to_elt<E>(da1 * w);

@@ -18,6 +18,10 @@
 //                       (bf16 scratch, operands of the weight-gradient products)
 //                       and reduces dw1, dp1, dw2, dp2 over its tokens with wave
 //                       shuffles, then one float atomic per column.
+//   Both chain kernels also take the other bottleneck activations (tanh,
+//   LeakyReLU, GELU in place of cos; see noble_act.hpp) and the
+//   one-application form C2 = f(H w1 + p1), which skips M and the second
+//   frequency/phase pair.
 //
 // The chain kernels run 32 tokens x 128 ranks per workgroup, four waves each
 // owning 32 rank columns.  M [r, r] is loaded into LDS once per workgroup in
@@ -75,21 +79,6 @@ struct BranchArgs {
     float* dp2;
     int T, r, S, pad_;
 };
-
-// sin and cos of x: reduction to one period in turns (x / 2 pi minus the
-// nearest integer), then the hardware v_sin_f32 / v_cos_f32, which take their
-// argument in turns.  Absolute error about 1e-6 for |x| in the range the
-// layer produces, far below the bf16 operand rounding that follows.
-__device__ __forceinline__ float turns(float x) {
-    const float t = x * 0.15915494309189535f;
-    return t - __builtin_rintf(t);
-}
-__device__ __forceinline__ float fast_cos(float x) { return __builtin_amdgcn_cosf(turns(x)); }
-__device__ __forceinline__ void fast_sincos(float x, float& s, float& c) {
-    const float t = turns(x);
-    s = __builtin_amdgcn_sinf(t);
-    c = __builtin_amdgcn_cosf(t);
-}
 
 // One 64-element K chunk of the projection operands: 4 DMA instructions per
 // wave (two for A, two for B).
@@ -323,6 +312,9 @@ __device__ __forceinline__ float block_colsum(const float (&x)[16]) {
     return s + __shfl_xor(s, 32);
 }
 
+// Forward chain.  L2: the two-application form with M (CosNet for F = Cos);
+// otherwise C2 = f(H w1 + p1) and M, w2, p2 are not read.
+template <Act F, bool L2>
 __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds[kSkLds];
     char* mt = lds;
@@ -332,7 +324,7 @@ __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
     const int row0 = blockIdx.x * kSkRows;
     const int r = a.r;
 
-    m_dma(a.M, r, mt, wave, lane);   // lands while the partials are summed
+    if constexpr (L2) m_dma(a.M, r, mt, wave, lane);   // lands while the partials are summed
     // acc[v]: token row0 + 8(v/4) + 4h + v%4, rank column 32 wave + r32
     const int col = 32 * wave + r32;
     f32x16 acc;
@@ -340,34 +332,43 @@ __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
 
     const bool cv = col < r;
     const float w1 = cv ? a.w1[col] : 0.f, p1 = cv ? a.p1[col] : 0.f;
-    const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
     const __amdgpu_buffer_rsrc_t rh =
         make_rsrc(reinterpret_cast<const char*>(a.H) + (int64_t)row0 * r * 4, (int64_t)(a.T - row0) * r * 4);
     const __amdgpu_buffer_rsrc_t rc =
         make_rsrc(reinterpret_cast<const char*>(a.C2s) + (int64_t)row0 * r * 2, (int64_t)(a.T - row0) * r * 2);
     const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
     const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * r + col) * 2) : kOOB;
+    auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * r * es); };
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4,
-                                              (uint32_t)((8 * (v >> 2) + (v & 3)) * r * 4), 0);
-        const float c1 = cv ? fast_cos(acc[v] * w1 + p1) : 0.f;
-        *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = (uint16_t)f2bf(c1);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), 0);
+        const float c1 = cv ? act_value<F, true>(acc[v] * w1 + p1) : 0.f;
+        if constexpr (L2) {
+            const int row = 8 * (v >> 2) + 4 * h + (v & 3);
+            *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = (uint16_t)f2bf(c1);
+        } else {
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(c1), rc, vo2, soff(v, 2), 0);
+        }
     }
-    wait_vmcnt<0>();   // this wave's part of M has landed
-    __syncthreads();   // C1 tile and M complete
+    if constexpr (L2) {
+        const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
+        wait_vmcnt<0>();   // this wave's part of M has landed
+        __syncthreads();   // C1 tile and M complete
 
-    f32x16 h2;
+        f32x16 h2;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) h2[v] = 0.f;
-    mix_mma<false>(ct, mt, wave, lane, h2);
+        for (int v = 0; v < 16; ++v) h2[v] = 0.f;
+        mix_mma<false>(ct, mt, wave, lane, h2);
 #pragma unroll
-    for (int v = 0; v < 16; ++v)
-        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(fast_cos(h2[v] * w2 + p2)), rc, vo2,
-                                              (uint32_t)((8 * (v >> 2) + (v & 3)) * r * 2), 0);
+        for (int v = 0; v < 16; ++v)
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(act_value<F, true>(h2[v] * w2 + p2)), rc, vo2,
+                                                  soff(v, 2), 0);
+    }
 }
 
+// Backward chain, same forms as branch_fwd_kernel.  The one-application form
+// writes C2 and dH only (no C1, dH2 and no second frequency/phase).
+template <Act F, bool L2>
 __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds[kSkLds];
     char* mt = lds;
@@ -377,87 +378,104 @@ __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
     const int row0 = blockIdx.x * kSkRows;
     const int r = a.r;
 
-    m_dma(a.M, r, mt, wave, lane);
+    if constexpr (L2) m_dma(a.M, r, mt, wave, lane);
     const int col = 32 * wave + r32;
     f32x16 dc2;
     sum_partials(a, row0, col, h, dc2);   // dC2 = dy W_up^T
 
     const bool cv = col < r;
     const float w1 = cv ? a.w1[col] : 0.f, p1 = cv ? a.p1[col] : 0.f;
-    const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
     const int64_t rows_left = a.T - row0;
     const __amdgpu_buffer_rsrc_t rh =
         make_rsrc(reinterpret_cast<const char*>(a.H) + (int64_t)row0 * r * 4, rows_left * r * 4);
     auto rs16 = [&](uint16_t* base) {
         return make_rsrc(reinterpret_cast<const char*>(base) + (int64_t)row0 * r * 2, rows_left * r * 2);
     };
-    const __amdgpu_buffer_rsrc_t rc1 = rs16(a.C1s), rc2 = rs16(a.C2s), rdh2 = rs16(a.dH2s), rdh = rs16(a.dHs);
+    const __amdgpu_buffer_rsrc_t rc2 = rs16(a.C2s), rdh = rs16(a.dHs);
     const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
     const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * r + col) * 2) : kOOB;
     auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * r * es); };
 
-    // H from the reserve (rows past T and columns past r read as zero)
-    float hr[16], s1[16];
+    // H from the reserve (rows past T and columns past r read as zero);
+    // A1 = H w1 + p1, keep f'(A1)
+    float hr[16], d1[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v)
         hr[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rh, vo4, soff(v, 4), 0));
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
-        float sn = 0.f, cs = 0.f;
-        if (cv) fast_sincos(hr[v] * w1 + p1, sn, cs);
-        s1[v] = sn;
-        const uint16_t c1 = (uint16_t)f2bf(cs);
-        *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = c1;
-        __builtin_amdgcn_raw_buffer_store_b16(c1, rc1, vo2, soff(v, 2), 0);
-    }
-    wait_vmcnt<0>();   // this wave's part of M has landed
-    __syncthreads();   // C1 tile and M complete
 
-    f32x16 h2;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) h2[v] = 0.f;
-    mix_mma<false>(ct, mt, wave, lane, h2);   // H2 = C1 M
-    __syncthreads();                           // done reading C1 from LDS
-
-    float da2h2[16], da2[16];
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
-        const bool ok = cv && row < rows_left;
-        float sn = 0.f, cs = 0.f;
-        if (cv) fast_sincos(h2[v] * w2 + p2, sn, cs);
-        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(cs), rc2, vo2, soff(v, 2), 0);
-        const float d = ok ? -sn * dc2[v] : 0.f;   // dA2
-        da2[v] = d;
-        da2h2[v] = d * h2[v];
-        const uint16_t dh2 = (uint16_t)f2bf(d * w2);
-        *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = dh2;
-        __builtin_amdgcn_raw_buffer_store_b16(dh2, rdh2, vo2, soff(v, 2), 0);
-    }
-    {
-        const float sw = block_colsum(da2h2), sp = block_colsum(da2);
-        if (h == 0 && cv) {
-            unsafeAtomicAdd(a.dw2 + col, sw);
-            unsafeAtomicAdd(a.dp2 + col, sp);
-        }
-    }
-    __syncthreads();   // dH2 tile complete
-
+    // dC1: dC2 itself (one application) or dH2 M^T (two)
     f32x16 dc1;
+    if constexpr (!L2) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) dc1[v] = 0.f;
-    mix_mma<true>(ct, mt, wave, lane, dc1);   // dC1 = dH2 M^T
+        for (int v = 0; v < 16; ++v) {
+            float f = 0.f, d = 0.f;
+            if (cv) act_value_slope<F, true>(hr[v] * w1 + p1, f, d);
+            d1[v] = d;
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(f), rc2, vo2, soff(v, 2), 0);   // C2 = C1
+            dc1[v] = dc2[v];
+        }
+    } else {
+        const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
+        const __amdgpu_buffer_rsrc_t rc1 = rs16(a.C1s), rdh2 = rs16(a.dH2s);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int row = 8 * (v >> 2) + 4 * h + (v & 3);
+            float f = 0.f, d = 0.f;
+            if (cv) act_value_slope<F, true>(hr[v] * w1 + p1, f, d);
+            d1[v] = d;
+            const uint16_t c1 = (uint16_t)f2bf(f);
+            *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = c1;
+            __builtin_amdgcn_raw_buffer_store_b16(c1, rc1, vo2, soff(v, 2), 0);
+        }
+        wait_vmcnt<0>();   // this wave's part of M has landed
+        __syncthreads();   // C1 tile and M complete
 
+        f32x16 h2;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) h2[v] = 0.f;
+        mix_mma<false>(ct, mt, wave, lane, h2);   // H2 = C1 M
+        __syncthreads();                           // done reading C1 from LDS
+
+        // A2 = H2 w2 + p2, C2 = f(A2), dA2 = f'(A2) dC2, dH2 = dA2 w2
+        float da2h2[16], da2[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int row = 8 * (v >> 2) + 4 * h + (v & 3);
+            const bool ok = cv && row < rows_left;
+            float f = 0.f, d = 0.f;
+            if (cv) act_value_slope<F, true>(h2[v] * w2 + p2, f, d);
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(f), rc2, vo2, soff(v, 2), 0);
+            const float g = ok ? d * dc2[v] : 0.f;
+            da2[v] = g;
+            da2h2[v] = g * h2[v];
+            const uint16_t dh2 = (uint16_t)f2bf(g * w2);
+            *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = dh2;
+            __builtin_amdgcn_raw_buffer_store_b16(dh2, rdh2, vo2, soff(v, 2), 0);
+        }
+        {
+            const float sw = block_colsum(da2h2), sp = block_colsum(da2);
+            if (h == 0 && cv) {
+                unsafeAtomicAdd(a.dw2 + col, sw);
+                unsafeAtomicAdd(a.dp2 + col, sp);
+            }
+        }
+        __syncthreads();   // dH2 tile complete
+
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dc1[v] = 0.f;
+        mix_mma<true>(ct, mt, wave, lane, dc1);   // dC1 = dH2 M^T
+    }
+
+    // dA1 = f'(A1) dC1; dw1 += dA1 H, dp1 += dA1; dH = dA1 w1
     float da1h[16], da1[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
         const int row = 8 * (v >> 2) + 4 * h + (v & 3);
         const bool ok = cv && row < rows_left;
-        const float d = ok ? -s1[v] * dc1[v] : 0.f;   // dA1
-        da1[v] = d;
-        da1h[v] = d * hr[v];
-        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(d * w1), rdh, vo2, soff(v, 2), 0);
+        const float g = ok ? d1[v] * dc1[v] : 0.f;
+        da1[v] = g;
+        da1h[v] = g * hr[v];
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(g * w1), rdh, vo2, soff(v, 2), 0);
     }
     const float sw = block_colsum(da1h), sp = block_colsum(da1);
     if (h == 0 && cv) {

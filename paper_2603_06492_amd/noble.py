@@ -8,6 +8,9 @@ is not built, or the device is not gfx950, calls raise.
 Functions keep the C names: ``noble_linear_workspace_size``,
 ``noble_linear_fwd``, ``noble_linear_bwd``, ``noble_status_string``.
 ``NobleLinearFunction`` wraps the pair as a ``torch.autograd.Function``.
+
+``activation`` (keyword of the calls) is a noble_activation code or one of the
+names in ``ACTIVATIONS``; the default is the CosNet.
 """
 
 from __future__ import annotations
@@ -31,7 +34,36 @@ STATUS = {
     5: "NOBLE_ERR_WORKSPACE_TOO_SMALL",
     6: "NOBLE_ERR_UNSUPPORTED_DEVICE",
     7: "NOBLE_ERR_HIP",
+    8: "NOBLE_ERR_BAD_ACTIVATION",
 }
+
+# noble_activation codes by name.
+ACTIVATIONS = {
+    "cosnet": 0,
+    "cos": 1,
+    "tanh": 2,
+    "tanh_m": 3,
+    "leaky_relu": 4,
+    "leaky_relu_m": 5,
+    "gelu": 6,
+    "gelu_m": 7,
+}
+TWO_LAYER = {"cosnet", "tanh_m", "leaky_relu_m", "gelu_m"}
+
+
+def activation_code(activation) -> int:
+    """noble_activation code of a name (or of a code, returned as is)."""
+    if isinstance(activation, str):
+        if activation not in ACTIVATIONS:
+            raise ValueError(f"unknown activation {activation!r}; expected one of {sorted(ACTIVATIONS)}")
+        return ACTIVATIONS[activation]
+    return int(activation)
+
+
+def two_layers(activation) -> bool:
+    """True for the forms with the mixing matrix M (CosNet and the _m names)."""
+    code = activation_code(activation)
+    return code in {ACTIVATIONS[n] for n in TWO_LAYER}
 
 
 class NobleError(RuntimeError):
@@ -47,7 +79,7 @@ class noble_linear_desc(ctypes.Structure):
         ("d_out", ctypes.c_int64),
         ("r", ctypes.c_int64),
         ("dtype", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("activation", ctypes.c_int32),
     ]
 
 
@@ -83,13 +115,14 @@ def noble_status_string(status: int) -> str:
     return lib().noble_status_string(int(status)).decode()
 
 
-def make_desc(T: int, d_in: int, d_out: int, r: int, dtype: int) -> noble_linear_desc:
-    return noble_linear_desc(int(T), int(d_in), int(d_out), int(r), int(dtype), 0)
+def make_desc(T: int, d_in: int, d_out: int, r: int, dtype: int, activation=0) -> noble_linear_desc:
+    return noble_linear_desc(int(T), int(d_in), int(d_out), int(r), int(dtype), activation_code(activation))
 
 
-def noble_linear_workspace_size(T: int, d_in: int, d_out: int, r: int, dtype: int) -> Tuple[int, int]:
+def noble_linear_workspace_size(T: int, d_in: int, d_out: int, r: int, dtype: int,
+                                activation=0) -> Tuple[int, int]:
     """(reserve_bytes, scratch_bytes) for the problem."""
-    d = make_desc(T, d_in, d_out, r, dtype)
+    d = make_desc(T, d_in, d_out, r, dtype, activation)
     res, scr = ctypes.c_size_t(0), ctypes.c_size_t(0)
     st = lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(res), ctypes.byref(scr))
     if st != 0:
@@ -137,13 +170,14 @@ def _stream(stream) -> Optional[int]:
 
 
 def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
-                     stream=None) -> None:
+                     stream=None, activation=0) -> None:
     """Enqueue the forward on ``stream`` (default: torch's current stream).
 
     Storage tensors (x, W, W_down, M, W_up, y) share one dtype (bf16 or f32);
     b, omega*, phi* are float32.  reserve/scratch are byte (uint8) tensors of
     at least the sizes from noble_linear_workspace_size.  With r = 0 pass None
-    for the branch tensors.
+    for the branch tensors; one-application activations do not read M,
+    omega2, phi2 (None allowed).
     """
     torch = _torch()
     T, d_in = x.shape
@@ -152,7 +186,7 @@ def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, re
     dt = _dtype_code(x)
     sd = x.dtype
     f32 = torch.float32
-    d = make_desc(T, d_in, d_out, r, dt)
+    d = make_desc(T, d_in, d_out, r, dt, activation)
     args = [
         _ptr(x, "x", sd, (T, d_in)), _ptr(W, "W", sd, (d_in, d_out)), _ptr(b, "b", f32, (d_out,)),
         _ptr(W_down, "W_down", sd, (d_in, r)), _ptr(omega1, "omega1", f32, (r,)), _ptr(phi1, "phi1", f32, (r,)),
@@ -168,11 +202,13 @@ def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, re
 
 def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve,
                      dx, dW, db, dW_down, dM, dW_up, domega1, dphi1, domega2, dphi2, scratch,
-                     stream=None) -> None:
+                     stream=None, activation=0) -> None:
     """Enqueue the backward on ``stream``; overwrites every gradient tensor.
 
     dx has the storage dtype; dW, db (optional), dW_down, dM, dW_up and the
-    four frequency/phase gradients are float32.
+    four frequency/phase gradients are float32.  One-application activations
+    accept None for M, omega2, phi2, dM, domega2 and dphi2 (given gradient
+    tensors are set to zero).
     """
     torch = _torch()
     T, d_in = x.shape
@@ -181,7 +217,7 @@ def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, rese
     dt = _dtype_code(x)
     sd = x.dtype
     f32 = torch.float32
-    d = make_desc(T, d_in, d_out, r, dt)
+    d = make_desc(T, d_in, d_out, r, dt, activation)
     args = [
         _ptr(dy, "dy", sd, (T, d_out)), _ptr(x, "x", sd, (T, d_in)), _ptr(W, "W", sd, (d_in, d_out)),
         _ptr(W_down, "W_down", sd, (d_in, r)), _ptr(omega1, "omega1", f32, (r,)), _ptr(phi1, "phi1", f32, (r,)),
@@ -214,20 +250,25 @@ def _make_function():
     torch = _torch()
 
     class NobleLinearFunction(torch.autograd.Function):
-        """y = x W + b + CosNet(x W_down) W_up with the libnoble kernels.
-
-        Parameter gradients are float32 (master-weight convention)."""
+        """y = x W + b + sigma(x W_down) W_up with the libnoble kernels, sigma
+        the CosNet or another bottleneck activation (``activation``, not
+        differentiated).  One-application activations take None for M,
+        omega2, phi2.  Parameter gradients are float32 (master-weight
+        convention)."""
 
         @staticmethod
-        def forward(ctx, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up):
+        def forward(ctx, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation=0):
             T, d_in = x.shape
             d_out, r = W.shape[1], W_down.shape[1]
             dt = _dtype_code(x)
+            act = activation_code(activation)
             reserve, scratch = alloc_workspace(T, d_in, d_out, r, dt, x.device)
             y = torch.empty((T, d_out), dtype=x.dtype, device=x.device)
-            noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch)
+            noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
+                             activation=act)
             ctx.save_for_backward(x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve)
             ctx.has_bias = b is not None
+            ctx.act = act
             return y
 
         @staticmethod
@@ -236,18 +277,22 @@ def _make_function():
             T, d_in = x.shape
             d_out, r = W.shape[1], W_down.shape[1]
             dev, f32 = x.device, torch.float32
+            two = two_layers(ctx.act)
             dy = dy.contiguous().to(x.dtype)
             _, scratch = alloc_workspace(T, d_in, d_out, r, _dtype_code(x), dev)
             dx = torch.empty_like(x)
             g = {n: torch.empty(s, dtype=f32, device=dev) for n, s in (
                 ("dW", (d_in, d_out)), ("db", (d_out,)), ("dW_down", (d_in, r)), ("dM", (r, r)),
                 ("dW_up", (r, d_out)), ("domega1", (r,)), ("dphi1", (r,)), ("domega2", (r,)), ("dphi2", (r,)))}
+            if not two:
+                g["dM"] = g["domega2"] = g["dphi2"] = None
             noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve,
                              dx, g["dW"], g["db"], g["dW_down"], g["dM"], g["dW_up"],
-                             g["domega1"], g["dphi1"], g["domega2"], g["dphi2"], scratch)
+                             g["domega1"], g["dphi1"], g["domega2"], g["dphi2"], scratch, activation=ctx.act)
+            dM = g["dM"].to(M.dtype) if two else None
             return (dx, g["dW"].to(W.dtype), g["db"] if ctx.has_bias else None, g["dW_down"].to(W_down.dtype),
-                    g["domega1"], g["dphi1"], g["dM"].to(M.dtype), g["domega2"], g["dphi2"],
-                    g["dW_up"].to(W_up.dtype))
+                    g["domega1"], g["dphi1"], dM, g["domega2"], g["dphi2"],
+                    g["dW_up"].to(W_up.dtype), None)
 
     return NobleLinearFunction
 

@@ -26,11 +26,15 @@ class DeviceProblem:
     ``canary=True`` surrounds every output with guard bands filled with a NaN
     pattern, so out-of-bounds writes can be detected with ``guards_intact``.
     ``branch=False`` runs the same shapes as a plain linear (r = 0).
+    ``activation`` names the bottleneck activation (noble.ACTIVATIONS).  For a
+    one-application activation, M, omega2, phi2 and their gradients are passed
+    as None unless ``pass_unused`` (then the gradients must come back zero).
     """
 
     def __init__(self, p: Projection, device: str = "cuda", *, with_bias: bool = True,
                  with_db: bool = True, branch: bool = True, canary: bool = False,
-                 inputs_from: Optional["DeviceProblem"] = None):
+                 inputs_from: Optional["DeviceProblem"] = None, activation: str = "cosnet",
+                 pass_unused: bool = False):
         torch = _torch()
         if not torch.cuda.is_available():
             raise RuntimeError("DeviceProblem needs a GPU")
@@ -40,6 +44,9 @@ class DeviceProblem:
         self.code = noble.NOBLE_BF16 if p.dtype == "bf16" else noble.NOBLE_F32
         self.r = p.r if branch else 0
         self.canary = canary
+        self.activation = activation
+        self.act = noble.activation_code(activation)
+        unused = () if noble.two_layers(activation) or pass_unused else ("M", "omega2", "phi2")
         self.guards = []
         self.t: Dict[str, object] = {}
         if inputs_from is not None:
@@ -56,6 +63,8 @@ class DeviceProblem:
         if self.r == 0:
             for k in ("W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up"):
                 self.t[k] = None
+        for k in unused:
+            self.t[k] = None
         T, di, do, r = p.T, p.d_in, p.d_out, self.r
         f32 = torch.float32
         self.y = self._out((T, do), self.sdt)
@@ -68,10 +77,12 @@ class DeviceProblem:
             for n, s in (("dW_down", (di, r)), ("dM", (r, r)), ("dW_up", (r, do)), ("domega1", (r,)),
                          ("dphi1", (r,)), ("domega2", (r,)), ("dphi2", (r,))):
                 self.g[n] = self._out(s, f32)
+            for n in unused:
+                self.g["d" + n] = None
         else:
             for n in ("dW_down", "dM", "dW_up", "domega1", "dphi1", "domega2", "dphi2"):
                 self.g[n] = None
-        res, scr = noble.noble_linear_workspace_size(T, di, do, r, self.code)
+        res, scr = noble.noble_linear_workspace_size(T, di, do, r, self.code, self.act)
         self.reserve = torch.empty(max(res, 16), dtype=torch.uint8, device=device)
         self.scratch = torch.empty(max(scr, 16), dtype=torch.uint8, device=device)
 
@@ -97,7 +108,7 @@ class DeviceProblem:
         t = self.t
         noble.noble_linear_fwd(t["x"], t["W"], t["b"], t["W_down"], t["omega1"], t["phi1"], t["M"],
                                t["omega2"], t["phi2"], t["W_up"], self.y, self.reserve, self.scratch,
-                               stream=stream)
+                               stream=stream, activation=self.act)
 
     def bwd(self, stream=None):
         t, g = self.t, self.g
@@ -105,7 +116,7 @@ class DeviceProblem:
                                t["omega2"], t["phi2"], t["W_up"], self.reserve,
                                g["dx"], g["dW"], g["db"], g["dW_down"], g["dM"], g["dW_up"],
                                g["domega1"], g["dphi1"], g["domega2"], g["dphi2"], self.scratch,
-                               stream=stream)
+                               stream=stream, activation=self.act)
 
     def outputs(self, rows: Optional[np.ndarray] = None, dw_rows: Optional[np.ndarray] = None):
         """Host float64 copies of y and every gradient (optionally row-sampled)."""

@@ -5,6 +5,7 @@ from __future__ import annotations
 import numpy as np
 
 import oracle
+from paper_2603_06492_amd import inputs as inp
 
 # max over rows of max_j |gpu - ref| / (max_j |ref| + 1e-6): bf16 operands with
 # float32 accumulation, and the float32 path
@@ -22,7 +23,14 @@ def row_err(gpu: np.ndarray, ref: np.ndarray) -> float:
     return float(np.max(np.max(np.abs(gpu - ref), axis=1) / denom))
 
 
-def oracle_outputs(p, *, with_bias=True, branch=True, rows=None, dw_rows=None):
+def round_bf16_f64(a):
+    """float64 -> float32 -> bf16 (round to nearest even) -> float64: the
+    rounding a bf16 kernel applies to a float32 value before an MFMA."""
+    return inp.round_bf16(np.asarray(a, dtype=np.float32)).astype(np.float64)
+
+
+def oracle_outputs(p, *, with_bias=True, branch=True, rows=None, dw_rows=None, activation="cosnet",
+                   mix_round=None):
     """fp64 oracle y and gradients for projection ``p`` (optionally row-sampled)."""
     a = p.arrays
     if branch:
@@ -34,12 +42,33 @@ def oracle_outputs(p, *, with_bias=True, branch=True, rows=None, dw_rows=None):
     b = a["b"] if with_bias else None
     x = a["x"] if rows is None else a["x"][rows]
     Y, _ = oracle.forward(x, a["W"], b, br["W_down"], br["omega1"], br["phi1"], br["M"],
-                          br["omega2"], br["phi2"], br["W_up"])
+                          br["omega2"], br["phi2"], br["W_up"], activation=activation, mix_round=mix_round)
     g = oracle.backward(a["dy"], a["x"], a["W"], br["W_down"], br["omega1"], br["phi1"], br["M"],
-                        br["omega2"], br["phi2"], br["W_up"], dx_rows=rows, dW_rows=dw_rows)
+                        br["omega2"], br["phi2"], br["W_up"], dx_rows=rows, dW_rows=dw_rows,
+                        activation=activation, mix_round=mix_round)
     g["y"] = Y
     return g
 
 
 def parity_report(gpu: dict, ref: dict, names=OUTPUTS) -> dict:
     return {n: row_err(gpu[n], ref[n]) for n in names if gpu.get(n) is not None and ref.get(n) is not None}
+
+
+def kink_margin(p, activation, mix_round=None, rel=1e-5):
+    """Smallest |A| / band over the pre-activations A1 (and A2) of the
+    LeakyReLU forms, band = rel * (|w| max_t |h| + |p|) per rank column (h the
+    column that w scales).  Below 1 an element sits where float32 and float64
+    can take different branches of the kink; a parity case needs > 1."""
+    a = {k: np.asarray(v, dtype=np.float64) for k, v in p.arrays.items()}
+    H = a["x"] @ a["W_down"]
+    fw = oracle.branch_forward(H, activation, a["omega1"], a["phi1"], a["M"], a["omega2"], a["phi2"],
+                               mix_round=mix_round)
+
+    def margin(A, h, w, ph):
+        band = rel * (np.abs(w) * np.max(np.abs(h), axis=0) + np.abs(ph))
+        return float(np.min(np.abs(A) / band))
+
+    m = margin(fw["A1"], H, a["omega1"], a["phi1"])
+    if "A2" in fw:
+        m = min(m, margin(fw["A2"], fw["H2"], a["omega2"], a["phi2"]))
+    return m

@@ -14,7 +14,7 @@ from paper_2603_06492_amd import noble
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "noble.h")
 
-OK, NULL, SHAPE, DTYPE, MISAL, WS = 0, 1, 2, 3, 4, 5
+OK, NULL, SHAPE, DTYPE, MISAL, WS, BADACT = 0, 1, 2, 3, 4, 5, 8
 
 # fake, 16-byte aligned addresses: never dereferenced because every call below
 # fails validation first
@@ -34,7 +34,7 @@ def test_library_exports_every_declared_function():
     L = noble.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.noble_abi_version() == 1
+    assert L.noble_abi_version() == 2
 
 
 def test_status_strings():
@@ -217,3 +217,82 @@ def test_plain_backward_needs_scratch_when_dW_splits():
     assert _bwd(d, ptrs, scr) == NULL
     ptrs[BWD_ARGS.index("scratch")] = FAKE[21]
     assert _bwd(d, ptrs, scr - 256) == WS
+
+
+# ----------------------------------------------------------- activations --
+
+def _header_enum(prefix):
+    src = open(HEADER).read()
+    return {m.group(1): int(m.group(2)) for m in re.finditer(prefix + r"([A-Z_0-9]+)\s*=\s*(\d+)", src)}
+
+
+def test_activation_codes_match_header_and_oracle():
+    """The binding's names and codes are the header's enum, and name the same
+    (f, applications) pairs as the oracle's activation table."""
+    import oracle
+    hdr = _header_enum("NOBLE_ACT_")
+    assert {k.lower(): v for k, v in hdr.items()} == noble.ACTIVATIONS
+    assert set(noble.ACTIVATIONS) == set(oracle.ACTIVATIONS)
+    for name, (_, layers) in oracle.ACTIVATIONS.items():
+        assert noble.two_layers(name) == (layers == 2), name
+    assert _header_enum("NOBLE_ERR_")["BAD_ACTIVATION"] == BADACT
+
+
+@pytest.mark.parametrize("act", [-1, 8, 1 << 20])
+def test_bad_activation_rejected(act):
+    d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_BF16, act)
+    a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert noble.lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(a), ctypes.byref(b)) == BADACT
+    assert _fwd(d, FAKE[:13], 1 << 30) == BADACT
+    assert _bwd(d, FAKE[:22], 1 << 30) == BADACT
+    with pytest.raises(ValueError):
+        noble.activation_code("relu")
+
+
+def test_workspace_does_not_depend_on_activation():
+    for dt in (noble.NOBLE_BF16, noble.NOBLE_F32):
+        sizes = {noble.noble_linear_workspace_size(300, 64, 1024, 40, dt, a) for a in noble.ACTIVATIONS}
+        assert len(sizes) == 1
+
+
+ONE = [a for a in noble.ACTIVATIONS if not noble.two_layers(a)]
+TWO = [a for a in noble.ACTIVATIONS if noble.two_layers(a)]
+
+
+@pytest.mark.parametrize("act", ONE)
+def test_one_layer_second_layer_pointers_optional(act):
+    """One application reads no M, omega2, phi2 and writes no dM, domega2,
+    dphi2: NULL passes their checks (a misaligned pointer checked after them
+    is what fails), a misaligned one is still rejected."""
+    d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_BF16, act)
+    _, scr = noble.noble_linear_workspace_size(64, 64, 64, 16, noble.NOBLE_BF16, act)
+    ptrs = list(FAKE[:13])
+    for k in ("M", "omega2", "phi2"):
+        ptrs[FWD_ARGS.index(k)] = None
+    ptrs[FWD_ARGS.index("reserve")] = FAKE[0] + 4
+    assert _fwd(d, ptrs, scr) == MISAL
+    ptrs[FWD_ARGS.index("reserve")] = FAKE[0]
+    ptrs[FWD_ARGS.index("M")] = FAKE[0] + 4
+    assert _fwd(d, ptrs, scr) == MISAL
+    ptrs = list(FAKE[:22])
+    for k in ("M", "omega2", "phi2", "dM", "domega2", "dphi2"):
+        ptrs[BWD_ARGS.index(k)] = None
+    ptrs[BWD_ARGS.index("scratch")] = FAKE[0] + 4
+    assert _bwd(d, ptrs, scr) == MISAL
+    ptrs[BWD_ARGS.index("scratch")] = FAKE[0]
+    ptrs[BWD_ARGS.index("dM")] = FAKE[0] + 8
+    assert _bwd(d, ptrs, scr) == MISAL
+
+
+@pytest.mark.parametrize("act", TWO)
+def test_two_layer_second_layer_pointers_required(act):
+    d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_F32, act)
+    _, scr = noble.noble_linear_workspace_size(64, 64, 64, 16, noble.NOBLE_F32, act)
+    for k in ("M", "omega2", "phi2"):
+        ptrs = list(FAKE[:13])
+        ptrs[FWD_ARGS.index(k)] = None
+        assert _fwd(d, ptrs, scr) == NULL, k
+    for k in ("M", "omega2", "phi2", "dM", "domega2", "dphi2"):
+        ptrs = list(FAKE[:22])
+        ptrs[BWD_ARGS.index(k)] = None
+        assert _bwd(d, ptrs, scr) == NULL, k

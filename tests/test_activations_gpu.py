@@ -1,0 +1,118 @@
+"""Parity of the bottleneck activation variants through the C ABI against the
+fp64 oracle: single cosine, tanh, LeakyReLU and GELU, each as one application
+and (except cosine, whose two-application form is the CosNet covered by
+test_parity_gpu.py) as two applications with the mixing matrix M.
+
+Same metric and bounds as test_parity_gpu.py.  On the bf16 path the
+two-application forms compute A2 from bf16-rounded C1 (the mixing product's
+MFMA operand, as bf16 mixed precision rounds it), so the oracle is run with
+the same operand rounding (mix_round) there.  Two variants need it:
+LeakyReLU's slope is a sign decision on A2 (without the rounding the oracle
+moves by up to 0.2 in dx), and GELU's relative slope grows like |a| for
+negative a, which amplifies the rounding in rank columns whose C2 is near zero
+(0.0215 in dW_up at r = 128 between the oracle with and without it).  Every
+seeded LeakyReLU case also keeps its pre-activations clear of the band where
+float32 and float64 can disagree on the sign (kink_margin > 1).
+"""
+
+import numpy as np
+import pytest
+
+from paper_2603_06492_amd import inputs as inp
+from paper_2603_06492_amd import noble
+
+from _parity import OUTPUTS, TOL, kink_margin, oracle_outputs, parity_report, round_bf16_f64
+
+pytestmark = pytest.mark.gpu
+
+VARIANTS = sorted(a for a in noble.ACTIVATIONS if a != "cosnet")
+CASES = [
+    # id, T, d_in, d_out, r, dtype, seed
+    ("bf16_ragged_r40", 300, 200, 264, 40, "bf16", 204),
+    ("bf16_r128_multitile", 777, 512, 384, 128, "bf16", 205),
+    ("f32_ragged_r24", 333, 96, 136, 24, "f32", 204),
+]
+SECOND = ("dM", "domega2", "dphi2")
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _run(p, act, **kw):
+    import torch
+    from paper_2603_06492_amd.runner import DeviceProblem
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    dp = DeviceProblem(p, canary=True, activation=act, **kw)
+    dp.fwd()
+    dp.bwd()
+    return dp
+
+
+def _mix_round(act, dt):
+    return round_bf16_f64 if dt == "bf16" and noble.two_layers(act) else None
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+@pytest.mark.parametrize("act", VARIANTS)
+def test_activation_parity(act, case):
+    name, T, di, do, r, dt, seed = case
+    _say(f"[activation] {act} {name}: T={T} d_in={di} d_out={do} r={r} {dt} seed={seed}")
+    p = inp.draw_projection(name, T, di, do, r, dt, seed=seed, bias_std=0.5)
+    mix = _mix_round(act, dt)
+    if act.startswith("leaky"):
+        m = kink_margin(p, act, mix)
+        assert m > 1.0, f"seeded case has a pre-activation inside the kink band (margin {m:.3f})"
+    dp = _run(p, act)
+    got = dp.outputs()
+    ref = oracle_outputs(p, activation=act, mix_round=mix)
+    rep = parity_report(got, ref)
+    _say(rep)
+    want = set(OUTPUTS) - (set() if noble.two_layers(act) else set(SECOND))
+    assert set(rep) == want
+    for k, e in rep.items():
+        assert e <= TOL[dt], (k, e)
+    assert dp.guards_intact(), "write outside an output buffer"
+
+
+@pytest.mark.parametrize("act", [a for a in VARIANTS if not noble.two_layers(a)])
+def test_one_layer_ignores_and_zeroes_second_layer(act):
+    """Passing M, omega2, phi2 changes nothing (bit for bit) and the given
+    dM, domega2, dphi2 buffers come back exactly zero."""
+    import torch
+    p = inp.draw_projection("one", 257, 128, 136, 32, "bf16", seed=206, bias_std=0.5)
+    _say(f"[activation] {act}: second-layer buffers")
+    a = _run(p, act)
+    b = _run(p, act, pass_unused=True)
+    torch.cuda.synchronize()
+    assert bool((a.y.view(torch.int16) == b.y.view(torch.int16)).all())
+    assert bool((a.g["dx"].view(torch.int16) == b.g["dx"].view(torch.int16)).all())
+    for n in ("dW", "dW_down", "dW_up"):
+        assert bool((a.g[n] == b.g[n]).all()), n
+    for n in SECOND:
+        assert a.g[n] is None
+        assert bool((b.g[n] == 0).all()), n
+    assert b.guards_intact()
+
+
+@pytest.mark.parametrize("act", ["gelu_m", "tanh"])
+def test_activation_full_size_block(act):
+    """One projection of the 1.5B block at full size (T = 8192, 2048 -> 2048,
+    r = 128) with a variant activation: sampled rows of y, dx, dW, every rank
+    gradient in full."""
+    p = inp.draw_workload_projection("llm1p5b_block_r128", 1)
+    _say(f"[activation] full {act} {p.name}: T={p.T} d_in={p.d_in} d_out={p.d_out} r={p.r}")
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([[0, 1, 255, 256, p.T - 1], rng.integers(0, p.T, 24)]))
+    dw_rows = np.unique(np.concatenate([[0, p.d_in - 1], rng.integers(0, p.d_in, 8)]))
+    mix = _mix_round(act, "bf16")
+    dp = _run(p, act)
+    got = dp.outputs(rows=rows, dw_rows=dw_rows)
+    ok = dp.guards_intact()
+    del dp
+    ref = oracle_outputs(p, rows=rows, dw_rows=dw_rows, activation=act, mix_round=mix)
+    rep = parity_report(got, ref)
+    _say(rep)
+    for k, e in rep.items():
+        assert e <= TOL["bf16"], (k, e)
+    assert ok
