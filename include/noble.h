@@ -118,6 +118,8 @@ noble_status noble_linear_workspace_size(const noble_linear_desc* desc,
  *          W_up [r, d_out].
  * Outputs: y [T, d_out]; reserve (>= reserve_bytes) receives H for the
  *          backward.  scratch must hold scratch_bytes.
+ * reserve may be NULL: an inference-only forward that keeps no H (the
+ * branch's permanent inference cost, Sec. 6); no backward can follow it.
  * With a one-application activation, M, omega2 and phi2 are not read and
  * may be NULL. */
 noble_status noble_linear_fwd(const noble_linear_desc* desc,
@@ -158,6 +160,67 @@ noble_status noble_linear_bwd(const noble_linear_desc* desc,
                               float* domega2, float* dphi2,
                               void* scratch, size_t scratch_bytes,
                               void* stream);
+
+/* ------------------------------------------------------------------------
+ * Training recipe around the layer (Sec. 3.3 "Key Design Choices", App. A
+ * "Hyperparameter Defaults").  Host-side values and one device fill; none
+ * of it is on the forward/backward path.
+ * ------------------------------------------------------------------------ */
+typedef struct noble_recipe {
+    double alpha;      /* W_up ~ N(0, (alpha / sqrt(r))^2); default 0.01 */
+    double w_scale;    /* W ~ N(0, (w_scale / sqrt(d_in))^2); default 0.5 */
+    double omega_min;  /* omega1, omega2 ~ U[omega_min, omega_max]; default 0.8 */
+    double omega_max;  /* default 1.2 */
+    double phi_std;    /* phi1, phi2 ~ N(0, phi_std^2); default 0.1 */
+    double gamma;      /* lr(W_up) = lr (min(d_in, d_out) / r)^(2 gamma); default 0.3 */
+    double gamma_M;    /* lr(M) = lr (min(d_in, d_out) / r)^gamma_M; default 0.45 */
+    double omega_lr;   /* learning-rate multiplier of omega1, omega2; default 3.0 */
+    double phi_lr;     /* learning-rate multiplier of phi1, phi2; default 5.0 */
+} noble_recipe;
+
+/* Fills *recipe with the defaults listed above (no-op for NULL). */
+void noble_recipe_defaults(noble_recipe* recipe);
+
+/* Learning-rate multipliers, relative to the base learning rate, of each
+ * parameter of one layer (Sec. 3.3 Eqs. 3-4): W, b and W_down take the base
+ * rate, W_up and M the elevated rates above, omega and phi the fixed
+ * multipliers.  With r = 0 only W and b are meaningful (the rest are 0). */
+typedef struct noble_lr_mults {
+    double W, b, W_down, W_up, M, omega, phi;
+} noble_lr_mults;
+
+/* Returns NOBLE_ERR_NULL_ARG (desc, recipe or out NULL), or the codes of
+ * noble_linear_workspace_size for a bad desc; makes no HIP call. */
+noble_status noble_lr_multipliers(const noble_linear_desc* desc,
+                                  const noble_recipe* recipe,
+                                  noble_lr_mults* out);
+
+/* Initialises the layer's parameters on the device (Sec. 3.3 and App. A):
+ *   W ~ N(0, (w_scale / sqrt(d_in))^2), b = 0,
+ *   W_down ~ U(-1/sqrt(d_in), 1/sqrt(d_in))  (the paper gives no W_down
+ *     init; this is the usual linear-layer default),
+ *   omega1, omega2 ~ U[omega_min, omega_max], phi1, phi2 ~ N(0, phi_std^2),
+ *   M ~ U(-sqrt(3 / r), sqrt(3 / r))  (Xavier uniform, fan_in = fan_out = r),
+ *   W_up ~ N(0, (alpha / sqrt(r))^2).
+ * Storage tensors (W, W_down, M, W_up) in desc->dtype, the rest float32;
+ * shapes as in noble_linear_fwd.  A NULL pointer skips that tensor.
+ * Random numbers: Philox4x32-10 (Salmon et al., SC 2011) keyed by `seed`
+ * (key = low, high 32 bits); element e (row-major) of tensor t takes the
+ * block at counter (e mod 2^32, e / 2^32, t, 0), t = 0 W, 1 W_down,
+ * 2 omega1, 3 phi1, 4 M, 5 omega2, 6 phi2, 7 W_up.  With words x0, x1 and
+ * u_i = (x_i + 1/2) 2^-32, a uniform draw on [lo, hi] is lo + (hi - lo) u0
+ * and a normal draw is sqrt(-2 ln u0) cos(2 pi u1), both in double, then
+ * rounded to float32 (and to bf16, nearest even, for bf16 storage).  The
+ * values do not depend on the launch, so a layer is reproducible from its
+ * seed.  Enqueued on `stream`; returns NOBLE_ERR_NULL_ARG (desc or recipe
+ * NULL), a desc error, NOBLE_ERR_MISALIGNED (a pointer not aligned to its
+ * element size) or NOBLE_ERR_HIP. */
+noble_status noble_init_params(const noble_linear_desc* desc,
+                               const noble_recipe* recipe, uint64_t seed,
+                               void* W, float* b, void* W_down,
+                               float* omega1, float* phi1, void* M,
+                               float* omega2, float* phi2, void* W_up,
+                               void* stream);
 
 /* Static, human-readable name of a status code (never NULL). */
 const char* noble_status_string(int status);

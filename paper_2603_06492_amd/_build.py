@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libnoble.so")
 SOURCES = ["noble_api.hip"]
-HEADERS = ["noble_act.hpp", "noble_kernels.hpp", "noble_tiles.hpp", "noble_gemm.hpp", "noble_gemm_dma.hpp", "noble_skinny.hpp"]
+HEADERS = ["noble_act.hpp", "noble_init.hpp", "noble_kernels.hpp", "noble_tiles.hpp", "noble_gemm.hpp", "noble_gemm_dma.hpp", "noble_skinny.hpp"]
 
 HIP_FLAGS = [
     "-O3",

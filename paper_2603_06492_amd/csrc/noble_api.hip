@@ -8,10 +8,12 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstring>
 
 #include "noble.h"
 #include "noble_gemm_dma.hpp"
+#include "noble_init.hpp"
 #include "noble_kernels.hpp"
 #include "noble_skinny.hpp"
 
@@ -566,7 +568,7 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, cons
         NOBLE_TRY(l2 ? need(omega2, true) : optional(omega2));
         NOBLE_TRY(l2 ? need(phi2, true) : optional(phi2));
         NOBLE_TRY(need(W_up, true));
-        NOBLE_TRY(need(reserve, rows));
+        NOBLE_TRY(optional(reserve));   // NULL: inference-only forward
         NOBLE_TRY(need(scratch, rows));
         if (scratch_bytes < scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
     }
@@ -621,6 +623,78 @@ noble_status noble_linear_bwd(const noble_linear_desc* desc, const void* dy, con
                                   dW_down, dM, dW_up, domega1, dphi1, domega2, dphi2, scratch, st);
     return bwd_impl<float>(desc, dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve, dx, dW, db, dW_down,
                            dM, dW_up, domega1, dphi1, domega2, dphi2, scratch, st);
+}
+
+void noble_recipe_defaults(noble_recipe* r) {
+    if (!r) return;
+    r->alpha = 0.01;
+    r->w_scale = 0.5;
+    r->omega_min = 0.8;
+    r->omega_max = 1.2;
+    r->phi_std = 0.1;
+    r->gamma = 0.3;
+    r->gamma_M = 0.45;
+    r->omega_lr = 3.0;
+    r->phi_lr = 5.0;
+}
+
+noble_status noble_lr_multipliers(const noble_linear_desc* desc, const noble_recipe* recipe, noble_lr_mults* out) {
+    if (!recipe || !out) return NOBLE_ERR_NULL_ARG;
+    NOBLE_TRY(check_desc(desc));
+    *out = noble_lr_mults{1.0, 1.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+    if (desc->r == 0) return NOBLE_OK;
+    // Sec. 3.3 Eqs. 3-4: the ratio of the smaller layer width to the rank,
+    // raised to 2 gamma (W_up) and gamma_M (M)
+    const double ratio = (double)std::min(desc->d_in, desc->d_out) / (double)desc->r;
+    out->W_down = 1.0;
+    out->W_up = std::pow(ratio, 2.0 * recipe->gamma);
+    out->M = std::pow(ratio, recipe->gamma_M);
+    out->omega = recipe->omega_lr;
+    out->phi = recipe->phi_lr;
+    return NOBLE_OK;
+}
+
+noble_status noble_init_params(const noble_linear_desc* desc, const noble_recipe* recipe, uint64_t seed, void* W,
+                               float* b, void* W_down, float* omega1, float* phi1, void* M, float* omega2,
+                               float* phi2, void* W_up, void* stream) {
+    if (!recipe) return NOBLE_ERR_NULL_ARG;
+    NOBLE_TRY(check_desc(desc));
+    const bool bf = desc->dtype == NOBLE_BF16;
+    const int64_t din = desc->d_in, dout = desc->d_out, r = desc->r;
+    InitList L{};
+    L.k0 = (uint32_t)seed;
+    L.k1 = (uint32_t)(seed >> 32);
+    auto add = [&](void* p, int64_t n, int kind, double a, double bb, bool storage, int id) -> noble_status {
+        if (!p || n == 0) return NOBLE_OK;
+        const uintptr_t align = storage && bf ? 2 : 4;
+        if (reinterpret_cast<uintptr_t>(p) % align) return NOBLE_ERR_MISALIGNED;
+        InitTensor& t = L.t[L.count++];
+        t.ptr = p;
+        t.n = n;
+        t.kind = kind;
+        t.a = a;
+        t.b = bb;
+        t.bf16 = storage && bf ? 1 : 0;
+        t.tensor_id = id;
+        return NOBLE_OK;
+    };
+    NOBLE_TRY(add(W, din * dout, 0, recipe->w_scale / std::sqrt((double)din), 0.0, true, 0));
+    NOBLE_TRY(add(b, dout, 2, 0.0, 0.0, false, 8));
+    if (r > 0) {
+        const double dbound = 1.0 / std::sqrt((double)din);
+        const double mbound = std::sqrt(3.0 / (double)r);   // Xavier uniform, fan_in = fan_out = r
+        NOBLE_TRY(add(W_down, din * r, 1, -dbound, dbound, true, 1));
+        NOBLE_TRY(add(omega1, r, 1, recipe->omega_min, recipe->omega_max, false, 2));
+        NOBLE_TRY(add(phi1, r, 0, recipe->phi_std, 0.0, false, 3));
+        NOBLE_TRY(add(M, r * r, 1, -mbound, mbound, true, 4));
+        NOBLE_TRY(add(omega2, r, 1, recipe->omega_min, recipe->omega_max, false, 5));
+        NOBLE_TRY(add(phi2, r, 0, recipe->phi_std, 0.0, false, 6));
+        NOBLE_TRY(add(W_up, r * dout, 0, recipe->alpha / std::sqrt((double)r), 0.0, true, 7));
+    }
+    if (L.count == 0) return NOBLE_OK;
+    NOBLE_TRY(check_device());
+    hipLaunchKernelGGL(init_kernel, dim3(1024), dim3(256), 0, static_cast<hipStream_t>(stream), L);
+    return last_launch();
 }
 
 }  // extern "C"

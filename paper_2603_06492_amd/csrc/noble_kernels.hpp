@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
         for (int v = 0; v < 4; ++v) {
             const int row = wm0 + 4 * g + v, grow = m0 + row;
             const float h = acc[0][j][v];
-            if (cv && grow < a.T) a.H[(int64_t)grow * r + col] = h;
+            if (a.H && cv && grow < a.T) a.H[(int64_t)grow * r + col] = h;
             const float c1 = cv ? act_value<F, false>(h * w + p) : 0.f;
             if constexpr (L2)
                 *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = to_elt<E>(c1);

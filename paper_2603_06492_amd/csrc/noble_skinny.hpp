@@ -339,9 +339,10 @@ __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
     const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
     const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * r + col) * 2) : kOOB;
     auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * r * es); };
+    const bool keep_h = a.H != nullptr;   // NULL: inference-only forward
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), 0);
+        if (keep_h) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), 0);
         const float c1 = cv ? act_value<F, true>(acc[v] * w1 + p1) : 0.f;
         if constexpr (L2) {
             const int row = 8 * (v >> 2) + 4 * h + (v & 3);

@@ -6,7 +6,10 @@ and turns status codes into exceptions.  There is no fallback: if the library
 is not built, or the device is not gfx950, calls raise.
 
 Functions keep the C names: ``noble_linear_workspace_size``,
-``noble_linear_fwd``, ``noble_linear_bwd``, ``noble_status_string``.
+``noble_linear_fwd``, ``noble_linear_bwd``, ``noble_status_string``, and the
+training-recipe calls ``noble_recipe_defaults``, ``noble_lr_multipliers``,
+``noble_init_params`` (plus ``param_groups``, which only arranges the
+multipliers into optimizer parameter groups).
 ``NobleLinearFunction`` wraps the pair as a ``torch.autograd.Function``.
 
 ``activation`` (keyword of the calls) is a noble_activation code or one of the
@@ -83,6 +86,15 @@ class noble_linear_desc(ctypes.Structure):
     ]
 
 
+class noble_recipe(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in
+                ("alpha", "w_scale", "omega_min", "omega_max", "phi_std", "gamma", "gamma_M", "omega_lr", "phi_lr")]
+
+
+class noble_lr_mults(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("W", "b", "W_down", "W_up", "M", "omega", "phi")]
+
+
 _lib = None
 _vp = ctypes.c_void_p
 
@@ -107,6 +119,14 @@ def lib() -> ctypes.CDLL:
         L.noble_linear_fwd.argtypes = [ctypes.POINTER(noble_linear_desc)] + [_vp] * 13 + [ctypes.c_size_t, _vp]
         L.noble_linear_bwd.restype = ctypes.c_int
         L.noble_linear_bwd.argtypes = [ctypes.POINTER(noble_linear_desc)] + [_vp] * 22 + [ctypes.c_size_t, _vp]
+        L.noble_recipe_defaults.restype = None
+        L.noble_recipe_defaults.argtypes = [ctypes.POINTER(noble_recipe)]
+        L.noble_lr_multipliers.restype = ctypes.c_int
+        L.noble_lr_multipliers.argtypes = [ctypes.POINTER(noble_linear_desc), ctypes.POINTER(noble_recipe),
+                                           ctypes.POINTER(noble_lr_mults)]
+        L.noble_init_params.restype = ctypes.c_int
+        L.noble_init_params.argtypes = [ctypes.POINTER(noble_linear_desc), ctypes.POINTER(noble_recipe),
+                                        ctypes.c_uint64] + [_vp] * 10
         _lib = L
     return _lib
 
@@ -234,6 +254,74 @@ def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, rese
     st = lib().noble_linear_bwd(ctypes.byref(d), *args, nbytes, _stream(stream))
     if st != 0:
         raise NobleError(st, "noble_linear_bwd")
+
+
+# --------------------------------------------------------- training recipe --
+
+def noble_recipe_defaults(**overrides) -> noble_recipe:
+    """The recipe defaults (Sec. 3.3, App. A), with keyword overrides."""
+    rc = noble_recipe()
+    lib().noble_recipe_defaults(ctypes.byref(rc))
+    for k, v in overrides.items():
+        if k not in dict(noble_recipe._fields_):
+            raise TypeError(f"unknown recipe field {k!r}")
+        setattr(rc, k, float(v))
+    return rc
+
+
+def noble_lr_multipliers(d_in: int, d_out: int, r: int, recipe: Optional[noble_recipe] = None) -> dict:
+    """Learning-rate multipliers of W, b, W_down, W_up, M, omega, phi."""
+    rc = noble_recipe_defaults() if recipe is None else recipe
+    d = make_desc(0, d_in, d_out, r, NOBLE_BF16)
+    out = noble_lr_mults()
+    st = lib().noble_lr_multipliers(ctypes.byref(d), ctypes.byref(rc), ctypes.byref(out))
+    if st != 0:
+        raise NobleError(st, "noble_lr_multipliers")
+    return {n: getattr(out, n) for n, _ in noble_lr_mults._fields_}
+
+
+def noble_init_params(W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, seed: int,
+                      recipe: Optional[noble_recipe] = None, stream=None) -> None:
+    """Fill the layer's parameter tensors on the device from ``seed``
+    (None skips a tensor).  Storage tensors share one dtype (bf16 or f32)."""
+    torch = _torch()
+    rc = noble_recipe_defaults() if recipe is None else recipe
+    d_in, d_out = W.shape
+    r = 0
+    for t, dim in ((W_down, 1), (W_up, 0), (M, 0), (omega1, 0), (phi1, 0), (omega2, 0), (phi2, 0)):
+        if t is not None:
+            r = t.shape[dim]
+            break
+    dt = _dtype_code(W)
+    sd, f32 = W.dtype, torch.float32
+    d = make_desc(0, d_in, d_out, r, dt)
+    args = [_ptr(W, "W", sd, (d_in, d_out)), _ptr(b, "b", f32, (d_out,)), _ptr(W_down, "W_down", sd, (d_in, r)),
+            _ptr(omega1, "omega1", f32, (r,)), _ptr(phi1, "phi1", f32, (r,)), _ptr(M, "M", sd, (r, r)),
+            _ptr(omega2, "omega2", f32, (r,)), _ptr(phi2, "phi2", f32, (r,)), _ptr(W_up, "W_up", sd, (r, d_out))]
+    st = lib().noble_init_params(ctypes.byref(d), ctypes.byref(rc), int(seed) & (2 ** 64 - 1), *args,
+                                 _stream(stream))
+    if st != 0:
+        raise NobleError(st, "noble_init_params")
+
+
+def param_groups(params: dict, lr: float, d_in: int, d_out: int, r: int,
+                 recipe: Optional[noble_recipe] = None) -> list:
+    """Optimizer parameter groups for one layer: ``params`` maps the names
+    W, b, W_down, omega1, phi1, M, omega2, phi2, W_up to tensors (missing or
+    None entries are left out); each group's ``lr`` is ``lr`` times the
+    layer's multiplier from noble_lr_multipliers."""
+    m = noble_lr_multipliers(d_in, d_out, r, recipe)
+    which = {"W": "W", "b": "b", "W_down": "W_down", "W_up": "W_up", "M": "M",
+             "omega1": "omega", "omega2": "omega", "phi1": "phi", "phi2": "phi"}
+    groups = {}
+    for name, t in params.items():
+        if t is None:
+            continue
+        if name not in which:
+            raise KeyError(f"unknown parameter name {name!r}")
+        key = which[name]
+        groups.setdefault(key, []).append(t)
+    return [{"params": ts, "lr": lr * m[key], "name": key} for key, ts in groups.items()]
 
 
 # ------------------------------------------------------------ conveniences --

@@ -30,7 +30,8 @@ def _declared_functions():
 def test_library_exports_every_declared_function():
     names = _declared_functions()
     assert set(names) == {"noble_linear_workspace_size", "noble_linear_fwd", "noble_linear_bwd",
-                          "noble_status_string", "noble_abi_version"}
+                          "noble_status_string", "noble_abi_version", "noble_recipe_defaults",
+                          "noble_lr_multipliers", "noble_init_params"}
     L = noble.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -149,6 +150,7 @@ FWD_ARGS = ["x", "W", "b", "W_down", "omega1", "phi1", "M", "omega2", "phi2", "W
 BWD_ARGS = ["dy", "x", "W", "W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up", "reserve", "dx", "dW",
             "db", "dW_down", "dM", "dW_up", "domega1", "dphi1", "domega2", "dphi2", "scratch"]
 NULLABLE = {"b", "db"}
+FWD_NULLABLE = NULLABLE | {"reserve"}   # NULL reserve: inference-only forward
 
 
 @pytest.mark.parametrize("which", FWD_ARGS)
@@ -157,7 +159,7 @@ def test_fwd_rejects_null_and_misaligned(which):
     _, scr = noble.noble_linear_workspace_size(64, 64, 64, 16, noble.NOBLE_BF16)
     ptrs = list(FAKE[:len(FWD_ARGS)])
     i = FWD_ARGS.index(which)
-    if which not in NULLABLE:
+    if which not in FWD_NULLABLE:
         ptrs[i] = None
         assert _fwd(d, ptrs, scr) == NULL
     ptrs[i] = FAKE[i] + 4
