@@ -38,8 +38,17 @@ PEAK_F32 = 157.3e12  # dense fp32 MFMA, MI355X
 METRIC = "NOBLE linear fwd+bwd TFLOP/s, % bf16 MFMA peak, overhead vs plain GEMM"
 
 
-def flop_alg(T, d_in, d_out, r, mixing=True):
-    return 6.0 * T * (d_in * d_out + r * (d_in + d_out) + (r * r if mixing else 0))
+def flop_alg(T, d_in, d_out, r, mixing=True, groups=1):
+    """Forward + backward FLOPs: 6 T [d_in d_out + r (G d_in + d_out) + G r^2]
+    for G groups of rank r (each group maps d_in to d_out / G)."""
+    G = groups
+    return 6.0 * T * (d_in * d_out + r * (G * d_in + d_out) + (G * r * r if mixing else 0))
+
+
+def branch_floor(d_in, d_out, r, mixing=True, groups=1):
+    """Branch FLOPs over the main product's."""
+    G = groups
+    return (r * (G * d_in + d_out) + (G * r * r if mixing else 0)) / (d_in * d_out)
 
 
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "gemm_fwd_plain_ffn_up_T8192_traffic.md")
@@ -112,17 +121,26 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0, activ
     except Exception:  # pragma: no cover
         threads = 1
     shapes = inp.workload_shapes(workload)
+    groups = inp.workload_groups(workload)
     T_full = shapes[0][1]
+
+    def fwd(a, Ts, G):
+        args = (a["x"][:Ts], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"], a["omega2"], a["phi2"],
+                a["W_up"])
+        return oracle.forward_grouped(*args, G, **kw) if G > 1 else oracle.forward(*args, **kw)
+
+    def bwd(a, Ts, G):
+        args = (a["dy"][:Ts], a["x"][:Ts], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"], a["omega2"],
+                a["phi2"], a["W_up"])
+        return oracle.backward_grouped(*args, G, **kw) if G > 1 else oracle.backward(*args, **kw)
     T_max = min(T_full, samples[0]["x"].shape[0])
     Ts = 128
     while True:
         outs = []
         t0 = time.perf_counter()
-        for a in samples:
-            Y, _ = oracle.forward(a["x"][:Ts], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                                  a["omega2"], a["phi2"], a["W_up"], **kw)
-            g = oracle.backward(a["dy"][:Ts], a["x"][:Ts], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                                a["omega2"], a["phi2"], a["W_up"], **kw)
+        for a, G in zip(samples, groups):
+            Y, _ = fwd(a, Ts, G)
+            g = bwd(a, Ts, G)
             outs.append((Y, g["dx"]))
         dt = time.perf_counter() - t0
         if dt >= budget_s / 4 or Ts * 2 > T_max:
@@ -132,11 +150,9 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0, activ
     passes = 1
     while dt < budget_s:
         t0 = time.perf_counter()
-        for a in samples:
-            oracle.forward(a["x"][:Ts], a["W"], a["b"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                           a["omega2"], a["phi2"], a["W_up"], **kw)
-            oracle.backward(a["dy"][:Ts], a["x"][:Ts], a["W"], a["W_down"], a["omega1"], a["phi1"], a["M"],
-                            a["omega2"], a["phi2"], a["W_up"], **kw)
+        for a, G in zip(samples, groups):
+            fwd(a, Ts, G)
+            bwd(a, Ts, G)
         dt += time.perf_counter() - t0
         passes += 1
     parity = {"rows": Ts, "tol": 2e-2, "y": 0.0, "dx": 0.0}
@@ -144,7 +160,7 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0, activ
         gy, gdx = gpu_rows(i, Ts)
         parity["y"] = max(parity["y"], round(_row_err(gy, Y), 6))
         parity["dx"] = max(parity["dx"], round(_row_err(gdx, dx), 6))
-    flops = passes * sum(flop_alg(Ts, di, do, r, mixing) for (_, _, di, do, r) in shapes)
+    flops = passes * sum(flop_alg(Ts, di, do, r, mixing, G) for (_, _, di, do, r), G in zip(shapes, groups))
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"first {Ts} of {T_full} tokens of every projection (the bench's own arrays), "
                       f"numpy float64, {passes} fwd+bwd passes",
@@ -189,6 +205,7 @@ def main():
 
     wl = inp.WORKLOADS[args.workload]
     shapes = inp.workload_shapes(args.workload)
+    groups = inp.workload_groups(args.workload)
     print(f"[bench] workload {args.workload}: {len(shapes)} projections, T={wl['T']}, r={wl['r']}",
           file=sys.stderr, flush=True)
     probs, plain, samples = [], [], []
@@ -243,7 +260,7 @@ def main():
 
     per = []
     for dp, d0 in zip(probs, plain):
-        T, di, do, r = dp.p.T, dp.p.d_in, dp.p.d_out, dp.p.r
+        T, di, do, r, G = dp.p.T, dp.p.d_in, dp.p.d_out, dp.p.r, dp.G
         for _ in range(10):
             dp.fwd(); dp.bwd(); d0.fwd(); d0.bwd()
         torch.cuda.synchronize()
@@ -251,14 +268,14 @@ def main():
         tb = median_ms(dp.bwd, args.proj_reps)
         pf = median_ms(d0.fwd, args.proj_reps)
         pb = median_ms(d0.bwd, args.proj_reps)
-        fl = flop_alg(T, di, do, r, mixing)
-        entry = {"projection": dp.p.name.split("/")[-1], "T": T, "d_in": di, "d_out": do, "r": r,
+        fl = flop_alg(T, di, do, r, mixing, G)
+        entry = {"projection": dp.p.name.split("/")[-1], "T": T, "d_in": di, "d_out": do, "r": r, "groups": G,
                  "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4), "plain_fwd_ms": round(pf, 4),
                  "plain_bwd_ms": round(pb, 4), "tflops": round(fl / ((tf + tb) * 1e-3) / 1e12, 2),
                  "pct_bf16_peak": round(100 * fl / ((tf + tb) * 1e-3) / PEAK_BF16, 2),
                  "main_gemm_pct_peak": round(100 * 6.0 * T * di * do / ((pf + pb) * 1e-3) / PEAK_BF16, 2),
                  "overhead": round((tf + tb) / (pf + pb) - 1, 4),
-                 "overhead_floor": round((r * (di + do) + (r * r if mixing else 0)) / (di * do), 4)}
+                 "overhead_floor": round(branch_floor(di, do, r, mixing, G), 4)}
         if not args.no_blas:
             # Context only: hipBLASLt (through torch.mm) on the same plain
             # products and operands, bf16 in and out: y = x W, dx = dy W^T,
@@ -308,10 +325,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    flops_step = sum(flop_alg(T, di, do, r, mixing) for (_, T, di, do, r) in shapes)
+    flops_step = sum(flop_alg(T, di, do, r, mixing, G) for (_, T, di, do, r), G in zip(shapes, groups))
     main_flops = sum(6.0 * T * di * do for (_, T, di, do, r) in shapes)
     value = flops_step / (ms_noble * 1e-3) / 1e12
-    floor = sum(T * (r * (di + do) + (r * r if mixing else 0)) for (_, T, di, do, r) in shapes) / \
+    floor = sum(T * di * do * branch_floor(di, do, r, mixing, G) for (_, T, di, do, r), G in zip(shapes, groups)) / \
         sum(T * di * do for (_, T, di, do, r) in shapes)
     out = {
         "metric": METRIC,
@@ -327,7 +344,8 @@ def main():
         "dtype": wl["dtype"],
         "data": "synthetic",
         "config": {"workload": args.workload, "T": wl["T"], "r": wl["r"], "activation": args.activation,
-                   "projections": [f"{n} {di}->{do}" for (n, _, di, do, _) in shapes]},
+                   "projections": [f"{n} {di}->{do}" + (f" ({G} groups)" if G > 1 else "")
+                                   for (n, _, di, do, _), G in zip(shapes, groups)]},
         "pct_bf16_peak": round(100 * value / (PEAK_BF16 / 1e12), 2),
         "plain_ms_per_step": round(ms_plain, 4),
         "overhead_vs_plain": round(ms_noble / ms_plain - 1, 4),

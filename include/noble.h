@@ -34,8 +34,16 @@
  *    float32 throughout on the f32 path.
  *  - Shapes: T >= 0 (any value); d_in, d_out >= 8 and multiples of 8;
  *    r = 0 (plain linear: every branch pointer is ignored and may be NULL) or
- *    8 <= r <= 128 with r a multiple of 8.  Every pointer must be 16-byte
- *    aligned.  Outputs must not alias inputs or each other.
+ *    8 <= r <= 256 (bf16) / 128 (f32) with r a multiple of 8.  Every pointer
+ *    must be 16-byte aligned.  Outputs must not alias inputs or each other.
+ *  - Groups (desc->groups = G, 1 to 4; 0 means 1): the d_out output columns
+ *    form G equal blocks that share x, each with its own branch of rank r
+ *    (Q, K and V of an attention block, each with its own CosNet,
+ *    Sec. 4.1.1).  With d_g = d_out / G (a multiple of 8) and R = G r:
+ *      W_down [d_in, R]   (group g: columns g r .. g r + r - 1)
+ *      M [G, r, r], omega1/phi1/omega2/phi2 [R]   (group g: entries g r ..)
+ *      W_up [R, d_g]      (group g: rows g r .., mapping onto y[:, g d_g ..])
+ *    and the gradients have the same shapes.  G = 1 is the single layer.
  *  - Argument checking is complete before any HIP call: on any error the call
  *    returns a status and enqueues nothing.
  *  - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
@@ -94,12 +102,14 @@ typedef struct noble_linear_desc {
     int64_t r;      /* bottleneck rank; 0 = plain linear */
     int32_t dtype;  /* noble_dtype */
     int32_t activation; /* noble_activation */
+    int32_t groups;     /* output column groups, each with its own branch (0 = 1) */
+    int32_t reserved;   /* must be 0 */
 } noble_linear_desc;
 
 /* Sizes of the two caller-owned work buffers for `desc`.
- *   reserve_bytes: written by noble_linear_fwd (H = x W_down, float32 [T, r])
+ *   reserve_bytes: written by noble_linear_fwd (H = x W_down, float32 [T, R])
  *                  and read by the matching noble_linear_bwd; keep it intact
- *                  in between.  4*T*r bytes.
+ *                  in between.  4*T*R bytes (R = groups * r).
  *   scratch_bytes: temporary space used within one call (fwd or bwd) only;
  *                  its contents need no initialisation.  The forward uses it
  *                  only when r > 0; the backward may use it also when r = 0
@@ -184,7 +194,8 @@ void noble_recipe_defaults(noble_recipe* recipe);
 /* Learning-rate multipliers, relative to the base learning rate, of each
  * parameter of one layer (Sec. 3.3 Eqs. 3-4): W, b and W_down take the base
  * rate, W_up and M the elevated rates above, omega and phi the fixed
- * multipliers.  With r = 0 only W and b are meaningful (the rest are 0). */
+ * multipliers.  With r = 0 only W and b are meaningful (the rest are 0).
+ * For a grouped layer the widths are those of one group (d_in, d_out / G). */
 typedef struct noble_lr_mults {
     double W, b, W_down, W_up, M, omega, phi;
 } noble_lr_mults;
@@ -228,7 +239,7 @@ const char* noble_status_string(int status);
 /* ABI version of this header (bumped on incompatible changes). */
 int noble_abi_version(void);
 
-#define NOBLE_ABI_VERSION 2
+#define NOBLE_ABI_VERSION 3
 
 #ifdef __cplusplus
 }

@@ -13,10 +13,12 @@ from .noble_oracle import (  # noqa: F401
     activation_slope,
     activation_value,
     backward,
+    backward_grouped,
     branch_backward,
     branch_forward,
     branch_param_shapes,
     cosnet_backward,
     cosnet_forward,
     forward,
+    forward_grouped,
 )

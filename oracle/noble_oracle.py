@@ -58,6 +58,8 @@ __all__ = [
     "forward",
     "backward",
     "branch_param_shapes",
+    "forward_grouped",
+    "backward_grouped",
 ]
 
 # The bottleneck activations of the ablation in §4.4 (Table 5): each nonlinearity
@@ -255,3 +257,61 @@ def branch_param_shapes(d_in, d_out, r):
         "omega2": (r,),
         "phi2": (r,),
     }
+
+
+# ------------------------------------------------------------ grouped layers --
+# NOBLE puts a branch on every linear projection, Q, K and V included
+# (§4.1.1).  When Q, K and V are computed as one product of the shared x, the
+# layer's d_out columns form G equal blocks, and block g is a layer of its own:
+#     y[:, g] = x W[:, g] + b[g] + sigma_g(x W_down[:, g]) W_up[g]
+# with W_down's column block g (r columns), M[g], the vectors' entries
+# g r .. g r + r - 1 and W_up's row block g ([G r, d_out / G]).
+
+
+def _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g):
+    r, dg = R // G, d_out // G
+    rs = slice(g * r, (g + 1) * r)
+    pick = lambda v: None if v is None else _f64(v)[rs]
+    Mg = None if M is None else (_f64(M) if G == 1 else _f64(M)[g])
+    return (slice(g * dg, (g + 1) * dg), _f64(W_down)[:, rs], pick(omega1), pick(phi1), Mg, pick(omega2),
+            pick(phi2), _f64(W_up)[rs])
+
+
+def forward_grouped(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, groups,
+                    activation="cosnet", mix_round=None):
+    """Eq. (1) for each of ``groups`` column blocks sharing x.  Returns
+    ``(Y, H)`` with H = x W_down ([T, G r])."""
+    W = _f64(W)
+    G, d_out, R = int(groups), W.shape[1], _f64(W_down).shape[1]
+    Ys = []
+    for g in range(G):
+        cs, Dg, w1, p1, Mg, w2, p2, Ug = _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g)
+        Y, _ = forward(x, W[:, cs], None if b is None else _f64(b)[cs], Dg, w1, p1, Mg, w2, p2, Ug,
+                       activation=activation, mix_round=mix_round)
+        Ys.append(Y)
+    return np.concatenate(Ys, axis=1), _f64(x) @ _f64(W_down)
+
+
+def backward_grouped(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, groups,
+                     dx_rows=None, dW_rows=None, activation="cosnet", mix_round=None):
+    """Gradients of L = sum(dy * Y) for the grouped layer: each block's
+    backward on its columns of dy; dx, which every block reaches through x,
+    is the sum of the blocks' dx, every other gradient is the blocks'
+    gradients side by side (dM stacked [G, r, r], or [r, r] for G = 1)."""
+    W, dy = _f64(W), _f64(dy)
+    G, d_out, R = int(groups), W.shape[1], _f64(W_down).shape[1]
+    parts = []
+    for g in range(G):
+        cs, Dg, w1, p1, Mg, w2, p2, Ug = _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g)
+        parts.append(backward(dy[:, cs], x, W[:, cs], Dg, w1, p1, Mg, w2, p2, Ug, dx_rows=dx_rows,
+                              dW_rows=dW_rows, activation=activation, mix_round=mix_round))
+    cat = lambda k, ax: None if parts[0][k] is None else np.concatenate([q[k] for q in parts], axis=ax)
+    out = {"dx": sum(q["dx"] for q in parts), "dW": cat("dW", 1), "db": cat("db", 0),
+           "dW_down": cat("dW_down", 1), "dW_up": cat("dW_up", 0)}
+    for k in ("domega1", "dphi1", "domega2", "dphi2"):
+        out[k] = cat(k, 0)
+    if parts[0]["dM"] is None:
+        out["dM"] = None
+    else:
+        out["dM"] = parts[0]["dM"] if G == 1 else np.stack([q["dM"] for q in parts])
+    return out

@@ -83,9 +83,13 @@ def to_bf16(a):
     return u.astype(np.uint32).view(np.float32)
 
 
-def init_values(d_in, d_out, r, seed, dtype="bf16", recipe=None):
+def init_values(d_in, d_out, r, seed, dtype="bf16", recipe=None, groups=1):
     """Initial values of every parameter, as float32 arrays (storage tensors
-    rounded to bf16 when ``dtype`` is "bf16")."""
+    rounded to bf16 when ``dtype`` is "bf16").  ``groups`` G > 1: W_down
+    [d_in, G r], M [G, r, r], the vectors [G r], W_up [G r, d_out / G], each
+    tensor drawn as one row-major stream."""
+    G = groups
+    R, dog = G * r, d_out // G
     rc = dict(DEFAULTS, **(recipe or {}))
     store = (lambda a: to_bf16(a.astype(np.float32))) if dtype == "bf16" else (lambda a: a.astype(np.float32))
     out = {
@@ -96,14 +100,15 @@ def init_values(d_in, d_out, r, seed, dtype="bf16", recipe=None):
     if r > 0:
         db = 1.0 / np.sqrt(d_in)
         mb = np.sqrt(6.0 / (r + r))
-        out["W_down"] = store(draw_uniform(seed, TENSOR_IDS["W_down"], d_in * r, -db, db)).reshape(d_in, r)
-        out["M"] = store(draw_uniform(seed, TENSOR_IDS["M"], r * r, -mb, mb)).reshape(r, r)
-        out["W_up"] = store(draw_normal(seed, TENSOR_IDS["W_up"], r * d_out, rc["alpha"] / np.sqrt(r))
-                            ).reshape(r, d_out)
+        out["W_down"] = store(draw_uniform(seed, TENSOR_IDS["W_down"], d_in * R, -db, db)).reshape(d_in, R)
+        M = store(draw_uniform(seed, TENSOR_IDS["M"], G * r * r, -mb, mb))
+        out["M"] = M.reshape(r, r) if G == 1 else M.reshape(G, r, r)
+        out["W_up"] = store(draw_normal(seed, TENSOR_IDS["W_up"], R * dog, rc["alpha"] / np.sqrt(r))
+                            ).reshape(R, dog)
         for i in (1, 2):
-            out[f"omega{i}"] = draw_uniform(seed, TENSOR_IDS[f"omega{i}"], r, rc["omega_min"],
+            out[f"omega{i}"] = draw_uniform(seed, TENSOR_IDS[f"omega{i}"], R, rc["omega_min"],
                                             rc["omega_max"]).astype(np.float32)
-            out[f"phi{i}"] = draw_normal(seed, TENSOR_IDS[f"phi{i}"], r, rc["phi_std"]).astype(np.float32)
+            out[f"phi{i}"] = draw_normal(seed, TENSOR_IDS[f"phi{i}"], R, rc["phi_std"]).astype(np.float32)
     return out
 
 

@@ -22,6 +22,7 @@ using namespace noble;
 namespace {
 
 constexpr int64_t kMaxDim = int64_t(1) << 20;
+constexpr int kMaxGroups = 4;
 constexpr int64_t kMaxTokens = (int64_t(1) << 31) - 4096;
 constexpr size_t kAlign = 256;
 
@@ -35,9 +36,22 @@ noble_status check_desc(const noble_linear_desc* d) {
     if (d->T < 0 || d->T > kMaxTokens) return NOBLE_ERR_BAD_SHAPE;
     if (d->d_in < 8 || d->d_in % 8 || d->d_in > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
     if (d->d_out < 8 || d->d_out % 8 || d->d_out > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
-    if (d->r < 0 || (d->r > 0 && (d->r < 8 || d->r % 8 || d->r > 128))) return NOBLE_ERR_BAD_SHAPE;
+    const int64_t rmax = d->dtype == NOBLE_BF16 ? 256 : 128;
+    if (d->r < 0 || (d->r > 0 && (d->r < 8 || d->r % 8 || d->r > rmax))) return NOBLE_ERR_BAD_SHAPE;
+    if (d->groups < 0 || d->groups > kMaxGroups) return NOBLE_ERR_BAD_SHAPE;
+    const int64_t G = d->groups > 0 ? d->groups : 1;
+    if (d->d_out % (8 * G)) return NOBLE_ERR_BAD_SHAPE;
     return NOBLE_OK;
 }
+
+// Groups of output columns, each with its own branch (0 counts as 1).
+int ngroups(const noble_linear_desc* d) { return d->groups > 0 ? d->groups : 1; }
+// Total rank G r: the width of H and of the rank-side scratch arrays.
+int64_t rank_total(const noble_linear_desc* d) { return ngroups(d) * d->r; }
+// Output columns of one group.
+int64_t group_dout(const noble_linear_desc* d) { return d->d_out / ngroups(d); }
+// 128-rank blocks of one group.
+int rank_blocks(const noble_linear_desc* d) { return (int)((d->r + kSkN - 1) / kSkN); }
 
 size_t elt_size(const noble_linear_desc* d) { return d->dtype == NOBLE_BF16 ? 2 : 4; }
 
@@ -73,33 +87,37 @@ noble_status with_act(int a, Fn&& fn) {
     return NOBLE_ERR_BAD_ACTIVATION;
 }
 
-// Pieces of K for the bf16 rank projection [T, K] x [K, r]: enough
-// workgroups of 128 tokens to cover the CUs, at least kPjMinChunks K chunks
-// per piece, at most kPjMaxSplit pieces.
-int proj_split(int64_t T, int64_t K) {
+// Pieces of K for the bf16 rank projection [T, K] x [K, r] run as J jobs
+// (group, 128-rank block): enough workgroups of 128 tokens to cover the CUs,
+// at least kPjMinChunks K chunks per piece, at most kPjMaxSplit pieces.
+int proj_split(int64_t T, int64_t K, int J) {
     const int64_t blocks = (T + kPjRows - 1) / kPjRows;
     const int64_t nkc = (K + 63) / 64;
     int s = 1;
-    while (blocks * s < 256 && 2 * s * kPjMinChunks <= nkc && 2 * s <= kPjMaxSplit) s *= 2;
+    while (blocks * s * J < 256 && 2 * s * kPjMinChunks <= nkc && 2 * s <= kPjMaxSplit) s *= 2;
     return s;
 }
+int proj_jobs(const noble_linear_desc* d) { return ngroups(d) * rank_blocks(d); }
 
 // Scratch layout, each part 256-byte aligned: four [T, r] storage-type
 // regions C1, C2, dH2, dH (the forward uses only C2); on the bf16 path the
 // float32 projection partials [S][T][r] for the larger split of the forward
 // and backward projections; then the float32 split-K partials of the
 // weight-gradient products (backward only).
-size_t scratch_region(const noble_linear_desc* d) { return align_up((size_t)d->T * d->r * elt_size(d)); }
+size_t scratch_region(const noble_linear_desc* d) {
+    return align_up((size_t)d->T * rank_total(d) * elt_size(d));
+}
 size_t partial_need(const noble_linear_desc* d) {
     if (d->r == 0 || d->dtype != NOBLE_BF16) return 0;
-    const int s = std::max(proj_split(d->T, d->d_in), proj_split(d->T, d->d_out));
-    return align_up((size_t)s * d->T * d->r * 4);
+    const int J = proj_jobs(d);
+    const int s = std::max(proj_split(d->T, d->d_in, J), proj_split(d->T, group_dout(d), J));
+    return align_up((size_t)s * d->T * rank_total(d) * 4);
 }
 size_t wgrad_need(const noble_linear_desc* d);
 size_t scratch_need(const noble_linear_desc* d) {
     return (d->r > 0 ? 4 * scratch_region(d) + partial_need(d) : 0) + wgrad_need(d);
 }
-size_t reserve_need(const noble_linear_desc* d) { return (size_t)d->T * d->r * 4; }
+size_t reserve_need(const noble_linear_desc* d) { return (size_t)d->T * rank_total(d) * 4; }
 
 // A required buffer: non-NULL and 16-byte aligned, unless it holds no bytes.
 noble_status need(const void* p, bool nonempty) {
@@ -264,7 +282,8 @@ noble_status launch_gemm(const Batch& bt, hipStream_t st, bool plain = false) {
     return last_launch();
 }
 
-// float32 path: chain kernels with their own rank projection.
+// float32 path: chain kernels with their own rank projection, one launch per
+// group (the arguments already point at the group's operands and columns).
 noble_status launch_chain(bool fwd, int RP, int act, const ChainArgs& a, int T, hipStream_t st) {
     const dim3 grid(cdiv(T, kChainRows)), block(kThreads);
     return with_act(act, [&]<Act F, bool L2>() -> noble_status {
@@ -284,21 +303,37 @@ noble_status launch_chain(bool fwd, int RP, int act, const ChainArgs& a, int T, 
     });
 }
 
-// bf16 path, step 1: split-K rank projection of c.A against c.B into the
-// float32 partials P [S][T][r] (K = c.nk chunks of 64).
-noble_status launch_proj(bool fwd, const ChainArgs& c, float* P, int S, hipStream_t st,
-                         const ZeroList* zero = nullptr) {
+// bf16 path, step 1: split-K rank projection into the float32 partials
+// P [S][T][R], one job per (group, 128-rank block).  Forward: A = x, B =
+// W_down's column block (MN-major, row stride R).  Backward: A = the group's
+// column block of dy, B = the group's rows of W_up [R, d_out / G] (K-major).
+noble_status launch_proj(bool fwd, const noble_linear_desc* d, const void* A, const void* B, float* P, int S,
+                         hipStream_t st, const ZeroList* zero = nullptr) {
+    const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r, R = rank_total(d), dog = group_dout(d);
+    const int G = ngroups(d), NB = rank_blocks(d);
     ProjArgs a{};
     if (zero) a.z = *zero;
-    a.A = c.A;
-    a.B = c.B;
+    a.J = 0;
+    for (int g = 0; g < G; ++g)
+        for (int b = 0; b < NB; ++b) {
+            ProjJob& j = a.job[a.J++];
+            const int64_t c0 = g * r + (int64_t)b * kSkN, n = std::min<int64_t>(kSkN, r - (int64_t)b * kSkN);
+            if (fwd) {
+                j.A = operand1(seg(A, din, din), T);
+                j.B = operand1(seg(static_cast<const uint16_t*>(B) + c0, R, din), n);
+            } else {
+                j.A = operand1(seg(static_cast<const uint16_t*>(A) + g * dog, dout, dog), T);
+                j.B = operand1(seg(static_cast<const uint16_t*>(B) + c0 * dog, dog, dog), n);
+            }
+            j.c0 = (int)c0;
+        }
     a.P = P;
-    a.pstride = (int64_t)c.T * c.r;
-    a.T = c.T;
-    a.r = c.r;
-    a.nk = c.nk;
+    a.ldp = (int)R;
+    a.pstride = T * R;
+    a.T = (int)T;
+    a.nk = cdiv(fwd ? din : dog, 64);
     a.S = S;
-    const dim3 grid(cdiv(c.T, kPjRows) * S), block(kPjThreads);
+    const dim3 grid(cdiv(T, kPjRows) * S * a.J), block(kPjThreads);
     if (fwd)
         hipLaunchKernelGGL(proj_kernel<false>, grid, block, 0, st, a);
     else
@@ -307,11 +342,12 @@ noble_status launch_proj(bool fwd, const ChainArgs& c, float* P, int S, hipStrea
 }
 
 // bf16 path, step 2: the branch nonlinearity (forward or backward) from the
-// summed partials.
-noble_status launch_branch(bool fwd, int act, const ChainArgs& c, const float* P, int S, hipStream_t st) {
+// summed partials, one workgroup per (32 tokens, group).
+noble_status launch_branch(bool fwd, const noble_linear_desc* d, const ChainArgs& c, const float* P, int S,
+                           hipStream_t st) {
     BranchArgs a{};
     a.P = P;
-    a.pstride = (int64_t)c.T * c.r;
+    a.pstride = d->T * rank_total(d);
     a.S = S;
     a.M = reinterpret_cast<const uint16_t*>(c.M);
     a.w1 = c.w1;
@@ -327,14 +363,24 @@ noble_status launch_branch(bool fwd, int act, const ChainArgs& c, const float* P
     a.dp1 = c.dp1;
     a.dw2 = c.dw2;
     a.dp2 = c.dp2;
-    a.T = c.T;
-    a.r = c.r;
-    const dim3 grid(cdiv(c.T, kSkRows)), block(kThreads);
-    return with_act(act, [&]<Act F, bool L2>() -> noble_status {
-        if (fwd)
-            hipLaunchKernelGGL((branch_fwd_kernel<F, L2>), grid, block, 0, st, a);
-        else
-            hipLaunchKernelGGL((branch_bwd_kernel<F, L2>), grid, block, 0, st, a);
+    a.T = (int)d->T;
+    a.r = (int)d->r;
+    a.G = ngroups(d);
+    a.R = (int)rank_total(d);
+    const int NT = rank_blocks(d);
+    const dim3 grid(cdiv(d->T, kSkRows) * a.G), block(kThreads * NT);
+    return with_act(d->activation, [&]<Act F, bool L2>() -> noble_status {
+        if (NT == 1) {
+            if (fwd)
+                hipLaunchKernelGGL((branch_fwd_kernel<F, L2, 1>), grid, block, 0, st, a);
+            else
+                hipLaunchKernelGGL((branch_bwd_kernel<F, L2, 1>), grid, block, 0, st, a);
+        } else {
+            if (fwd)
+                hipLaunchKernelGGL((branch_fwd_kernel<F, L2, 2>), grid, block, 0, st, a);
+            else
+                hipLaunchKernelGGL((branch_bwd_kernel<F, L2, 2>), grid, block, 0, st, a);
+        }
         return last_launch();
     });
 }
@@ -353,17 +399,42 @@ int chain_rp(int64_t r) {
     return r <= 64 ? 64 : 128;
 }
 
+// Per-group view of the branch arguments for the float32 chain kernels: the
+// group's operands, vectors and columns of the [T, R] arrays.
+ChainArgs group_chain(const ChainArgs& a, const noble_linear_desc* d, int g, size_t es) {
+    const int64_t r = d->r, c0 = g * r;
+    ChainArgs c = a;
+    auto off = [&](char* p, int64_t elems, size_t e) { return p ? p + elems * (int64_t)e : p; };
+    auto offf = [&](auto* p, int64_t elems) { return p ? p + elems : p; };
+    c.M = a.M ? a.M + g * r * r * (int64_t)es : a.M;
+    c.w1 = offf(a.w1, c0);
+    c.p1 = offf(a.p1, c0);
+    c.w2 = offf(a.w2, c0);
+    c.p2 = offf(a.p2, c0);
+    c.H = offf(a.H, c0);
+    c.C1s = off(a.C1s, c0, es);
+    c.C2s = off(a.C2s, c0, es);
+    c.dH2s = off(a.dH2s, c0, es);
+    c.dHs = off(a.dHs, c0, es);
+    c.dw1 = offf(a.dw1, c0);
+    c.dp1 = offf(a.dp1, c0);
+    c.dw2 = offf(a.dw2, c0);
+    c.dp2 = offf(a.dp2, c0);
+    return c;
+}
+
 template <typename E>
 noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, const float* b, const void* Wd,
                       const float* w1, const float* p1, const void* M, const float* w2, const float* p2,
                       const void* Wu, void* y, void* reserve, void* scratch, hipStream_t st) {
     constexpr int BK = Elt<E>::BK;
+    constexpr size_t ES = sizeof(E);
     const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
+    const int64_t R = rank_total(d), dog = group_dout(d);
+    const int G = ngroups(d);
     char* C2s = static_cast<char*>(scratch) + scratch_region(d);
     if (r > 0) {
         ChainArgs a{};
-        a.A = operand1(seg(x, din, din), T);
-        a.B = operand1(seg(Wd, r, din), r);
         a.M = static_cast<const char*>(M);
         a.w1 = w1;
         a.p1 = p1;
@@ -373,23 +444,37 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
         a.C2s = C2s;
         a.T = (int)T;
         a.r = (int)r;
+        a.ldr = (int)R;
         a.nk = cdiv(din, BK);
         if constexpr (sizeof(E) == 2) {
             float* P = reinterpret_cast<float*>(static_cast<char*>(scratch) + 4 * scratch_region(d));
-            const int S = proj_split(T, din);
-            NOBLE_TRY(launch_proj(true, a, P, S, st));
-            NOBLE_TRY(launch_branch(true, d->activation, a, P, S, st));
-        } else
-            NOBLE_TRY(launch_chain(true, chain_rp<E>(r), d->activation, a, (int)T, st));
+            const int S = proj_split(T, din, proj_jobs(d));
+            NOBLE_TRY(launch_proj(true, d, x, Wd, P, S, st));
+            NOBLE_TRY(launch_branch(true, d, a, P, S, st));
+        } else {
+            for (int g = 0; g < G; ++g) {
+                ChainArgs c = group_chain(a, d, g, ES);
+                c.A = operand1(seg(x, din, din), T);
+                c.B = operand1(seg(static_cast<const E*>(Wd) + g * r, R, din), r);
+                NOBLE_TRY(launch_chain(true, chain_rp<E>(r), d->activation, c, (int)T, st));
+            }
+        }
     }
-    // y = [x | C2] [W ; W_up] + b
+    // y[:, g] = [x | C2_g] [W_g ; W_up_g] + b_g, one problem per group (the
+    // rank-r up-projection is a K-extension of the main product)
     constexpr int GBK = gemm_bk<E>();
     const int nk1 = cdiv(din, GBK);
     const int nk = nk1 + (r > 0 ? cdiv(r, GBK) : 0);
     Batch bt;
-    bt.add(operand2(seg(x, din, din), seg(C2s, r, r), nk1, T), operand2(seg(W, dout, din), seg(Wu, dout, r), nk1, dout),
-           (int)T, (int)dout, nk, y, dout, sizeof(E) == 4, b, nullptr, 1);
-    return launch_gemm<E, true, false>(bt, st, r == 0);
+    for (int g = 0; g < G; ++g) {
+        const E* Wg = static_cast<const E*>(W) + g * dog;
+        const char* C2g = C2s + g * r * (int64_t)ES;
+        const E* Wug = r > 0 ? static_cast<const E*>(Wu) + g * r * dog : nullptr;
+        bt.add(operand2(seg(x, din, din), seg(C2g, R, r), nk1, T), operand2(seg(Wg, dout, din), seg(Wug, dog, r), nk1, dog),
+               (int)T, (int)dog, nk, static_cast<E*>(y) + g * dog, dout, sizeof(E) == 4, b ? b + g * dog : nullptr,
+               nullptr, 1);
+    }
+    return launch_gemm<E, true, false>(bt, st, r == 0 && G == 1);
 }
 
 template <typename E>
@@ -398,7 +483,11 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
                       const void* Wu, const void* reserve, void* dx, float* dW, float* db, float* dWd, float* dM,
                       float* dWu, float* dw1, float* dp1, float* dw2, float* dp2, void* scratch, hipStream_t st) {
     constexpr int BK = Elt<E>::BK;
+    constexpr size_t ES = sizeof(E);
     const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
+    const int64_t R = rank_total(d), dog = group_dout(d);
+    const int G = ngroups(d);
+    const bool two = act_two_layers(d->activation);
     const size_t reg = scratch_region(d);
     char* base = static_cast<char*>(scratch);
     char* C1s = base;
@@ -427,13 +516,13 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     if (T == 0) zero(dW, din * dout);
     zero(db, dout);
     if (r > 0) {
-        zero(dWd, din * r);
-        zero(dM, r * r);
-        zero(dWu, r * dout);
-        zero(dw1, r);
-        zero(dp1, r);
-        zero(dw2, r);
-        zero(dp2, r);
+        zero(dWd, din * R);
+        zero(dM, G * r * r);
+        zero(dWu, R * dog);
+        zero(dw1, R);
+        zero(dp1, R);
+        zero(dw2, R);
+        zero(dp2, R);
     }
     // On the bf16 path with a branch, the projection kernel does the zeroing.
     const bool zero_in_proj = sizeof(E) == 2 && r > 0 && T > 0;
@@ -445,8 +534,6 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
 
     if (r > 0) {
         ChainArgs a{};
-        a.A = operand1(seg(dy, dout, dout), T);
-        a.B = operand1(seg(Wu, dout, dout), r);   // B(k=j, n=q) = W_up[q][j]
         a.M = static_cast<const char*>(M);
         a.w1 = w1;
         a.p1 = p1;
@@ -463,30 +550,38 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         a.dp2 = dp2;
         a.T = (int)T;
         a.r = (int)r;
-        a.nk = cdiv(dout, BK);
+        a.ldr = (int)R;
+        a.nk = cdiv(dog, BK);
         if constexpr (sizeof(E) == 2) {
             float* P = reinterpret_cast<float*>(base + 4 * reg);
-            const int S = proj_split(T, dout);
-            NOBLE_TRY(launch_proj(false, a, P, S, st, &z));
-            NOBLE_TRY(launch_branch(false, d->activation, a, P, S, st));
-        } else
-            NOBLE_TRY(launch_chain(false, chain_rp<E>(r), d->activation, a, (int)T, st));
+            const int S = proj_split(T, dog, proj_jobs(d));
+            NOBLE_TRY(launch_proj(false, d, dy, Wu, P, S, st, &z));
+            NOBLE_TRY(launch_branch(false, d, a, P, S, st));
+        } else {
+            for (int g = 0; g < G; ++g) {
+                ChainArgs c = group_chain(a, d, g, ES);
+                // dC2_g = dy_g W_up_g^T: A = the group's columns of dy, B(k = j, n = q) = W_up_g[q][j]
+                c.A = operand1(seg(static_cast<const E*>(dy) + g * dog, dout, dog), T);
+                c.B = operand1(seg(static_cast<const E*>(Wu) + g * r * dog, dog, dog), r);
+                NOBLE_TRY(launch_chain(false, chain_rp<E>(r), d->activation, c, (int)T, st));
+            }
+        }
     }
 
     // dx = [dy | dH] [W^T ; W_down^T]   (B(k, n) stored [n][k]: K-major)
     {
         const int nk1 = cdiv(dout, GBK);
-        const int nk = nk1 + (r > 0 ? cdiv(r, GBK) : 0);
+        const int nk = nk1 + (r > 0 ? cdiv(R, GBK) : 0);
         Batch bt;
-        bt.add(operand2(seg(dy, dout, dout), seg(dHs, r, r), nk1, T), operand2(seg(W, dout, dout), seg(Wd, r, r), nk1, din),
+        bt.add(operand2(seg(dy, dout, dout), seg(dHs, R, R), nk1, T), operand2(seg(W, dout, dout), seg(Wd, R, R), nk1, din),
                (int)T, (int)din, nk, dx, din, sizeof(E) == 4, nullptr, nullptr, 1);
         NOBLE_TRY((launch_gemm<E, true, true>(bt, st)));
     }
 
     // Weight gradients, reduced over tokens (K = T), A and B both MN-major, in
-    // one grouped launch: the rank-r gradients (dW_down, dW_up, dM) add
-    // atomically and fill the CUs that dW leaves idle; a split dW stores
-    // partials that reduce_kernel then sums into dW.
+    // one grouped launch: the rank-r gradients (dW_down, and dW_up, dM per
+    // group) add atomically and fill the CUs that dW leaves idle; a split dW
+    // stores partials that reduce_kernel then sums into dW.
     {
         Batch bt;
         const Operand xT = operand1(seg(x, din, T), din);
@@ -494,16 +589,21 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split,
                wp.split > 1 ? wpart : nullptr);
         if (r > 0) {
-            const Operand dHN = operand1(seg(dHs, r, T), r);
-            const Operand C2T = operand1(seg(C2s, r, T), r);
-            const Operand C1T = operand1(seg(C1s, r, T), r);
-            const Operand dH2N = operand1(seg(dH2s, r, T), r);
-            bt.add(xT, dHN, (int)din, (int)r, nkT, dWd, r, true, nullptr, nullptr,
-                   choose_split_atomic(cdiv(din, kBM), nkT));
-            bt.add(C2T, dyN, (int)r, (int)dout, nkT, dWu, dout, true, nullptr, nullptr,
-                   choose_split_atomic(cdiv(dout, kBN), nkT));
-            if (act_two_layers(d->activation))
-                bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM, r, true, nullptr, nullptr, choose_split_atomic(1, nkT));
+            bt.add(xT, operand1(seg(dHs, R, T), R), (int)din, (int)R, nkT, dWd, R, true, nullptr, nullptr,
+                   choose_split_atomic(cdiv(din, kBM) * cdiv(R, kBN), nkT));
+            for (int g = 0; g < G; ++g) {
+                const int64_t c0 = g * r;
+                const Operand C2T = operand1(seg(C2s + c0 * (int64_t)ES, R, T), r);
+                const Operand dyg = operand1(seg(static_cast<const E*>(dy) + g * dog, dout, T), dog);
+                bt.add(C2T, dyg, (int)r, (int)dog, nkT, dWu + c0 * dog, dog, true, nullptr, nullptr,
+                       choose_split_atomic(cdiv(r, kBM) * cdiv(dog, kBN), nkT));
+                if (two) {
+                    const Operand C1T = operand1(seg(C1s + c0 * (int64_t)ES, R, T), r);
+                    const Operand dH2N = operand1(seg(dH2s + c0 * (int64_t)ES, R, T), r);
+                    bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM + g * r * r, r, true, nullptr, nullptr,
+                           choose_split_atomic(cdiv(r, kBM) * cdiv(r, kBN), nkT));
+                }
+            }
         }
         NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
         if (wp.split > 1) {
@@ -644,8 +744,9 @@ noble_status noble_lr_multipliers(const noble_linear_desc* desc, const noble_rec
     *out = noble_lr_mults{1.0, 1.0, 0.0, 0.0, 0.0, 0.0, 0.0};
     if (desc->r == 0) return NOBLE_OK;
     // Sec. 3.3 Eqs. 3-4: the ratio of the smaller layer width to the rank,
-    // raised to 2 gamma (W_up) and gamma_M (M)
-    const double ratio = (double)std::min(desc->d_in, desc->d_out) / (double)desc->r;
+    // raised to 2 gamma (W_up) and gamma_M (M); for a grouped layer the width
+    // of one group (each group is its own d_in -> d_out / G layer)
+    const double ratio = (double)std::min(desc->d_in, group_dout(desc)) / (double)desc->r;
     out->W_down = 1.0;
     out->W_up = std::pow(ratio, 2.0 * recipe->gamma);
     out->M = std::pow(ratio, recipe->gamma_M);
@@ -661,6 +762,7 @@ noble_status noble_init_params(const noble_linear_desc* desc, const noble_recipe
     NOBLE_TRY(check_desc(desc));
     const bool bf = desc->dtype == NOBLE_BF16;
     const int64_t din = desc->d_in, dout = desc->d_out, r = desc->r;
+    const int64_t R = rank_total(desc), G = ngroups(desc), dog = group_dout(desc);
     InitList L{};
     L.k0 = (uint32_t)seed;
     L.k1 = (uint32_t)(seed >> 32);
@@ -683,13 +785,13 @@ noble_status noble_init_params(const noble_linear_desc* desc, const noble_recipe
     if (r > 0) {
         const double dbound = 1.0 / std::sqrt((double)din);
         const double mbound = std::sqrt(3.0 / (double)r);   // Xavier uniform, fan_in = fan_out = r
-        NOBLE_TRY(add(W_down, din * r, 1, -dbound, dbound, true, 1));
-        NOBLE_TRY(add(omega1, r, 1, recipe->omega_min, recipe->omega_max, false, 2));
-        NOBLE_TRY(add(phi1, r, 0, recipe->phi_std, 0.0, false, 3));
-        NOBLE_TRY(add(M, r * r, 1, -mbound, mbound, true, 4));
-        NOBLE_TRY(add(omega2, r, 1, recipe->omega_min, recipe->omega_max, false, 5));
-        NOBLE_TRY(add(phi2, r, 0, recipe->phi_std, 0.0, false, 6));
-        NOBLE_TRY(add(W_up, r * dout, 0, recipe->alpha / std::sqrt((double)r), 0.0, true, 7));
+        NOBLE_TRY(add(W_down, din * R, 1, -dbound, dbound, true, 1));
+        NOBLE_TRY(add(omega1, R, 1, recipe->omega_min, recipe->omega_max, false, 2));
+        NOBLE_TRY(add(phi1, R, 0, recipe->phi_std, 0.0, false, 3));
+        NOBLE_TRY(add(M, G * r * r, 1, -mbound, mbound, true, 4));
+        NOBLE_TRY(add(omega2, R, 1, recipe->omega_min, recipe->omega_max, false, 5));
+        NOBLE_TRY(add(phi2, R, 0, recipe->phi_std, 0.0, false, 6));
+        NOBLE_TRY(add(W_up, R * dog, 0, recipe->alpha / std::sqrt((double)r), 0.0, true, 7));
     }
     if (L.count == 0) return NOBLE_OK;
     NOBLE_TRY(check_device());

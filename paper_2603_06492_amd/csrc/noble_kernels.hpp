@@ -102,7 +102,8 @@ struct ChainArgs {
     float* dp1;
     float* dw2;
     float* dp2;
-    int T, r, nk, pad_;
+    int T, r, nk;
+    int ldr;            // row stride of H and of the scratch arrays (G r for grouped layers)
 };
 
 constexpr int kChainRows = 32;  // tokens per workgroup in the chain kernels
@@ -185,12 +186,12 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
         for (int v = 0; v < 4; ++v) {
             const int row = wm0 + 4 * g + v, grow = m0 + row;
             const float h = acc[0][j][v];
-            if (a.H && cv && grow < a.T) a.H[(int64_t)grow * r + col] = h;
+            if (a.H && cv && grow < a.T) a.H[(int64_t)grow * a.ldr + col] = h;
             const float c1 = cv ? act_value<F, false>(h * w + p) : 0.f;
             if constexpr (L2)
                 *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = to_elt<E>(c1);
             else if (cv && grow < a.T)
-                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = to_elt<E>(c1);
+                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * a.ldr + col] = to_elt<E>(c1);
         }
     }
     if constexpr (!L2) return;
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
         for (int v = 0; v < 4; ++v) {
             const int grow = m0 + wm0 + 4 * g + v;
             if (grow < a.T)
-                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] =
+                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * a.ldr + col] =
                     to_elt<E>(act_value<F, false>(mix[0][j][v] * w + p));
         }
     }
@@ -254,7 +255,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
         for (int v = 0; v < 4; ++v) {
             const int row = wm0 + 4 * g + v, grow = m0 + row;
             const bool ok = cv && grow < a.T;
-            const float h = ok ? a.H[(int64_t)grow * r + col] : 0.f;
+            const float h = ok ? a.H[(int64_t)grow * a.ldr + col] : 0.f;
             float f = 0.f, d = 0.f;
             if (cv) act_value_slope<F, false>(h * w + p, f, d);
             hr[j][v] = h;
@@ -262,9 +263,9 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
             const E c1 = to_elt<E>(f);
             if constexpr (L2) {
                 *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = c1;
-                if (ok) reinterpret_cast<E*>(a.C1s)[(int64_t)grow * r + col] = c1;
+                if (ok) reinterpret_cast<E*>(a.C1s)[(int64_t)grow * a.ldr + col] = c1;
             } else if (ok) {
-                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = c1;
+                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * a.ldr + col] = c1;
             }
         }
     }
@@ -308,8 +309,8 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
                 const E dh2 = to_elt<E>(da2 * w);
                 *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = dh2;
                 if (ok) {
-                    reinterpret_cast<E*>(a.C2s)[(int64_t)grow * r + col] = to_elt<E>(f);
-                    reinterpret_cast<E*>(a.dH2s)[(int64_t)grow * r + col] = dh2;
+                    reinterpret_cast<E*>(a.C2s)[(int64_t)grow * a.ldr + col] = to_elt<E>(f);
+                    reinterpret_cast<E*>(a.dH2s)[(int64_t)grow * a.ldr + col] = dh2;
                 }
             }
             sw = wave_colsum(sw);
@@ -342,7 +343,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
             const float da1 = ok ? d1[j][v] * dc1[0][j][v] : 0.f;
             sw += da1 * hr[j][v];
             sp += da1;
-            if (ok) reinterpret_cast<E*>(a.dHs)[(int64_t)grow * r + col] = to_elt<E>(da1 * w);
+            if (ok) reinterpret_cast<E*>(a.dHs)[(int64_t)grow * a.ldr + col] = to_elt<E>(da1 * w);
         }
         sw = wave_colsum(sw);
         sp = wave_colsum(sp);

@@ -23,10 +23,16 @@
 //   one-application form C2 = f(H w1 + p1), which skips M and the second
 //   frequency/phase pair.
 //
-// The chain kernels run 32 tokens x 128 ranks per workgroup, four waves each
-// owning 32 rank columns.  M [r, r] is loaded into LDS once per workgroup in
-// its HBM layout [r_in][r_out]; C1 M reads it with ds_read_b64_tr_b16 and
+// The chain kernels run 32 tokens x one group's ranks per workgroup: four
+// waves (r <= 128) or eight (r <= 256), each owning 32 rank columns.  M [r, r]
+// is loaded into LDS once per workgroup as 128 x 128 tiles in its HBM
+// orientation [r_in][r_out]; C1 M reads it with ds_read_b64_tr_b16 and
 // dH2 M^T with ds_read_b128.
+//
+// Grouped layers (several output column blocks of one x, each with its own
+// branch, e.g. Q, K and V): the rank side is stored token-major as [T, G r];
+// the projection runs one job per (group, 128-rank block) and the chain one
+// workgroup per (token block, group).
 #pragma once
 
 #include "noble_gemm_dma.hpp"
@@ -35,10 +41,15 @@
 namespace noble {
 
 constexpr int kSkRows = 32;     // tokens per chain workgroup
-constexpr int kSkN = 128;       // padded rank columns
-constexpr int kSkM = kSkN * kSkN * 2;     // M tile, 128 x 128 bf16
-constexpr int kSkC = kSkRows * kSkN * 2;  // C1 / dH2 operand tile, 32 x 128 bf16
-constexpr int kSkLds = kSkM + kSkC;
+constexpr int kSkN = 128;       // rank columns of one M tile
+constexpr int kSkM = kSkN * kSkN * 2;     // one M tile, 128 x 128 bf16
+constexpr int kSkC = kSkRows * kSkN * 2;  // 32 x 128 bf16 of the C1 / dH2 operand tile
+constexpr int kSkMaxNT = 2;               // ranks up to 2 x 128 per group
+// LDS of a chain workgroup with NT x NT M tiles and a 32 x 128 NT operand tile
+template <int NT>
+constexpr int sk_lds() {
+    return NT * NT * kSkM + NT * kSkC;
+}
 
 constexpr int kPjRows = 128;                 // tokens per projection workgroup
 constexpr int kPjThreads = 512;              // eight waves: 4 token blocks x 2 rank halves
@@ -49,41 +60,57 @@ constexpr int kPjStage = kPjA + kPjB;
 constexpr int kPjLoads = 4;                  // DMA instructions per wave per K chunk
 constexpr int kPjMinChunks = 4;              // 64-element K chunks per piece, at least
 constexpr int kPjMaxSplit = 8;
+constexpr int kPjMaxJobs = 8;                // (group, 128-rank block) pairs per launch
+
+// One block of at most 128 rank columns of the projection: A [T, K] K-major
+// (x in the forward, a group's column block of dy in the backward) times B
+// (W_down's column block [K, n] MN-major, or W_up's row block [n, K] K-major),
+// written to partial columns c0 .. c0 + n - 1 (n = B.rows).
+struct ProjJob {
+    Operand A;
+    Operand B;
+    int c0, pad_;
+};
 
 struct ProjArgs {
-    Operand A;          // [T, K] K-major: x (forward) or dy (backward)
-    Operand B;          // W_down [K, r] MN-major (forward) or W_up [r, K] K-major (backward)
-    float* P;           // partials [S][T][r] float32
-    int64_t pstride;    // T * r
-    int T, r, nk, S;    // nk: 64-element K chunks
+    ProjJob job[kPjMaxJobs];
+    float* P;           // partials [S][T][ldp] float32
+    int64_t pstride;    // T * ldp
+    int T, ldp, nk, S;  // nk: 64-element K chunks (the same for every job)
+    int J, pad_;        // jobs
     ZeroList z;         // float arrays to clear on the side (the backward's
                         // atomically accumulated gradients)
 };
 
+// G groups of r ranks, stored token-major with row stride R = G r: group g
+// owns columns g r .. g r + r - 1 of H, C1, C2, dH2, dH and of the partials,
+// rows g r .. of the frequency / phase vectors and M + g r r.
 struct BranchArgs {
-    const float* P;       // projection partials [S][T][r]
+    const float* P;       // projection partials [S][T][R]
     int64_t pstride;
-    const uint16_t* M;    // [r, r]
-    const float* w1;
+    const uint16_t* M;    // [G][r][r]
+    const float* w1;      // [R]
     const float* p1;
     const float* w2;
     const float* p2;
-    float* H;             // reserve [T, r] float32
-    uint16_t* C1s;        // scratch [T, r] bf16 (backward)
-    uint16_t* C2s;        // scratch [T, r] bf16
-    uint16_t* dH2s;       // scratch [T, r] bf16 (backward)
-    uint16_t* dHs;        // scratch [T, r] bf16 (backward)
-    float* dw1;
+    float* H;             // reserve [T, R] float32 (NULL in an inference forward)
+    uint16_t* C1s;        // scratch [T, R] bf16 (backward)
+    uint16_t* C2s;        // scratch [T, R] bf16
+    uint16_t* dH2s;       // scratch [T, R] bf16 (backward)
+    uint16_t* dHs;        // scratch [T, R] bf16 (backward)
+    float* dw1;           // [R]
     float* dp1;
     float* dw2;
     float* dp2;
-    int T, r, S, pad_;
+    int T, r, S, G, R, pad_;
 };
+
 
 // One 64-element K chunk of the projection operands: 4 DMA instructions per
 // wave (two for A, two for B).
 template <bool BKM>
-__device__ __forceinline__ void proj_dma(const ProjArgs& a, int row0, int kc, char* st, int wave, int lane) {
+__device__ __forceinline__ void proj_dma(const Operand& A, const Operand& B, int row0, int kc, char* st, int wave,
+                                         int lane) {
     constexpr int ES = 2;
     const int k0 = kc * 64;
     // K-major tiles store logical 16-byte chunk c of row q at physical chunk
@@ -102,14 +129,14 @@ __device__ __forceinline__ void proj_dma(const ProjArgs& a, int row0, int kc, ch
             dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)8 * b * ld * ES));
         }
     };
-    kmajor(a.A, row0, st);
+    kmajor(A, row0, st);
     char* dst = st + kPjA;
     if constexpr (BKM) {
-        kmajor(a.B, 0, dst);
+        kmajor(B, 0, dst);
     } else {
         // 64 k-rows x 256 B, block b = 8i + w holds k-rows 4b .. 4b+3; lane p ->
         // k-row 4b + p/16, physical segment p%16 holding logical (p%16) ^ 4(p/16)
-        const Operand& op = a.B;
+        const Operand& op = B;
         const int64_t ld = op.s[0].ld;
         const int klen = op.s[0].klen;
         const i32x4 rs = make_desc(op.s[0].ptr + (int64_t)k0 * ld * ES, (int64_t)(klen - k0) * ld * ES);
@@ -125,19 +152,28 @@ __device__ __forceinline__ void proj_dma(const ProjArgs& a, int row0, int kc, ch
     }
 }
 
-// M [r, r] into LDS as [128 r_in][256 B], 16-byte segment s of row p at
-// physical segment s ^ 4(p & 3); rows / columns past r read as zero.
+// M [r, r] into LDS as NT x NT tiles of [128 r_in][256 B]; tile i NT + j
+// holds M[128 i .., 128 j ..], and 16-byte segment s of tile row p sits at
+// physical segment s ^ 4(p & 3).  Rows / columns past r read as zero.
+template <int NT>
 __device__ __forceinline__ void m_dma(const uint16_t* M, int r, char* dst, int wave, int lane) {
+    constexpr int NW = 4 * NT;   // waves of the workgroup
     const i32x4 rs = make_desc(reinterpret_cast<const char*>(M), (int64_t)r * r * 2);
     const int kq = lane >> 4;
     const int seg = (lane & 15) ^ (4 * kq);
-    const int col = 8 * seg;
-    const uint32_t vo = col < r ? (uint32_t)(((int64_t)kq * r + col) * 2) : kOOB;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int b = 4 * i + wave;   // rows 4b .. 4b+3
-        dma16(rs, dst + b * 1024, vo, (uint32_t)((int64_t)4 * b * r * 2));
-    }
+    for (int ti = 0; ti < NT; ++ti)
+#pragma unroll
+        for (int tj = 0; tj < NT; ++tj) {
+            const int col = 128 * tj + 8 * seg;
+            const uint32_t vo = col < r ? (uint32_t)(((int64_t)(128 * ti + kq) * r + col) * 2) : kOOB;
+            char* tile = dst + (ti * NT + tj) * kSkM;
+#pragma unroll
+            for (int i = 0; i < 32 / NW; ++i) {
+                const int b = NW * i + wave;   // tile rows 4b .. 4b+3
+                dma16(rs, tile + b * 1024, vo, (uint32_t)((int64_t)4 * b * r * 2));
+            }
+        }
 }
 
 // Transposed 8-row read of a [k][256 B] tile (16-byte segments swizzled by
@@ -160,46 +196,56 @@ __device__ __forceinline__ u32x4 tr_read8(const char* tile, uint32_t base, int s
     return v;
 }
 
-// Byte offset of element (row, col) of the 32 x 128 bf16 operand tile, laid
-// out K-major as two 64-column chunks of [32 rows][128 B], chunk c of row
+// Byte offset of element (row, col) of the 32 x 128 NT bf16 operand tile,
+// laid out K-major as 64-column chunks of [32 rows][128 B], chunk c of row
 // stored at c ^ swz(row).
 __device__ __forceinline__ int ctile_off(int row, int col) {
     return (col >> 6) * 4096 + row * 128 + ((((col >> 3) & 7) ^ ((row ^ (row >> 3)) & 7)) << 4) + (col & 7) * 2;
 }
 
-// acc (one 32x32 block per wave) over K steps of a [32 x 128] tile in LDS
-// (A, K-major) times the M tile, either M itself (TRANS_M = false: B(k, n) =
-// M[k][n]) or M^T (B(k, n) = M[n][k]).
-template <bool TRANS_M>
+// acc (one 32x32 block per wave, columns 32 w .. of the 128 NT) over the K
+// steps of a [32 x 128 NT] tile in LDS (A, K-major) times M (TRANS_M = false:
+// B(k, n) = M[k][n]) or M^T (B(k, n) = M[n][k]), M held as NT x NT tiles.
+template <bool TRANS_M, int NT>
 __device__ __forceinline__ void mix_mma(const char* ctile, const char* mt, int wave, int lane, f32x16& acc) {
     const int r32 = lane & 31, h = lane >> 5;
-    const uint32_t tb = tr_base(wave, lane);
-    const int p = 32 * wave + r32;   // row of M for the M^T product
+    const int wl = wave & 3, nb = wave >> 2;   // 32-column block within tile column nb
+    const uint32_t tb = tr_base(wl, lane);
+    const int p = 32 * wl + r32;   // tile row of M for the M^T product
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-        const int q = 2 * s + h;  // 8-element K group of this lane
-        const u32x4 av = *reinterpret_cast<const u32x4*>(ctile + (q >> 3) * 4096 + r32 * 128 +
-                                                         ((((q & 7) ^ (r32 & 7) ^ (r32 >> 3))) << 4));
-        u32x4 bv;
-        if constexpr (!TRANS_M)
-            bv = tr_read8(mt, tb, s);
-        else
-            bv = *reinterpret_cast<const u32x4*>(mt + p * 256 + ((q ^ (4 * (p & 3))) << 4));
-        mma32<uint16_t>(acc, av, bv);
+    for (int kb = 0; kb < NT; ++kb) {
+        const char* tile = mt + (TRANS_M ? nb * NT + kb : kb * NT + nb) * kSkM;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            const int ql = 2 * s + h;     // 8-element K group of this lane within the tile
+            const int q = 16 * kb + ql;   // ... within the whole rank
+            const u32x4 av = *reinterpret_cast<const u32x4*>(ctile + (q >> 3) * 4096 + r32 * 128 +
+                                                             ((((q & 7) ^ (r32 & 7) ^ (r32 >> 3))) << 4));
+            u32x4 bv;
+            if constexpr (!TRANS_M)
+                bv = tr_read8(tile, tb, s);
+            else
+                bv = *reinterpret_cast<const u32x4*>(tile + p * 256 + ((ql ^ (4 * (p & 3))) << 4));
+            mma32<uint16_t>(acc, av, bv);
+        }
     }
 }
 
 // Split-K rank projection.  Workgroup g: token block g % blocks, K piece
-// g / blocks.  Wave w owns rows 32 (w / 2) .. +31 and rank columns
-// 64 (w % 2) .. +63 of the 128 x 128 tile (two 32x32x16 MFMAs per K step).
+// (g / blocks) % S, job g / (blocks S).  Wave w owns rows 32 (w / 2) .. +31
+// and rank columns 64 (w % 2) .. +63 of the job's 128 x 128 tile (two
+// 32x32x16 MFMAs per K step).
 template <bool BKM>
 __global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds[kPjStages * kPjStage];
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
     const int blocks = (a.T + kPjRows - 1) / kPjRows;
-    const int piece = blockIdx.x / blocks;
-    const int row0 = (blockIdx.x - piece * blocks) * kPjRows;
+    const int ji = blockIdx.x / (blocks * a.S);
+    const int rem = blockIdx.x - ji * blocks * a.S;
+    const int piece = rem / blocks;
+    const int row0 = (rem - piece * blocks) * kPjRows;
+    const ProjJob& jb = a.job[ji];
     const int kc0 = (int)((int64_t)a.nk * piece / a.S), kc1 = (int)((int64_t)a.nk * (piece + 1) / a.S);
     const int wr = wave >> 1, wc = wave & 1;
 
@@ -222,7 +268,7 @@ __global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
     const int n = kc1 - kc0;
 #pragma unroll
     for (int c = 0; c < kPjStages - 1; ++c)
-        if (c < n) proj_dma<BKM>(a, row0, kc0 + c, lds + c * kPjStage, wave, lane);
+        if (c < n) proj_dma<BKM>(jb.A, jb.B, row0, kc0 + c, lds + c * kPjStage, wave, lane);
 
     // The zeroing rides on the projection: every workgroup clears a strided
     // share while its first loads are in flight.
@@ -249,8 +295,8 @@ __global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
             wait_vmcnt<0>();
         __syncthreads();
         if (i + kPjStages - 1 < n)
-            proj_dma<BKM>(a, row0, kc0 + i + kPjStages - 1, lds + ((i + kPjStages - 1) % kPjStages) * kPjStage,
-                          wave, lane);
+            proj_dma<BKM>(jb.A, jb.B, row0, kc0 + i + kPjStages - 1,
+                          lds + ((i + kPjStages - 1) % kPjStages) * kPjStage, wave, lane);
         const char* st = lds + (i % kPjStages) * kPjStage;
         const char* sb = st + kPjA;
 #pragma unroll
@@ -268,38 +314,39 @@ __global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
         }
     }
 
-    // acc[j][v]: row 32 wr + 8(v/4) + 4h + v%4, column 64 wc + 32 j + r32;
-    // rows past T and columns past r are dropped by the buffer range check
-    const int r = a.r;
+    // acc[j][v]: row 32 wr + 8(v/4) + 4h + v%4, column c0 + 64 wc + 32 j + r32;
+    // rows past T are dropped by the buffer range check, columns past the
+    // job's width by the kOOB offset
+    const int ldp = a.ldp, n_cols = jb.B.rows;
     const __amdgpu_buffer_rsrc_t rp =
-        make_rsrc(reinterpret_cast<const char*>(a.P + piece * a.pstride) + (int64_t)row0 * r * 4,
-                  (int64_t)(a.T - row0) * r * 4);
+        make_rsrc(reinterpret_cast<const char*>(a.P + piece * a.pstride + jb.c0) + (int64_t)row0 * ldp * 4,
+                  (int64_t)(a.T - row0) * ldp * 4);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int col = 64 * wc + 32 * j + r32;
-        const uint32_t vo = col < r ? (uint32_t)(((32 * wr + 4 * h) * r + col) * 4) : kOOB;
+        const uint32_t vo = col < n_cols ? (uint32_t)(((32 * wr + 4 * h) * ldp + col) * 4) : kOOB;
 #pragma unroll
         for (int v = 0; v < 16; ++v)
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[j][v]), rp, vo,
-                                                  (uint32_t)((8 * (v >> 2) + (v & 3)) * r * 4), 0);
+                                                  (uint32_t)((8 * (v >> 2) + (v & 3)) * ldp * 4), 0);
     }
 }
 
 // acc[v] = sum over the S partials of token row0 + 8(v/4) + 4h + v%4, rank
-// column col (zero past T or r).
-__device__ __forceinline__ void sum_partials(const BranchArgs& a, int row0, int col, int h, f32x16& acc) {
-    const int r = a.r;
-    const uint32_t vo = col < r ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
+// column c0 + col of the group (zero past T or past the group's r).
+__device__ __forceinline__ void sum_partials(const BranchArgs& a, int row0, int c0, int col, int h, f32x16& acc) {
+    const int R = a.R;
+    const uint32_t vo = col < a.r ? (uint32_t)(((4 * h) * R + col) * 4) : kOOB;
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[v] = 0.f;
     for (int s = 0; s < a.S; ++s) {
         const __amdgpu_buffer_rsrc_t rp =
-            make_rsrc(reinterpret_cast<const char*>(a.P + s * a.pstride) + (int64_t)row0 * r * 4,
-                      (int64_t)(a.T - row0) * r * 4);
+            make_rsrc(reinterpret_cast<const char*>(a.P + s * a.pstride + c0) + (int64_t)row0 * R * 4,
+                      (int64_t)(a.T - row0) * R * 4);
 #pragma unroll
         for (int v = 0; v < 16; ++v)
             acc[v] += __uint_as_float(
-                __builtin_amdgcn_raw_buffer_load_b32(rp, vo, (uint32_t)((8 * (v >> 2) + (v & 3)) * r * 4), 0));
+                __builtin_amdgcn_raw_buffer_load_b32(rp, vo, (uint32_t)((8 * (v >> 2) + (v & 3)) * R * 4), 0));
     }
 }
 
@@ -312,33 +359,51 @@ __device__ __forceinline__ float block_colsum(const float (&x)[16]) {
     return s + __shfl_xor(s, 32);
 }
 
+// Workgroup b of a chain launch: token block b / G, group b % G.  Wave w
+// owns rank column 32 w + lane % 32 of the group (NT = 1: 4 waves, 128 ranks;
+// NT = 2: 8 waves, 256 ranks).
+struct ChainPos {
+    int row0, g, c0;
+};
+__device__ __forceinline__ ChainPos chain_pos(const BranchArgs& a) {
+    const int tb = blockIdx.x / a.G;
+    const int g = blockIdx.x - tb * a.G;
+    return ChainPos{tb * kSkRows, g, g * a.r};
+}
+
+// Buffer resource over the group's columns of a [T, R] array from token row0
+// (element size es): offsets (row * R + col) * es, col < r.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t group_rsrc(const void* base, const BranchArgs& a, const ChainPos& q,
+                                                             int es) {
+    return make_rsrc(reinterpret_cast<const char*>(base) + ((int64_t)q.row0 * a.R + q.c0) * es,
+                     (int64_t)(a.T - q.row0) * a.R * es);
+}
+
 // Forward chain.  L2: the two-application form with M (CosNet for F = Cos);
 // otherwise C2 = f(H w1 + p1) and M, w2, p2 are not read.
-template <Act F, bool L2>
-__global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
-    __shared__ __attribute__((aligned(1024))) char lds[kSkLds];
+template <Act F, bool L2, int NT>
+__global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs a) {
+    __shared__ __attribute__((aligned(1024))) char lds[sk_lds<NT>()];
     char* mt = lds;
-    char* ct = mt + kSkM;
+    char* ct = mt + NT * NT * kSkM;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
-    const int row0 = blockIdx.x * kSkRows;
-    const int r = a.r;
+    const ChainPos q = chain_pos(a);
+    const int r = a.r, R = a.R;
 
-    if constexpr (L2) m_dma(a.M, r, mt, wave, lane);   // lands while the partials are summed
-    // acc[v]: token row0 + 8(v/4) + 4h + v%4, rank column 32 wave + r32
+    if constexpr (L2) m_dma<NT>(a.M + (int64_t)q.g * r * r, r, mt, wave, lane);   // lands while the partials are summed
+    // acc[v]: token row0 + 8(v/4) + 4h + v%4, rank column 32 wave + r32 of the group
     const int col = 32 * wave + r32;
     f32x16 acc;
-    sum_partials(a, row0, col, h, acc);
+    sum_partials(a, q.row0, q.c0, col, h, acc);
 
     const bool cv = col < r;
-    const float w1 = cv ? a.w1[col] : 0.f, p1 = cv ? a.p1[col] : 0.f;
-    const __amdgpu_buffer_rsrc_t rh =
-        make_rsrc(reinterpret_cast<const char*>(a.H) + (int64_t)row0 * r * 4, (int64_t)(a.T - row0) * r * 4);
-    const __amdgpu_buffer_rsrc_t rc =
-        make_rsrc(reinterpret_cast<const char*>(a.C2s) + (int64_t)row0 * r * 2, (int64_t)(a.T - row0) * r * 2);
-    const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
-    const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * r + col) * 2) : kOOB;
-    auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * r * es); };
+    const float w1 = cv ? a.w1[q.c0 + col] : 0.f, p1 = cv ? a.p1[q.c0 + col] : 0.f;
+    const __amdgpu_buffer_rsrc_t rh = group_rsrc(a.H, a, q, 4);
+    const __amdgpu_buffer_rsrc_t rc = group_rsrc(a.C2s, a, q, 2);
+    const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * R + col) * 4) : kOOB;
+    const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * R + col) * 2) : kOOB;
+    auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * R * es); };
     const bool keep_h = a.H != nullptr;   // NULL: inference-only forward
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -352,14 +417,14 @@ __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
         }
     }
     if constexpr (L2) {
-        const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
+        const float w2 = cv ? a.w2[q.c0 + col] : 0.f, p2 = cv ? a.p2[q.c0 + col] : 0.f;
         wait_vmcnt<0>();   // this wave's part of M has landed
         __syncthreads();   // C1 tile and M complete
 
         f32x16 h2;
 #pragma unroll
         for (int v = 0; v < 16; ++v) h2[v] = 0.f;
-        mix_mma<false>(ct, mt, wave, lane, h2);
+        mix_mma<false, NT>(ct, mt, wave, lane, h2);
 #pragma unroll
         for (int v = 0; v < 16; ++v)
             __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(act_value<F, true>(h2[v] * w2 + p2)), rc, vo2,
@@ -369,33 +434,30 @@ __global__ __launch_bounds__(kThreads, 1) void branch_fwd_kernel(BranchArgs a) {
 
 // Backward chain, same forms as branch_fwd_kernel.  The one-application form
 // writes C2 and dH only (no C1, dH2 and no second frequency/phase).
-template <Act F, bool L2>
-__global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
-    __shared__ __attribute__((aligned(1024))) char lds[kSkLds];
+template <Act F, bool L2, int NT>
+__global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs a) {
+    __shared__ __attribute__((aligned(1024))) char lds[sk_lds<NT>()];
     char* mt = lds;
-    char* ct = mt + kSkM;
+    char* ct = mt + NT * NT * kSkM;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
-    const int row0 = blockIdx.x * kSkRows;
-    const int r = a.r;
+    const ChainPos q = chain_pos(a);
+    const int r = a.r, R = a.R;
 
-    if constexpr (L2) m_dma(a.M, r, mt, wave, lane);
+    if constexpr (L2) m_dma<NT>(a.M + (int64_t)q.g * r * r, r, mt, wave, lane);
     const int col = 32 * wave + r32;
     f32x16 dc2;
-    sum_partials(a, row0, col, h, dc2);   // dC2 = dy W_up^T
+    sum_partials(a, q.row0, q.c0, col, h, dc2);   // dC2 = dy W_up^T
 
     const bool cv = col < r;
-    const float w1 = cv ? a.w1[col] : 0.f, p1 = cv ? a.p1[col] : 0.f;
-    const int64_t rows_left = a.T - row0;
-    const __amdgpu_buffer_rsrc_t rh =
-        make_rsrc(reinterpret_cast<const char*>(a.H) + (int64_t)row0 * r * 4, rows_left * r * 4);
-    auto rs16 = [&](uint16_t* base) {
-        return make_rsrc(reinterpret_cast<const char*>(base) + (int64_t)row0 * r * 2, rows_left * r * 2);
-    };
-    const __amdgpu_buffer_rsrc_t rc2 = rs16(a.C2s), rdh = rs16(a.dHs);
-    const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * r + col) * 4) : kOOB;
-    const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * r + col) * 2) : kOOB;
-    auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * r * es); };
+    const int gc = q.c0 + col;   // column of the [R] vectors
+    const float w1 = cv ? a.w1[gc] : 0.f, p1 = cv ? a.p1[gc] : 0.f;
+    const int64_t rows_left = a.T - q.row0;
+    const __amdgpu_buffer_rsrc_t rh = group_rsrc(a.H, a, q, 4);
+    const __amdgpu_buffer_rsrc_t rc2 = group_rsrc(a.C2s, a, q, 2), rdh = group_rsrc(a.dHs, a, q, 2);
+    const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * R + col) * 4) : kOOB;
+    const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * R + col) * 2) : kOOB;
+    auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * R * es); };
 
     // H from the reserve (rows past T and columns past r read as zero);
     // A1 = H w1 + p1, keep f'(A1)
@@ -416,8 +478,8 @@ __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
             dc1[v] = dc2[v];
         }
     } else {
-        const float w2 = cv ? a.w2[col] : 0.f, p2 = cv ? a.p2[col] : 0.f;
-        const __amdgpu_buffer_rsrc_t rc1 = rs16(a.C1s), rdh2 = rs16(a.dH2s);
+        const float w2 = cv ? a.w2[gc] : 0.f, p2 = cv ? a.p2[gc] : 0.f;
+        const __amdgpu_buffer_rsrc_t rc1 = group_rsrc(a.C1s, a, q, 2), rdh2 = group_rsrc(a.dH2s, a, q, 2);
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int row = 8 * (v >> 2) + 4 * h + (v & 3);
@@ -434,8 +496,8 @@ __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
         f32x16 h2;
 #pragma unroll
         for (int v = 0; v < 16; ++v) h2[v] = 0.f;
-        mix_mma<false>(ct, mt, wave, lane, h2);   // H2 = C1 M
-        __syncthreads();                           // done reading C1 from LDS
+        mix_mma<false, NT>(ct, mt, wave, lane, h2);   // H2 = C1 M
+        __syncthreads();                               // done reading C1 from LDS
 
         // A2 = H2 w2 + p2, C2 = f(A2), dA2 = f'(A2) dC2, dH2 = dA2 w2
         float da2h2[16], da2[16];
@@ -456,15 +518,15 @@ __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
         {
             const float sw = block_colsum(da2h2), sp = block_colsum(da2);
             if (h == 0 && cv) {
-                unsafeAtomicAdd(a.dw2 + col, sw);
-                unsafeAtomicAdd(a.dp2 + col, sp);
+                unsafeAtomicAdd(a.dw2 + gc, sw);
+                unsafeAtomicAdd(a.dp2 + gc, sp);
             }
         }
         __syncthreads();   // dH2 tile complete
 
 #pragma unroll
         for (int v = 0; v < 16; ++v) dc1[v] = 0.f;
-        mix_mma<true>(ct, mt, wave, lane, dc1);   // dC1 = dH2 M^T
+        mix_mma<true, NT>(ct, mt, wave, lane, dc1);   // dC1 = dH2 M^T
     }
 
     // dA1 = f'(A1) dC1; dw1 += dA1 H, dp1 += dA1; dH = dA1 w1
@@ -480,8 +542,8 @@ __global__ __launch_bounds__(kThreads, 1) void branch_bwd_kernel(BranchArgs a) {
     }
     const float sw = block_colsum(da1h), sp = block_colsum(da1);
     if (h == 0 && cv) {
-        unsafeAtomicAdd(a.dw1 + col, sw);
-        unsafeAtomicAdd(a.dp1 + col, sp);
+        unsafeAtomicAdd(a.dw1 + gc, sw);
+        unsafeAtomicAdd(a.dp1 + gc, sp);
     }
 }
 

@@ -61,9 +61,10 @@ class Projection:
     T: int
     d_in: int
     d_out: int
-    r: int
+    r: int                          # rank of each group's branch
     dtype: str                      # "bf16" or "f32" (storage type)
     arrays: Dict[str, np.ndarray]   # float32 arrays of exactly the device values
+    groups: int = 1                 # output column groups sharing x, one branch each
 
     def __getitem__(self, k):
         return self.arrays[k]
@@ -84,7 +85,10 @@ def draw_projection(name: str, T: int, d_in: int, d_out: int, r: int,
                     dtype: str = "bf16", seed: int = 0, *,
                     w_var: Optional[float] = None, d_var: Optional[float] = None,
                     m_var: Optional[float] = None, u_var: Optional[float] = None,
-                    bias_std: float = 0.0) -> Projection:
+                    bias_std: float = 0.0, groups: int = 1) -> Projection:
+    """Seeded inputs of one layer.  ``groups`` G > 1 gives the grouped layout:
+    W_down [d_in, G r], M [G, r, r], frequency / phase vectors [G r] and
+    W_up [G r, d_out / G]; G = 1 draws exactly the single-layer arrays."""
     if dtype not in ("bf16", "f32"):
         raise ValueError(f"dtype must be 'bf16' or 'f32', got {dtype!r}")
     w_var = 1.0 / d_in if w_var is None else w_var
@@ -101,28 +105,33 @@ def draw_projection(name: str, T: int, d_in: int, d_out: int, r: int,
             a *= f32(math.sqrt(var))
         return a
 
+    G = int(groups)
+    if G < 1 or d_out % G:
+        raise ValueError(f"d_out ({d_out}) must split into {G} groups")
+    R = G * r
+
     def freq():
-        return (f32(1.0) + f32(0.1) * rng.standard_normal(r, dtype=f32)).astype(f32)
+        return (f32(1.0) + f32(0.1) * rng.standard_normal(R, dtype=f32)).astype(f32)
 
     def phase():
-        return (rng.random(r, dtype=f32) * f32(2.0 * math.pi)).astype(f32)
+        return (rng.random(R, dtype=f32) * f32(2.0 * math.pi)).astype(f32)
 
     a = {}
     a["x"] = normal((T, d_in), 1.0)
     a["W"] = normal((d_in, d_out), w_var)
     a["b"] = (rng.standard_normal(d_out, dtype=f32) * f32(bias_std)).astype(f32)
-    a["W_down"] = normal((d_in, r), d_var)
+    a["W_down"] = normal((d_in, R), d_var)
     a["omega1"] = freq()
     a["phi1"] = phase()
-    a["M"] = normal((r, r), m_var)
+    a["M"] = normal((r, r) if G == 1 else (G, r, r), m_var)
     a["omega2"] = freq()
     a["phi2"] = phase()
-    a["W_up"] = normal((r, d_out), u_var)
+    a["W_up"] = normal((R, d_out // G), u_var)
     a["dy"] = normal((T, d_out), 1.0)
     if dtype == "bf16":
         for k in STORAGE:
             a[k] = round_bf16(a[k])
-    return Projection(name, T, d_in, d_out, r, dtype, a)
+    return Projection(name, T, d_in, d_out, r, dtype, a, G)
 
 
 # ---------------------------------------------------------------------------
@@ -153,13 +162,32 @@ WORKLOADS: Dict[str, dict] = {
                                                                  ("v", 2048, 2048), ("o", 2048, 2048),
                                                                  ("ffn_up", 2048, 8192),
                                                                  ("ffn_down", 8192, 2048))]),
+    # the same four blocks with Q, K and V as one grouped call per block (one
+    # shared x, three branches): four projections per block
+    "llm1p5b_stack4_r128_gqkv": dict(T=32768, r=128, dtype="bf16",
+                                     projections=[(f"b{blk}_{p}", di, do, g)
+                                                  for blk in range(4)
+                                                  for (p, di, do, g) in (("qkv", 2048, 6144, 3),
+                                                                         ("o", 2048, 2048, 1),
+                                                                         ("ffn_up", 2048, 8192, 1),
+                                                                         ("ffn_down", 8192, 2048, 1))]),
 }
 
 
+def _proj(entry):
+    """(name, d_in, d_out, groups) of a workload's projection entry."""
+    return (entry[0], entry[1], entry[2], entry[3] if len(entry) > 3 else 1)
+
+
 def workload_shapes(name: str) -> List[Tuple[str, int, int, int, int]]:
-    """[(projection name, T, d_in, d_out, r)] of a workload."""
+    """[(projection name, T, d_in, d_out, r)] of a workload (r per group)."""
     w = WORKLOADS[name]
-    return [(p, w["T"], di, do, w["r"]) for (p, di, do) in w["projections"]]
+    return [(p, w["T"], di, do, w["r"]) for (p, di, do, _) in map(_proj, w["projections"])]
+
+
+def workload_groups(name: str) -> List[int]:
+    """Branch groups of each projection of a workload."""
+    return [_proj(e)[3] for e in WORKLOADS[name]["projections"]]
 
 
 def draw_workload_projection(name: str, index: int, seed: int = 0, T: Optional[int] = None,
@@ -169,8 +197,9 @@ def draw_workload_projection(name: str, index: int, seed: int = 0, T: Optional[i
     ``T`` overrides the token count (a prefix sample of the workload's rows is
     not the same draw; use the full T for full-size checks)."""
     w = WORKLOADS[name]
-    p, di, do = w["projections"][index]
+    p, di, do, G = _proj(w["projections"][index])
     kw = dict(w.get("var", {}))
     kw.update(overrides)
+    kw.setdefault("groups", G)
     return draw_projection(f"{name}/{p}", w["T"] if T is None else T, di, do, w["r"],
                            w["dtype"], seed + index, **kw)

@@ -83,6 +83,8 @@ class noble_linear_desc(ctypes.Structure):
         ("r", ctypes.c_int64),
         ("dtype", ctypes.c_int32),
         ("activation", ctypes.c_int32),
+        ("groups", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 
@@ -135,14 +137,15 @@ def noble_status_string(status: int) -> str:
     return lib().noble_status_string(int(status)).decode()
 
 
-def make_desc(T: int, d_in: int, d_out: int, r: int, dtype: int, activation=0) -> noble_linear_desc:
-    return noble_linear_desc(int(T), int(d_in), int(d_out), int(r), int(dtype), activation_code(activation))
+def make_desc(T: int, d_in: int, d_out: int, r: int, dtype: int, activation=0, groups: int = 1) -> noble_linear_desc:
+    return noble_linear_desc(int(T), int(d_in), int(d_out), int(r), int(dtype), activation_code(activation),
+                             int(groups), 0)
 
 
 def noble_linear_workspace_size(T: int, d_in: int, d_out: int, r: int, dtype: int,
-                                activation=0) -> Tuple[int, int]:
-    """(reserve_bytes, scratch_bytes) for the problem."""
-    d = make_desc(T, d_in, d_out, r, dtype, activation)
+                                activation=0, groups: int = 1) -> Tuple[int, int]:
+    """(reserve_bytes, scratch_bytes) for the problem (r: rank per group)."""
+    d = make_desc(T, d_in, d_out, r, dtype, activation, groups)
     res, scr = ctypes.c_size_t(0), ctypes.c_size_t(0)
     st = lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(res), ctypes.byref(scr))
     if st != 0:
@@ -189,29 +192,42 @@ def _stream(stream) -> Optional[int]:
     return s.cuda_stream or None
 
 
+def _branch_shapes(d_in, d_out, R, groups):
+    """Shapes of W_down, the [R] vectors, M and W_up for ``groups`` groups of
+    total rank R (M is [r, r] for one group, [G, r, r] otherwise)."""
+    G = int(groups)
+    if R % G or d_out % G:
+        raise ValueError(f"d_out ({d_out}) and the total rank ({R}) must divide into {G} groups")
+    r = R // G
+    return dict(W_down=(d_in, R), vec=(R,), M=(r, r) if G == 1 else (G, r, r), W_up=(R, d_out // G)), r
+
+
 def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
-                     stream=None, activation=0) -> None:
+                     stream=None, activation=0, groups: int = 1) -> None:
     """Enqueue the forward on ``stream`` (default: torch's current stream).
 
     Storage tensors (x, W, W_down, M, W_up, y) share one dtype (bf16 or f32);
     b, omega*, phi* are float32.  reserve/scratch are byte (uint8) tensors of
     at least the sizes from noble_linear_workspace_size.  With r = 0 pass None
     for the branch tensors; one-application activations do not read M,
-    omega2, phi2 (None allowed).
+    omega2, phi2 (None allowed).  ``groups`` > 1: W_down [d_in, G r], M
+    [G, r, r], the vectors [G r], W_up [G r, d_out / G] (one branch per block
+    of d_out / G output columns).
     """
     torch = _torch()
     T, d_in = x.shape
     d_out = W.shape[1]
-    r = 0 if W_down is None else W_down.shape[1]
+    R = 0 if W_down is None else W_down.shape[1]
+    sh, r = _branch_shapes(d_in, d_out, R, groups)
     dt = _dtype_code(x)
     sd = x.dtype
     f32 = torch.float32
-    d = make_desc(T, d_in, d_out, r, dt, activation)
+    d = make_desc(T, d_in, d_out, r, dt, activation, groups)
     args = [
         _ptr(x, "x", sd, (T, d_in)), _ptr(W, "W", sd, (d_in, d_out)), _ptr(b, "b", f32, (d_out,)),
-        _ptr(W_down, "W_down", sd, (d_in, r)), _ptr(omega1, "omega1", f32, (r,)), _ptr(phi1, "phi1", f32, (r,)),
-        _ptr(M, "M", sd, (r, r)), _ptr(omega2, "omega2", f32, (r,)), _ptr(phi2, "phi2", f32, (r,)),
-        _ptr(W_up, "W_up", sd, (r, d_out)), _ptr(y, "y", sd, (T, d_out)),
+        _ptr(W_down, "W_down", sd, sh["W_down"]), _ptr(omega1, "omega1", f32, sh["vec"]),
+        _ptr(phi1, "phi1", f32, sh["vec"]), _ptr(M, "M", sd, sh["M"]), _ptr(omega2, "omega2", f32, sh["vec"]),
+        _ptr(phi2, "phi2", f32, sh["vec"]), _ptr(W_up, "W_up", sd, sh["W_up"]), _ptr(y, "y", sd, (T, d_out)),
         _ptr(reserve, "reserve"), _ptr(scratch, "scratch"),
     ]
     nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
@@ -222,7 +238,7 @@ def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, re
 
 def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve,
                      dx, dW, db, dW_down, dM, dW_up, domega1, dphi1, domega2, dphi2, scratch,
-                     stream=None, activation=0) -> None:
+                     stream=None, activation=0, groups: int = 1) -> None:
     """Enqueue the backward on ``stream``; overwrites every gradient tensor.
 
     dx has the storage dtype; dW, db (optional), dW_down, dM, dW_up and the
@@ -233,21 +249,23 @@ def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, rese
     torch = _torch()
     T, d_in = x.shape
     d_out = W.shape[1]
-    r = 0 if W_down is None else W_down.shape[1]
+    R = 0 if W_down is None else W_down.shape[1]
+    sh, r = _branch_shapes(d_in, d_out, R, groups)
     dt = _dtype_code(x)
     sd = x.dtype
     f32 = torch.float32
-    d = make_desc(T, d_in, d_out, r, dt, activation)
+    d = make_desc(T, d_in, d_out, r, dt, activation, groups)
+    v = sh["vec"]
     args = [
         _ptr(dy, "dy", sd, (T, d_out)), _ptr(x, "x", sd, (T, d_in)), _ptr(W, "W", sd, (d_in, d_out)),
-        _ptr(W_down, "W_down", sd, (d_in, r)), _ptr(omega1, "omega1", f32, (r,)), _ptr(phi1, "phi1", f32, (r,)),
-        _ptr(M, "M", sd, (r, r)), _ptr(omega2, "omega2", f32, (r,)), _ptr(phi2, "phi2", f32, (r,)),
-        _ptr(W_up, "W_up", sd, (r, d_out)), _ptr(reserve, "reserve"),
+        _ptr(W_down, "W_down", sd, sh["W_down"]), _ptr(omega1, "omega1", f32, v), _ptr(phi1, "phi1", f32, v),
+        _ptr(M, "M", sd, sh["M"]), _ptr(omega2, "omega2", f32, v), _ptr(phi2, "phi2", f32, v),
+        _ptr(W_up, "W_up", sd, sh["W_up"]), _ptr(reserve, "reserve"),
         _ptr(dx, "dx", sd, (T, d_in)), _ptr(dW, "dW", f32, (d_in, d_out)), _ptr(db, "db", f32, (d_out,)),
-        _ptr(dW_down, "dW_down", f32, (d_in, r)), _ptr(dM, "dM", f32, (r, r)),
-        _ptr(dW_up, "dW_up", f32, (r, d_out)),
-        _ptr(domega1, "domega1", f32, (r,)), _ptr(dphi1, "dphi1", f32, (r,)),
-        _ptr(domega2, "domega2", f32, (r,)), _ptr(dphi2, "dphi2", f32, (r,)),
+        _ptr(dW_down, "dW_down", f32, sh["W_down"]), _ptr(dM, "dM", f32, sh["M"]),
+        _ptr(dW_up, "dW_up", f32, sh["W_up"]),
+        _ptr(domega1, "domega1", f32, v), _ptr(dphi1, "dphi1", f32, v),
+        _ptr(domega2, "domega2", f32, v), _ptr(dphi2, "dphi2", f32, v),
         _ptr(scratch, "scratch"),
     ]
     nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
@@ -269,10 +287,11 @@ def noble_recipe_defaults(**overrides) -> noble_recipe:
     return rc
 
 
-def noble_lr_multipliers(d_in: int, d_out: int, r: int, recipe: Optional[noble_recipe] = None) -> dict:
+def noble_lr_multipliers(d_in: int, d_out: int, r: int, recipe: Optional[noble_recipe] = None,
+                         groups: int = 1) -> dict:
     """Learning-rate multipliers of W, b, W_down, W_up, M, omega, phi."""
     rc = noble_recipe_defaults() if recipe is None else recipe
-    d = make_desc(0, d_in, d_out, r, NOBLE_BF16)
+    d = make_desc(0, d_in, d_out, r, NOBLE_BF16, 0, groups)
     out = noble_lr_mults()
     st = lib().noble_lr_multipliers(ctypes.byref(d), ctypes.byref(rc), ctypes.byref(out))
     if st != 0:
@@ -281,23 +300,27 @@ def noble_lr_multipliers(d_in: int, d_out: int, r: int, recipe: Optional[noble_r
 
 
 def noble_init_params(W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, seed: int,
-                      recipe: Optional[noble_recipe] = None, stream=None) -> None:
+                      recipe: Optional[noble_recipe] = None, stream=None, groups: int = 1) -> None:
     """Fill the layer's parameter tensors on the device from ``seed``
     (None skips a tensor).  Storage tensors share one dtype (bf16 or f32)."""
     torch = _torch()
     rc = noble_recipe_defaults() if recipe is None else recipe
     d_in, d_out = W.shape
-    r = 0
-    for t, dim in ((W_down, 1), (W_up, 0), (M, 0), (omega1, 0), (phi1, 0), (omega2, 0), (phi2, 0)):
+    R = 0
+    for t, dim in ((W_down, 1), (W_up, 0), (omega1, 0), (phi1, 0), (omega2, 0), (phi2, 0)):
         if t is not None:
-            r = t.shape[dim]
+            R = t.shape[dim]
             break
+    if R == 0 and M is not None:
+        R = M.shape[-1] * groups
+    sh, r = _branch_shapes(d_in, d_out, R, groups)
     dt = _dtype_code(W)
     sd, f32 = W.dtype, torch.float32
-    d = make_desc(0, d_in, d_out, r, dt)
-    args = [_ptr(W, "W", sd, (d_in, d_out)), _ptr(b, "b", f32, (d_out,)), _ptr(W_down, "W_down", sd, (d_in, r)),
-            _ptr(omega1, "omega1", f32, (r,)), _ptr(phi1, "phi1", f32, (r,)), _ptr(M, "M", sd, (r, r)),
-            _ptr(omega2, "omega2", f32, (r,)), _ptr(phi2, "phi2", f32, (r,)), _ptr(W_up, "W_up", sd, (r, d_out))]
+    d = make_desc(0, d_in, d_out, r, dt, 0, groups)
+    v = sh["vec"]
+    args = [_ptr(W, "W", sd, (d_in, d_out)), _ptr(b, "b", f32, (d_out,)), _ptr(W_down, "W_down", sd, sh["W_down"]),
+            _ptr(omega1, "omega1", f32, v), _ptr(phi1, "phi1", f32, v), _ptr(M, "M", sd, sh["M"]),
+            _ptr(omega2, "omega2", f32, v), _ptr(phi2, "phi2", f32, v), _ptr(W_up, "W_up", sd, sh["W_up"])]
     st = lib().noble_init_params(ctypes.byref(d), ctypes.byref(rc), int(seed) & (2 ** 64 - 1), *args,
                                  _stream(stream))
     if st != 0:
@@ -326,10 +349,10 @@ def param_groups(params: dict, lr: float, d_in: int, d_out: int, r: int,
 
 # ------------------------------------------------------------ conveniences --
 
-def alloc_workspace(T, d_in, d_out, r, dtype_code, device="cuda"):
+def alloc_workspace(T, d_in, d_out, r, dtype_code, device="cuda", groups: int = 1):
     """(reserve, scratch) uint8 tensors of the required sizes."""
     torch = _torch()
-    res, scr = noble_linear_workspace_size(T, d_in, d_out, r, dtype_code)
+    res, scr = noble_linear_workspace_size(T, d_in, d_out, r, dtype_code, groups=groups)
     return (torch.empty(max(res, 16), dtype=torch.uint8, device=device),
             torch.empty(max(scr, 16), dtype=torch.uint8, device=device))
 

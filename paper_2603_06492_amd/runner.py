@@ -43,6 +43,7 @@ class DeviceProblem:
         self.sdt = torch.bfloat16 if p.dtype == "bf16" else torch.float32
         self.code = noble.NOBLE_BF16 if p.dtype == "bf16" else noble.NOBLE_F32
         self.r = p.r if branch else 0
+        self.G = getattr(p, "groups", 1) if branch else 1
         self.canary = canary
         self.activation = activation
         self.act = noble.activation_code(activation)
@@ -66,6 +67,8 @@ class DeviceProblem:
         for k in unused:
             self.t[k] = None
         T, di, do, r = p.T, p.d_in, p.d_out, self.r
+        G = self.G
+        R, dog = G * r, do // G
         f32 = torch.float32
         self.y = self._out((T, do), self.sdt)
         self.g = {
@@ -74,15 +77,16 @@ class DeviceProblem:
             "db": self._out((do,), f32) if with_db else None,
         }
         if r > 0:
-            for n, s in (("dW_down", (di, r)), ("dM", (r, r)), ("dW_up", (r, do)), ("domega1", (r,)),
-                         ("dphi1", (r,)), ("domega2", (r,)), ("dphi2", (r,))):
+            mshape = (r, r) if G == 1 else (G, r, r)
+            for n, s in (("dW_down", (di, R)), ("dM", mshape), ("dW_up", (R, dog)), ("domega1", (R,)),
+                         ("dphi1", (R,)), ("domega2", (R,)), ("dphi2", (R,))):
                 self.g[n] = self._out(s, f32)
             for n in unused:
                 self.g["d" + n] = None
         else:
             for n in ("dW_down", "dM", "dW_up", "domega1", "dphi1", "domega2", "dphi2"):
                 self.g[n] = None
-        res, scr = noble.noble_linear_workspace_size(T, di, do, r, self.code, self.act)
+        res, scr = noble.noble_linear_workspace_size(T, di, do, r, self.code, self.act, G)
         self.reserve = torch.empty(max(res, 16), dtype=torch.uint8, device=device)
         self.scratch = torch.empty(max(scr, 16), dtype=torch.uint8, device=device)
 
@@ -108,7 +112,7 @@ class DeviceProblem:
         t = self.t
         noble.noble_linear_fwd(t["x"], t["W"], t["b"], t["W_down"], t["omega1"], t["phi1"], t["M"],
                                t["omega2"], t["phi2"], t["W_up"], self.y, self.reserve, self.scratch,
-                               stream=stream, activation=self.act)
+                               stream=stream, activation=self.act, groups=self.G)
 
     def bwd(self, stream=None):
         t, g = self.t, self.g
@@ -116,7 +120,7 @@ class DeviceProblem:
                                t["omega2"], t["phi2"], t["W_up"], self.reserve,
                                g["dx"], g["dW"], g["db"], g["dW_down"], g["dM"], g["dW_up"],
                                g["domega1"], g["dphi1"], g["domega2"], g["dphi2"], self.scratch,
-                               stream=stream, activation=self.act)
+                               stream=stream, activation=self.act, groups=self.G)
 
     def outputs(self, rows: Optional[np.ndarray] = None, dw_rows: Optional[np.ndarray] = None):
         """Host float64 copies of y and every gradient (optionally row-sampled)."""

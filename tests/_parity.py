@@ -41,6 +41,16 @@ def oracle_outputs(p, *, with_bias=True, branch=True, rows=None, dw_rows=None, a
               "omega2": z(0), "phi2": z(0), "W_up": z((0, p.d_out))}
     b = a["b"] if with_bias else None
     x = a["x"] if rows is None else a["x"][rows]
+    G = getattr(p, "groups", 1)
+    if branch and G > 1:
+        Y, _ = oracle.forward_grouped(x, a["W"], b, br["W_down"], br["omega1"], br["phi1"], br["M"],
+                                      br["omega2"], br["phi2"], br["W_up"], G, activation=activation,
+                                      mix_round=mix_round)
+        g = oracle.backward_grouped(a["dy"], a["x"], a["W"], br["W_down"], br["omega1"], br["phi1"], br["M"],
+                                    br["omega2"], br["phi2"], br["W_up"], G, dx_rows=rows, dW_rows=dw_rows,
+                                    activation=activation, mix_round=mix_round)
+        g["y"] = Y
+        return g
     Y, _ = oracle.forward(x, a["W"], b, br["W_down"], br["omega1"], br["phi1"], br["M"],
                           br["omega2"], br["phi2"], br["W_up"], activation=activation, mix_round=mix_round)
     g = oracle.backward(a["dy"], a["x"], a["W"], br["W_down"], br["omega1"], br["phi1"], br["M"],

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
     L = noble.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.noble_abi_version() == 2
+    assert L.noble_abi_version() == 3
 
 
 def test_status_strings():
@@ -44,18 +44,19 @@ def test_status_strings():
     assert "UNKNOWN" in noble.noble_status_string(99)
 
 
-def _ws(T, di, do, r, dt):
-    d = noble.make_desc(T, di, do, r, dt)
+def _ws(T, di, do, r, dt, groups=1):
+    d = noble.make_desc(T, di, do, r, dt, 0, groups)
     a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
     st = noble.lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(a), ctypes.byref(b))
     return st, a.value, b.value
 
 
-def _proj_split(T, K):
-    """K pieces of the bf16 rank projection: workgroups of 128 tokens until
-    256 are in flight, at least 4 chunks of 64 per piece, at most 8 pieces."""
+def _proj_split(T, K, J=1):
+    """K pieces of the bf16 rank projection run as J jobs (group, 128-rank
+    block): workgroups of 128 tokens until 256 are in flight, at least 4
+    chunks of 64 per piece, at most 8 pieces."""
     blocks, nkc, s = -(-T // 128), -(-K // 64), 1
-    while blocks * s < 256 and 2 * s * 4 <= nkc and 2 * s <= 8:
+    while blocks * s * J < 256 and 2 * s * 4 <= nkc and 2 * s <= 8:
         s *= 2
     return s
 
@@ -123,14 +124,46 @@ def test_workspace_sizes():
     assert noble.lib().noble_linear_workspace_size(None, None, None) == NULL
 
 
+def test_workspace_sizes_grouped_and_rank_256():
+    """Grouped layers size every rank-side region by R = G r, and the
+    projection's split counts one job per (group, 128-rank block)."""
+    T, di, do, r, G = 8192, 2048, 6144, 128, 3
+    st, res, scr = _ws(T, di, do, r, noble.NOBLE_BF16, G)
+    R = G * r
+    S = max(_proj_split(T, di, G), _proj_split(T, do // G, G))
+    assert S == 2   # 64 token blocks x 3 jobs = 192 < 256 workgroups: split K in two
+    assert st == OK and res == 4 * T * R
+    assert scr == 4 * T * R * 2 + _align(S * T * R * 4) + _wgrad_bytes(T, di, do, r, 64)
+    T, di, do, r = 300, 264, 200, 256
+    st, res, scr = _ws(T, di, do, r, noble.NOBLE_BF16)
+    S = max(_proj_split(T, di, 2), _proj_split(T, do, 2))
+    assert st == OK and res == 4 * T * r
+    assert scr == 4 * _align(T * r * 2) + _align(S * T * r * 4)
+
+
 @pytest.mark.parametrize("shape,code", [
     ((-1, 64, 64, 8), SHAPE), ((16, 0, 64, 8), SHAPE), ((16, 12, 64, 8), SHAPE),
     ((16, 64, 60, 8), SHAPE), ((16, 64, 64, 4), SHAPE), ((16, 64, 64, 12), SHAPE),
-    ((16, 64, 64, 136), SHAPE), ((16, 64, 64, -8), SHAPE), ((16, 64, 64, 128), OK),
+    ((16, 64, 64, 136), OK), ((16, 64, 64, 256), OK), ((16, 64, 64, 264), SHAPE),
+    ((16, 64, 64, -8), SHAPE), ((16, 64, 64, 128), OK),
     ((16, 64, 64, 0), OK), ((1 << 31, 64, 64, 8), SHAPE),
 ])
 def test_shape_validation(shape, code):
     assert _ws(*shape, noble.NOBLE_BF16)[0] == code
+
+
+def test_f32_rank_limit():
+    assert _ws(16, 64, 64, 128, noble.NOBLE_F32)[0] == OK
+    assert _ws(16, 64, 64, 136, noble.NOBLE_F32)[0] == SHAPE
+
+
+@pytest.mark.parametrize("do,groups,code", [
+    (96, 3, OK), (96, 4, OK), (104, 4, SHAPE), (128, 4, OK), (64, 0, OK), (64, 1, OK), (80, 5, SHAPE),
+    (64, -1, SHAPE), (72, 3, OK), (64, 3, SHAPE),
+])
+def test_group_validation(do, groups, code):
+    """1 to 4 groups (0 counts as 1), d_out / G a multiple of 8."""
+    assert _ws(16, 64, do, 16, noble.NOBLE_BF16, groups)[0] == code
 
 
 def test_dtype_validation():

@@ -50,6 +50,11 @@ MUTATIONS = {
     "dM_uses_unrounded_C1": ("out[\"dM\"] = fw[\"C1m\"].T @ dH2", "out[\"dM\"] = fw[\"C1\"].T @ dH2"),
     "mix_round_applied_to_H2": ("    A2 = H2 * _f64(omega2) + _f64(phi2)          # w2 (.) h2 + p2",
                                 "    A2 = (H2 if mix_round is None else mix_round(H2)) * _f64(omega2) + _f64(phi2)"),
+    # grouped layers
+    "grouped_dx_last_block_only": ('out = {"dx": sum(q["dx"] for q in parts),', 'out = {"dx": parts[-1]["dx"],'),
+    "grouped_rank_slice_fixed": ("rs = slice(g * r, (g + 1) * r)", "rs = slice(0, r)"),
+    "grouped_first_M_only": ("(_f64(M) if G == 1 else _f64(M)[g])", "(_f64(M) if G == 1 else _f64(M)[0])"),
+    "grouped_column_block_shifted": ("return (slice(g * dg, (g + 1) * dg),", "return (slice((G - 1 - g) * dg, (G - g) * dg),"),
 }
 
 
@@ -128,7 +133,34 @@ def _battery_passes(mod):
                 fd = (loss(qp) - loss(qm)) / 2e-6
                 if abs(fd - g[gn][idx]) > 1e-6 * max(1.0, abs(g[gn][idx])):
                     return False
-    return _mix_round_pin(mod)
+    return _mix_round_pin(mod) and _grouped_pin(mod)
+
+
+def _grouped_pin(mod):
+    """A 3-group layer against the single layer with block-diagonal M and
+    W_up (the one-branch oracle, checked by the rest of the battery)."""
+    G, r, dg = 3, 2, 4
+    q = inp.draw_projection("grp", 5, 6, G * dg, r, "f32", 59, bias_std=0.5, groups=G)
+    p = {k: v.astype(np.float64) for k, v in q.arrays.items()}
+    R = G * r
+    Mb, Ub = np.zeros((R, R)), np.zeros((R, G * dg))
+    for g in range(G):
+        Mb[g * r:(g + 1) * r, g * r:(g + 1) * r] = p["M"][g]
+        Ub[g * r:(g + 1) * r, g * dg:(g + 1) * dg] = p["W_up"][g * r:(g + 1) * r]
+    a = (p["W_down"], p["omega1"], p["phi1"])
+    Yg, _ = mod.forward_grouped(p["x"], p["W"], p["b"], *a, p["M"], p["omega2"], p["phi2"], p["W_up"], G)
+    Ys, _ = good.forward(p["x"], p["W"], p["b"], *a, Mb, p["omega2"], p["phi2"], Ub)
+    if not np.allclose(Yg, Ys, rtol=0, atol=1e-12):
+        return False
+    gg = mod.backward_grouped(p["dy"], p["x"], p["W"], *a, p["M"], p["omega2"], p["phi2"], p["W_up"], G)
+    gs = good.backward(p["dy"], p["x"], p["W"], *a, Mb, p["omega2"], p["phi2"], Ub)
+    for k in ("dx", "dW", "db", "dW_down", "domega1", "dphi2"):
+        if not np.allclose(gg[k], gs[k], rtol=0, atol=1e-12):
+            return False
+    for g in range(G):
+        if not np.allclose(gg["dM"][g], gs["dM"][g * r:(g + 1) * r, g * r:(g + 1) * r], rtol=0, atol=1e-12):
+            return False
+    return True
 
 
 def _mix_round_pin(mod):

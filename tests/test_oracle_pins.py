@@ -532,3 +532,87 @@ def test_mix_round_identity_is_exact():
     g1 = oracle.backward(p["dy"], *(a for i, a in enumerate(args) if i != 2), mix_round=lambda a: a)
     for k in GRADS:
         np.testing.assert_array_equal(g0[k], g1[k])
+
+
+# ------------------------------------------------------------ grouped layers --
+
+def _block_diagonal(p, G):
+    """The grouped layer's parameters as one rank-G r layer: M and W_up block
+    diagonal (zeros off the blocks), everything else as is."""
+    R = p["W_down"].shape[1]
+    r, dg = R // G, p["W"].shape[1] // G
+    Mb = np.zeros((R, R))
+    Ub = np.zeros((R, G * dg))
+    for g in range(G):
+        Mb[g * r:(g + 1) * r, g * r:(g + 1) * r] = p["M"][g]
+        Ub[g * r:(g + 1) * r, g * dg:(g + 1) * dg] = p["W_up"][g * r:(g + 1) * r]
+    return Mb, Ub
+
+
+@pytest.mark.parametrize("act", ["cosnet", "gelu_m", "tanh"])
+def test_grouped_layer_is_block_diagonal_single_layer(act):
+    """G branches on G column blocks of one x equal one rank-G r branch whose
+    M and W_up are block diagonal: same y, dx, dW, db, dW_down and vector
+    gradients; dM and dW_up are the diagonal blocks of the single layer's."""
+    G = 3
+    q = inp.draw_projection("grp", 7, 10, 3 * 6, 4, "f32", 43, bias_std=0.5, groups=G)
+    p = {k: v.astype(np.float64) for k, v in q.arrays.items()}
+    Mb, Ub = _block_diagonal(p, G)
+    args = (p["W_down"], p["omega1"], p["phi1"])
+    Yg, Hg = oracle.forward_grouped(p["x"], p["W"], p["b"], *args, p["M"], p["omega2"], p["phi2"], p["W_up"], G,
+                                    activation=act)
+    Ys, Hs = oracle.forward(p["x"], p["W"], p["b"], *args, Mb, p["omega2"], p["phi2"], Ub, activation=act)
+    np.testing.assert_allclose(Yg, Ys, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(Hg, Hs, rtol=0, atol=1e-12)
+    gg = oracle.backward_grouped(p["dy"], p["x"], p["W"], *args, p["M"], p["omega2"], p["phi2"], p["W_up"], G,
+                                 activation=act)
+    gs = oracle.backward(p["dy"], p["x"], p["W"], *args, Mb, p["omega2"], p["phi2"], Ub, activation=act)
+    for k in ("dx", "dW", "db", "dW_down", "domega1", "dphi1", "domega2", "dphi2"):
+        if gs[k] is None:
+            assert gg[k] is None, k
+            continue
+        np.testing.assert_allclose(gg[k], gs[k], rtol=0, atol=1e-12, err_msg=k)
+    r, dg = 4, 6
+    for g in range(G):
+        np.testing.assert_allclose(gg["dW_up"][g * r:(g + 1) * r], gs["dW_up"][g * r:(g + 1) * r, g * dg:(g + 1) * dg],
+                                   rtol=0, atol=1e-12)
+        if gs["dM"] is not None:
+            np.testing.assert_allclose(gg["dM"][g], gs["dM"][g * r:(g + 1) * r, g * r:(g + 1) * r], rtol=0, atol=1e-12)
+
+
+def test_grouped_layer_with_one_group_is_the_layer():
+    q = inp.draw_projection("grp1", 6, 9, 8, 3, "f32", 47, bias_std=0.5)
+    p = {k: v.astype(np.float64) for k, v in q.arrays.items()}
+    a = (p["W_down"], p["omega1"], p["phi1"], p["M"], p["omega2"], p["phi2"], p["W_up"])
+    Y1, _ = oracle.forward_grouped(p["x"], p["W"], p["b"], *a, 1)
+    Y0, _ = oracle.forward(p["x"], p["W"], p["b"], *a)
+    np.testing.assert_array_equal(Y1, Y0)
+    g1 = oracle.backward_grouped(p["dy"], p["x"], p["W"], *a, 1)
+    g0 = oracle.backward(p["dy"], p["x"], p["W"], *a)
+    for k in GRADS:
+        np.testing.assert_array_equal(g1[k], g0[k])
+
+
+def test_grouped_gradients_match_central_differences():
+    G = 2
+    q = inp.draw_projection("grpfd", 4, 5, 2 * 3, 2, "f32", 53, bias_std=0.5, groups=G)
+    p = {k: v.astype(np.float64) for k, v in q.arrays.items()}
+    names = ("W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up")
+
+    def loss(qq):
+        Y, _ = oracle.forward_grouped(qq["x"], qq["W"], qq["b"], *(qq[n] for n in names), G)
+        return float(np.sum(qq["dy"] * Y))
+
+    g = oracle.backward_grouped(p["dy"], p["x"], p["W"], *(p[n] for n in names), G)
+    pairs = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "M": "dM", "W_up": "dW_up",
+             "omega1": "domega1", "phi1": "dphi1", "omega2": "domega2", "phi2": "dphi2"}
+    for pn, gn in pairs.items():
+        fd = np.zeros_like(p[pn])
+        for idx in np.ndindex(p[pn].shape):
+            qp, qm = dict(p), dict(p)
+            qp[pn] = p[pn].copy()
+            qm[pn] = p[pn].copy()
+            qp[pn][idx] += 1e-6
+            qm[pn][idx] -= 1e-6
+            fd[idx] = (loss(qp) - loss(qm)) / 2e-6
+        assert np.max(np.abs(fd - g[gn])) <= 1e-6 * max(1.0, float(np.max(np.abs(g[gn])))), gn
