@@ -10,6 +10,9 @@
 #include <atomic>
 #include <cmath>
 #include <cstring>
+#include <functional>
+#include <queue>
+#include <vector>
 
 #include "noble.h"
 #include "noble_gemm_dma.hpp"
@@ -99,11 +102,12 @@ int proj_split(int64_t T, int64_t K, int J) {
 }
 int proj_jobs(const noble_linear_desc* d) { return ngroups(d) * rank_blocks(d); }
 
-// Scratch layout, each part 256-byte aligned: four [T, r] storage-type
+// Scratch layout, each part 256-byte aligned: four [T, R] storage-type
 // regions C1, C2, dH2, dH (the forward uses only C2); on the bf16 path the
-// float32 projection partials [S][T][r] for the larger split of the forward
-// and backward projections; then the float32 split-K partials of the
-// weight-gradient products (backward only).
+// float32 projection partials [S][T][R] for the larger split of the forward
+// and backward projections and the copies of the frequency / phase gradients
+// (backward); then the float32 split-K partials of the weight-gradient
+// products (backward only).
 size_t scratch_region(const noble_linear_desc* d) {
     return align_up((size_t)d->T * rank_total(d) * elt_size(d));
 }
@@ -113,9 +117,15 @@ size_t partial_need(const noble_linear_desc* d) {
     const int s = std::max(proj_split(d->T, d->d_in, J), proj_split(d->T, group_dout(d), J));
     return align_up((size_t)s * d->T * rank_total(d) * 4);
 }
+// bf16 backward: kChainCopies copies of the four frequency / phase gradient
+// vectors, [4][kChainCopies][R] float32.
+size_t copies_need(const noble_linear_desc* d) {
+    if (d->r == 0 || d->dtype != NOBLE_BF16) return 0;
+    return align_up((size_t)4 * kChainCopies * rank_total(d) * 4);
+}
 size_t wgrad_need(const noble_linear_desc* d);
 size_t scratch_need(const noble_linear_desc* d) {
-    return (d->r > 0 ? 4 * scratch_region(d) + partial_need(d) : 0) + wgrad_need(d);
+    return (d->r > 0 ? 4 * scratch_region(d) + partial_need(d) + copies_need(d) : 0) + wgrad_need(d);
 }
 size_t reserve_need(const noble_linear_desc* d) { return (size_t)d->T * rank_total(d) * 4; }
 
@@ -213,6 +223,27 @@ struct Batch {
     }
 };
 
+// Makespan of a grouped launch, in microseconds of the cost model: its
+// workgroups, given as (count, K chunks each) in launch order, are dispatched
+// in that order to whichever of the 256 CUs frees first (one 256 x 256
+// workgroup per CU).  A workgroup costs kWgFixed plus kWgChunk per 64-token
+// chunk (fit to the measured time of the forward GEMM against K: prologue,
+// epilogue stores and ramp are about 12 us per tile, a chunk 1.45 us).
+double launch_makespan(const std::vector<std::pair<int, int>>& wgs) {
+    constexpr double kWgFixed = 12.0, kWgChunk = 1.45;
+    std::priority_queue<double, std::vector<double>, std::greater<double>> cu;
+    for (int i = 0; i < 256; ++i) cu.push(0.0);
+    double end = 0.0;
+    for (const auto& g : wgs)
+        for (int i = 0; i < g.first; ++i) {
+            const double t = cu.top() + kWgFixed + kWgChunk * g.second;
+            cu.pop();
+            cu.push(t);
+            end = std::max(end, t);
+        }
+    return end;
+}
+
 // K split of one weight-gradient product (K = T tokens) whose pieces store
 // float32 partials that a reduction sums afterwards.  Cost model: the longest
 // CU's share of 64-element K chunks (waves of 256 workgroups) plus the partial
@@ -236,12 +267,22 @@ int choose_split_partials(int tiles, int nk, int64_t MN) {
 }
 
 // Split-K factor of the rank-gradient products (dW_down, dW_up, dM), whose
-// pieces add atomically into zeroed outputs of at most a few MB: enough
-// workgroups to give every CU one, at least 8 K chunks per piece.
-int choose_split_atomic(int tiles, int nk) {
-    int s = 1;
-    while (tiles * s < 256 && s * 2 * 8 <= nk) s *= 2;
-    return s;
+// pieces add atomically into zeroed outputs of at most a few MB.  They share
+// a launch with dW (dw_wgs workgroups of dw_chunks K chunks each, launched
+// first); one factor for all of them, the one that minimises the launch's
+// makespan under the list-scheduling model above, with at least 8 K chunks
+// per piece.  rank_tiles: the rank problems' 256 x 256 tile count.
+int choose_rank_split(int dw_wgs, int dw_chunks, int rank_tiles, int nk) {
+    int best = 1;
+    double best_t = 0.0;
+    for (int s = 1; s <= 16 && (s == 1 || s * 8 <= nk); s *= 2) {
+        const double t = launch_makespan({{dw_wgs, dw_chunks}, {rank_tiles * s, cdiv(nk, s)}});
+        if (s == 1 || t < best_t) {
+            best_t = t;
+            best = s;
+        }
+    }
+    return best;
 }
 
 // Split of dW over K = T: its pieces store float32 partials in the scratch
@@ -344,8 +385,9 @@ noble_status launch_proj(bool fwd, const noble_linear_desc* d, const void* A, co
 // bf16 path, step 2: the branch nonlinearity (forward or backward) from the
 // summed partials, one workgroup per (32 tokens, group).
 noble_status launch_branch(bool fwd, const noble_linear_desc* d, const ChainArgs& c, const float* P, int S,
-                           hipStream_t st) {
+                           hipStream_t st, float* copies = nullptr) {
     BranchArgs a{};
+    a.copies = copies;
     a.P = P;
     a.pstride = d->T * rank_total(d);
     a.S = S;
@@ -503,7 +545,8 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     constexpr int GBK = gemm_bk<E>();
     const int nkT = cdiv(T, GBK);
     const WgradPlan wp = plan_wgrad(T, din, dout, GBK);
-    float* wpart = reinterpret_cast<float*>(base + (r > 0 ? 4 * reg + partial_need(d) : 0));
+    float* copies = copies_need(d) ? reinterpret_cast<float*>(base + 4 * reg + partial_need(d)) : nullptr;
+    float* wpart = reinterpret_cast<float*>(base + (r > 0 ? 4 * reg + partial_need(d) + copies_need(d) : 0));
 
     ZeroList z{};
     auto zero = [&](float* p, int64_t n) {
@@ -519,10 +562,19 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         zero(dWd, din * R);
         zero(dM, G * r * r);
         zero(dWu, R * dog);
-        zero(dw1, R);
-        zero(dp1, R);
-        zero(dw2, R);
-        zero(dp2, R);
+        if (copies && T > 0) {
+            // the reduction of the copies overwrites dw1, dp1 (and dw2, dp2)
+            zero(copies, (int64_t)4 * kChainCopies * R);
+            if (!two) {
+                zero(dw2, R);
+                zero(dp2, R);
+            }
+        } else {
+            zero(dw1, R);
+            zero(dp1, R);
+            zero(dw2, R);
+            zero(dp2, R);
+        }
     }
     // On the bf16 path with a branch, the projection kernel does the zeroing.
     const bool zero_in_proj = sizeof(E) == 2 && r > 0 && T > 0;
@@ -556,7 +608,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             float* P = reinterpret_cast<float*>(base + 4 * reg);
             const int S = proj_split(T, dog, proj_jobs(d));
             NOBLE_TRY(launch_proj(false, d, dy, Wu, P, S, st, &z));
-            NOBLE_TRY(launch_branch(false, d, a, P, S, st));
+            NOBLE_TRY(launch_branch(false, d, a, P, S, st, copies));
         } else {
             for (int g = 0; g < G; ++g) {
                 ChainArgs c = group_chain(a, d, g, ES);
@@ -589,31 +641,47 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split,
                wp.split > 1 ? wpart : nullptr);
         if (r > 0) {
-            bt.add(xT, operand1(seg(dHs, R, T), R), (int)din, (int)R, nkT, dWd, R, true, nullptr, nullptr,
-                   choose_split_atomic(cdiv(din, kBM) * cdiv(R, kBN), nkT));
+            const int rank_tiles = cdiv(din, kBM) * cdiv(R, kBN) +
+                                   G * (cdiv(r, kBM) * cdiv(dog, kBN) + (two ? cdiv(r, kBM) * cdiv(r, kBN) : 0));
+            const int rs = choose_rank_split(cdiv(din, kBM) * cdiv(dout, kBN) * wp.split, cdiv(nkT, wp.split),
+                                             rank_tiles, nkT);
+            bt.add(xT, operand1(seg(dHs, R, T), R), (int)din, (int)R, nkT, dWd, R, true, nullptr, nullptr, rs);
             for (int g = 0; g < G; ++g) {
                 const int64_t c0 = g * r;
                 const Operand C2T = operand1(seg(C2s + c0 * (int64_t)ES, R, T), r);
                 const Operand dyg = operand1(seg(static_cast<const E*>(dy) + g * dog, dout, T), dog);
-                bt.add(C2T, dyg, (int)r, (int)dog, nkT, dWu + c0 * dog, dog, true, nullptr, nullptr,
-                       choose_split_atomic(cdiv(r, kBM) * cdiv(dog, kBN), nkT));
+                bt.add(C2T, dyg, (int)r, (int)dog, nkT, dWu + c0 * dog, dog, true, nullptr, nullptr, rs);
                 if (two) {
                     const Operand C1T = operand1(seg(C1s + c0 * (int64_t)ES, R, T), r);
                     const Operand dH2N = operand1(seg(dH2s + c0 * (int64_t)ES, R, T), r);
-                    bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM + g * r * r, r, true, nullptr, nullptr,
-                           choose_split_atomic(cdiv(r, kBM) * cdiv(r, kBN), nkT));
+                    bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM + g * r * r, r, true, nullptr, nullptr, rs);
                 }
             }
         }
         NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
-        if (wp.split > 1) {
-            ReduceList red{};
-            red.part[0] = wpart;
-            red.out[0] = dW;
-            red.n[0] = din * dout;
-            red.S[0] = wp.split;
-            red.count = 1;
-            hipLaunchKernelGGL(reduce_kernel, dim3(1024), dim3(256), 0, st, red);
+        // One reduction pass: the split-K partials of dW, and the copies of
+        // the frequency / phase gradients.
+        ReduceList red{};
+        auto reduce = [&](const float* part, float* out, int64_t n, int S) {
+            red.part[red.count] = part;
+            red.out[red.count] = out;
+            red.n[red.count] = n;
+            red.S[red.count] = S;
+            ++red.count;
+        };
+        if (wp.split > 1) reduce(wpart, dW, din * dout, wp.split);
+        if (copies) {
+            const int64_t arr = (int64_t)kChainCopies * R;
+            reduce(copies, dw1, R, kChainCopies);
+            reduce(copies + arr, dp1, R, kChainCopies);
+            if (two) {
+                reduce(copies + 2 * arr, dw2, R, kChainCopies);
+                reduce(copies + 3 * arr, dp2, R, kChainCopies);
+            }
+        }
+        if (red.count > 0) {
+            const int blocks = wp.split > 1 ? 1024 : std::max(1, cdiv(R, 4 * 256));
+            hipLaunchKernelGGL(reduce_kernel, dim3(blocks), dim3(256), 0, st, red);
             NOBLE_TRY(last_launch());
         }
     }

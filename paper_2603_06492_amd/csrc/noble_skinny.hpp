@@ -102,8 +102,16 @@ struct BranchArgs {
     float* dp1;
     float* dw2;
     float* dp2;
+    // Backward: when set, the four frequency / phase gradients are added into
+    // kChainCopies zeroed copies [4][kChainCopies][R] (dw1, dp1, dw2, dp2),
+    // copy = workgroup % kChainCopies, instead of into dw1 .. dp2; a
+    // reduction sums the copies afterwards.  Fewer workgroups then add into
+    // one address, which float atomics serialise on.
+    float* copies;
     int T, r, S, G, R, pad_;
 };
+
+constexpr int kChainCopies = 8;
 
 
 // One 64-element K chunk of the projection operands: 4 DMA instructions per
@@ -443,6 +451,19 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     const int r32 = lane & 31, h = lane >> 5;
     const ChainPos q = chain_pos(a);
     const int r = a.r, R = a.R;
+    // targets of the frequency / phase gradient sums
+    float* gw1 = a.dw1;
+    float* gp1 = a.dp1;
+    float* gw2 = a.dw2;
+    float* gp2 = a.dp2;
+    if (a.copies) {
+        float* c = a.copies + (int64_t)(blockIdx.x % kChainCopies) * R;
+        const int64_t arr = (int64_t)kChainCopies * R;
+        gw1 = c;
+        gp1 = c + arr;
+        gw2 = c + 2 * arr;
+        gp2 = c + 3 * arr;
+    }
 
     if constexpr (L2) m_dma<NT>(a.M + (int64_t)q.g * r * r, r, mt, wave, lane);
     const int col = 32 * wave + r32;
@@ -518,8 +539,8 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
         {
             const float sw = block_colsum(da2h2), sp = block_colsum(da2);
             if (h == 0 && cv) {
-                unsafeAtomicAdd(a.dw2 + gc, sw);
-                unsafeAtomicAdd(a.dp2 + gc, sp);
+                unsafeAtomicAdd(gw2 + gc, sw);
+                unsafeAtomicAdd(gp2 + gc, sp);
             }
         }
         __syncthreads();   // dH2 tile complete
@@ -542,8 +563,8 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     }
     const float sw = block_colsum(da1h), sp = block_colsum(da1);
     if (h == 0 && cv) {
-        unsafeAtomicAdd(a.dw1 + gc, sw);
-        unsafeAtomicAdd(a.dp1 + gc, sp);
+        unsafeAtomicAdd(gw1 + gc, sw);
+        unsafeAtomicAdd(gp1 + gc, sp);
     }
 }
 

@@ -81,6 +81,11 @@ def _split_partials(tiles, nk, mn):
     return bs
 
 
+def _copies(R):
+    """bf16 backward: 8 copies of the four frequency / phase gradient vectors."""
+    return _align(4 * 8 * R * 4)
+
+
 def _wgrad_bytes(T, di, do, r, bk):
     """dW partials: only dW stores partials (the rank gradients add
     atomically)."""
@@ -100,13 +105,14 @@ def test_workspace_sizes():
     # square 2048 projection: dW in 4 pieces
     wg = 4 * 2048 * 2048 * 4
     assert _wgrad_bytes(8192, 2048, 2048, 128, 64) == wg
-    assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + wg
+    assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + _copies(128) + wg
     st, res, scr = _ws(8192, 2048, 8192, 128, noble.NOBLE_BF16)
-    assert st == OK and scr == 4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + _wgrad_bytes(8192, 2048, 8192, 128, 64)
+    assert st == OK and scr == (4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + _copies(128)
+                                + _wgrad_bytes(8192, 2048, 8192, 128, 64))
     st, res, scr = _ws(300, 64, 1024, 40, noble.NOBLE_BF16)
     S = max(_proj_split(300, 64), _proj_split(300, 1024))
     assert _wgrad_bytes(300, 64, 1024, 40, 64) == 0   # 5 K chunks: no split
-    assert S == 4 and st == OK and scr == 4 * _align(300 * 40 * 2) + _align(S * 300 * 40 * 4)
+    assert S == 4 and st == OK and scr == 4 * _align(300 * 40 * 2) + _align(S * 300 * 40 * 4) + _copies(40)
     st, res, scr = _ws(256, 64, 64, 8, noble.NOBLE_F32)
     assert st == OK and res == 4 * 256 * 8 and scr == 4 * 256 * 8 * 4
     st, res, scr = _ws(1000, 64, 64, 0, noble.NOBLE_BF16)
@@ -120,7 +126,7 @@ def test_workspace_sizes():
     assert st == OK and res == 0
     # each region of the scratch is 256-byte aligned
     st, res, scr = _ws(3, 64, 64, 8, noble.NOBLE_BF16)
-    assert st == OK and scr == 4 * 256 + 256
+    assert st == OK and scr == 4 * 256 + 256 + _copies(8)
     assert noble.lib().noble_linear_workspace_size(None, None, None) == NULL
 
 
@@ -133,12 +139,12 @@ def test_workspace_sizes_grouped_and_rank_256():
     S = max(_proj_split(T, di, G), _proj_split(T, do // G, G))
     assert S == 2   # 64 token blocks x 3 jobs = 192 < 256 workgroups: split K in two
     assert st == OK and res == 4 * T * R
-    assert scr == 4 * T * R * 2 + _align(S * T * R * 4) + _wgrad_bytes(T, di, do, r, 64)
+    assert scr == 4 * T * R * 2 + _align(S * T * R * 4) + _copies(R) + _wgrad_bytes(T, di, do, r, 64)
     T, di, do, r = 300, 264, 200, 256
     st, res, scr = _ws(T, di, do, r, noble.NOBLE_BF16)
     S = max(_proj_split(T, di, 2), _proj_split(T, do, 2))
     assert st == OK and res == 4 * T * r
-    assert scr == 4 * _align(T * r * 2) + _align(S * T * r * 4)
+    assert scr == 4 * _align(T * r * 2) + _align(S * T * r * 4) + _copies(r)
 
 
 @pytest.mark.parametrize("shape,code", [
