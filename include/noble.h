@@ -103,7 +103,7 @@ typedef struct noble_linear_desc {
     int32_t dtype;  /* noble_dtype */
     int32_t activation; /* noble_activation */
     int32_t groups;     /* output column groups, each with its own branch (0 = 1) */
-    int32_t reserved;   /* must be 0 */
+    int32_t reserved;   /* must be 0 (NOBLE_ERR_BAD_SHAPE otherwise) */
 } noble_linear_desc;
 
 /* Sizes of the two caller-owned work buffers for `desc`.

@@ -36,6 +36,7 @@ noble_status check_desc(const noble_linear_desc* d) {
     if (!d) return NOBLE_ERR_NULL_ARG;
     if (d->dtype != NOBLE_BF16 && d->dtype != NOBLE_F32) return NOBLE_ERR_BAD_DTYPE;
     if (d->activation < NOBLE_ACT_COSNET || d->activation > NOBLE_ACT_GELU_M) return NOBLE_ERR_BAD_ACTIVATION;
+    if (d->reserved != 0) return NOBLE_ERR_BAD_SHAPE;
     if (d->T < 0 || d->T > kMaxTokens) return NOBLE_ERR_BAD_SHAPE;
     if (d->d_in < 8 || d->d_in % 8 || d->d_in > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
     if (d->d_out < 8 || d->d_out % 8 || d->d_out > kMaxDim) return NOBLE_ERR_BAD_SHAPE;

@@ -337,3 +337,11 @@ def test_two_layer_second_layer_pointers_required(act):
         ptrs = list(FAKE[:22])
         ptrs[BWD_ARGS.index(k)] = None
         assert _bwd(d, ptrs, scr) == NULL, k
+
+
+def test_reserved_field_must_be_zero():
+    d = noble.make_desc(16, 64, 64, 8, noble.NOBLE_BF16)
+    d.reserved = 1
+    a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert noble.lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(a), ctypes.byref(b)) == SHAPE
+    assert _fwd(d, FAKE[:13], 1 << 30) == SHAPE
