@@ -363,54 +363,133 @@ def _make_function():
     class NobleLinearFunction(torch.autograd.Function):
         """y = x W + b + sigma(x W_down) W_up with the libnoble kernels, sigma
         the CosNet or another bottleneck activation (``activation``, not
-        differentiated).  One-application activations take None for M,
-        omega2, phi2.  Parameter gradients are float32 (master-weight
-        convention)."""
+        differentiated), optionally grouped (``groups``).  One-application
+        activations take None for M, omega2, phi2.  Parameter gradients are
+        computed in float32 and returned in each parameter's dtype."""
 
         @staticmethod
-        def forward(ctx, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation=0):
+        def forward(ctx, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation=0, groups=1):
             T, d_in = x.shape
-            d_out, r = W.shape[1], W_down.shape[1]
+            d_out, R = W.shape[1], W_down.shape[1]
+            r = R // groups
             dt = _dtype_code(x)
             act = activation_code(activation)
-            reserve, scratch = alloc_workspace(T, d_in, d_out, r, dt, x.device)
+            reserve, scratch = alloc_workspace(T, d_in, d_out, r, dt, x.device, groups=groups)
             y = torch.empty((T, d_out), dtype=x.dtype, device=x.device)
             noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
-                             activation=act)
+                             activation=act, groups=groups)
             ctx.save_for_backward(x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve)
             ctx.has_bias = b is not None
             ctx.act = act
+            ctx.groups = groups
             return y
 
         @staticmethod
         def backward(ctx, dy):
             x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve = ctx.saved_tensors
             T, d_in = x.shape
-            d_out, r = W.shape[1], W_down.shape[1]
+            d_out, R = W.shape[1], W_down.shape[1]
+            G = ctx.groups
+            sh, r = _branch_shapes(d_in, d_out, R, G)
             dev, f32 = x.device, torch.float32
             two = two_layers(ctx.act)
             dy = dy.contiguous().to(x.dtype)
-            _, scratch = alloc_workspace(T, d_in, d_out, r, _dtype_code(x), dev)
+            _, scratch = alloc_workspace(T, d_in, d_out, r, _dtype_code(x), dev, groups=G)
             dx = torch.empty_like(x)
             g = {n: torch.empty(s, dtype=f32, device=dev) for n, s in (
-                ("dW", (d_in, d_out)), ("db", (d_out,)), ("dW_down", (d_in, r)), ("dM", (r, r)),
-                ("dW_up", (r, d_out)), ("domega1", (r,)), ("dphi1", (r,)), ("domega2", (r,)), ("dphi2", (r,)))}
+                ("dW", (d_in, d_out)), ("db", (d_out,)), ("dW_down", sh["W_down"]), ("dM", sh["M"]),
+                ("dW_up", sh["W_up"]), ("domega1", sh["vec"]), ("dphi1", sh["vec"]), ("domega2", sh["vec"]),
+                ("dphi2", sh["vec"]))}
             if not two:
                 g["dM"] = g["domega2"] = g["dphi2"] = None
             noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve,
                              dx, g["dW"], g["db"], g["dW_down"], g["dM"], g["dW_up"],
-                             g["domega1"], g["dphi1"], g["domega2"], g["dphi2"], scratch, activation=ctx.act)
-            dM = g["dM"].to(M.dtype) if two else None
+                             g["domega1"], g["dphi1"], g["domega2"], g["dphi2"], scratch, activation=ctx.act,
+                             groups=G)
+            dM = g["dM"].to(M.dtype) if (two and M is not None) else None
+            cast = lambda gr, p: None if p is None or gr is None else gr.to(p.dtype)
             return (dx, g["dW"].to(W.dtype), g["db"] if ctx.has_bias else None, g["dW_down"].to(W_down.dtype),
-                    g["domega1"], g["dphi1"], dM, g["domega2"], g["dphi2"],
-                    g["dW_up"].to(W_up.dtype), None)
+                    cast(g["domega1"], omega1), cast(g["dphi1"], phi1), dM, cast(g["domega2"], omega2),
+                    cast(g["dphi2"], phi2), g["dW_up"].to(W_up.dtype), None, None)
 
     return NobleLinearFunction
 
 
+def _make_module():
+    torch = _torch()
+    Function = __getattr__("NobleLinearFunction")
+
+    class NobleLinear(torch.nn.Module):
+        """A linear layer with the NOBLE branch, parameters initialised by the
+        paper's recipe (noble_init_params) and its learning-rate multipliers
+        available as optimizer groups (param_groups).  Input [..., d_in] in
+        the storage dtype; any leading dimensions are tokens.  The storage
+        parameters (W, W_down, M, W_up) have the storage dtype; b and the
+        frequency / phase vectors are float32.  r = 0 is the plain layer."""
+
+        def __init__(self, d_in, d_out, r, *, bias=True, dtype=None, device="cuda", activation="cosnet",
+                     groups=1, seed=0, recipe=None):
+            super().__init__()
+            dtype = torch.bfloat16 if dtype is None else dtype
+            if dtype not in (torch.bfloat16, torch.float32):
+                raise TypeError("dtype must be torch.bfloat16 or torch.float32")
+            self.d_in, self.d_out, self.r, self.groups = int(d_in), int(d_out), int(r), int(groups)
+            self.activation = activation
+            self.recipe = recipe
+            R = self.groups * self.r
+            sh, _ = _branch_shapes(self.d_in, self.d_out, R, self.groups)
+            f32 = torch.float32
+            P = lambda shape, dt: torch.nn.Parameter(torch.empty(shape, dtype=dt, device=device))
+            self.W = P((self.d_in, self.d_out), dtype)
+            self.b = P((self.d_out,), f32) if bias else None
+            two = two_layers(activation)
+            if self.r > 0:
+                self.W_down = P(sh["W_down"], dtype)
+                self.omega1 = P(sh["vec"], f32)
+                self.phi1 = P(sh["vec"], f32)
+                self.M = P(sh["M"], dtype) if two else None
+                self.omega2 = P(sh["vec"], f32) if two else None
+                self.phi2 = P(sh["vec"], f32) if two else None
+                self.W_up = P(sh["W_up"], dtype)
+            self.reset_parameters(seed)
+
+        def _branch(self):
+            if self.r == 0:
+                return (None,) * 7
+            return (self.W_down, self.omega1, self.phi1, self.M, self.omega2, self.phi2, self.W_up)
+
+        @torch.no_grad()
+        def reset_parameters(self, seed=0):
+            noble_init_params(self.W, self.b, *self._branch(), seed=seed, recipe=self.recipe, groups=self.groups)
+
+        def param_groups(self, lr):
+            """Optimizer parameter groups with the layer's learning-rate
+            multipliers (Sec. 3.3 Eqs. 3-4, App. A)."""
+            names = ("W_down", "omega1", "phi1", "M", "omega2", "phi2", "W_up")
+            params = {"W": self.W, "b": self.b}
+            params.update({n: t for n, t in zip(names, self._branch())})
+            return param_groups(params, lr, self.d_in, self.d_out // self.groups, self.r, self.recipe)
+
+        def forward(self, x):
+            lead = x.shape[:-1]
+            x2 = x.reshape(-1, self.d_in).contiguous()
+            if self.r == 0:
+                # plain layer: the same library call with no branch
+                y = Function.apply(x2, self.W, self.b, torch.empty((self.d_in, 0), dtype=x.dtype, device=x.device),
+                                   None, None, None, None, None, torch.empty((0, self.d_out), dtype=x.dtype,
+                                                                               device=x.device), 0, 1)
+            else:
+                y = Function.apply(x2, self.W, self.b, *self._branch(), activation_code(self.activation),
+                                   self.groups)
+            return y.reshape(*lead, self.d_out)
+
+    return NobleLinear
+
+
 def __getattr__(name):
-    if name == "NobleLinearFunction":
-        fn = _make_function()
-        globals()[name] = fn
-        return fn
+    makers = {"NobleLinearFunction": _make_function, "NobleLinear": _make_module}
+    if name in makers:
+        obj = makers[name]()
+        globals()[name] = obj
+        return obj
     raise AttributeError(name)
