@@ -87,9 +87,11 @@ def _f64(a):
 
 
 def _phi_cdf(a):
-    """Standard normal CDF, 0.5 (1 + erf(a / sqrt 2))."""
-    from scipy.special import erf
-    return 0.5 * (1.0 + erf(a / np.sqrt(2.0)))
+    """Standard normal CDF, 0.5 (1 + erf(a / sqrt 2)), evaluated as
+    0.5 erfc(-a / sqrt 2), the same function without the cancellation of
+    1 + erf in the lower tail."""
+    from scipy.special import erfc
+    return 0.5 * erfc(-a / np.sqrt(2.0))
 
 
 def activation_value(f, a):

@@ -32,6 +32,11 @@ __device__ __forceinline__ void fast_sincos(float x, float& s, float& c) {
     c = __builtin_amdgcn_cosf(t);
 }
 
+// Standard normal distribution function as erfc(-a / sqrt 2) / 2: the form
+// 1 + erf(a / sqrt 2) loses every digit to cancellation once a is a few units
+// below zero, erfc keeps the relative accuracy of the tail.
+__device__ __forceinline__ float std_normal_cdf(float a) { return 0.5f * erfcf(-a * 0.70710678118654752f); }
+
 // f(a).  FAST selects the turn-reduced hardware cosine (bf16 path); the
 // float32 path uses the device math library throughout.
 template <Act F, bool FAST>
@@ -44,13 +49,16 @@ __device__ __forceinline__ float act_value(float a) {
     } else if constexpr (F == Act::Leaky) {
         return a > 0.f ? a : kLeakySlope * a;
     } else {
-        return 0.5f * a * (1.f + erff(a * 0.70710678118654752f));
+        return a * std_normal_cdf(a);
     }
 }
 
 // f(a) and f'(a): d cos = -sin; d tanh = 1 - tanh^2; LeakyReLU's slope is 1
 // above zero and kLeakySlope otherwise; d (a Phi(a)) = Phi(a) + a phi(a), phi
-// the standard normal density.
+// the standard normal density.  1 - tanh^2 is evaluated as sech^2 =
+// 4 e / (1 + e)^2 with e = exp(-2 |a|): taken as 1 - t t from a rounded t it
+// cancels where tanh saturates (about 10% relative error at |a| = 8 in
+// float32), and the gradient of a saturated unit would carry that error.
 template <Act F, bool FAST>
 __device__ __forceinline__ void act_value_slope(float a, float& f, float& d) {
     if constexpr (F == Act::Cos) {
@@ -60,14 +68,15 @@ __device__ __forceinline__ void act_value_slope(float a, float& f, float& d) {
         f = c;
         d = -s;
     } else if constexpr (F == Act::Tanh) {
-        const float t = tanhf(a);
-        f = t;
-        d = 1.f - t * t;
+        const float e = expf(-2.f * fabsf(a));
+        const float q = 1.f + e;
+        f = tanhf(a);
+        d = 4.f * e / (q * q);
     } else if constexpr (F == Act::Leaky) {
         f = a > 0.f ? a : kLeakySlope * a;
         d = a > 0.f ? 1.f : kLeakySlope;
     } else {
-        const float cdf = 0.5f * (1.f + erff(a * 0.70710678118654752f));
+        const float cdf = std_normal_cdf(a);
         f = a * cdf;
         d = cdf + a * 0.39894228040143268f * expf(-0.5f * a * a);
     }

@@ -116,3 +116,40 @@ def test_activation_full_size_block(act):
     for k, e in rep.items():
         assert e <= TOL["bf16"], (k, e)
     assert ok
+
+
+SATURATED = [("tanh", 9.0), ("tanh_m", 9.0), ("gelu", -6.5), ("gelu_m", -6.5)]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("act,shift", SATURATED, ids=[a for a, _ in SATURATED])
+def test_saturated_units_keep_relative_gradient_accuracy(act, shift, dt):
+    """Every other rank column gets a phase that puts its unit deep in the
+    flat part of tanh (|a| near 9, slope near 1e-7) or in GELU's lower tail
+    (a near -6.5).  At T = 1 the phase gradient of a column is f'(A) dC of
+    that one element, so it is compared element by element, relative to its
+    own size: a slope taken as 1 - t^2 from a rounded tanh, or a normal
+    distribution function taken as 1 + erf, loses most of its digits there
+    while the row-normalised metric above does not see it.  Columns whose dC
+    cancels (sum of |terms| over 1e3 times |dC|) are left out."""
+    T, di, do, r = 1, 96, 160, 64
+    _say(f"[saturated] {act} {dt}: T={T} d_in={di} d_out={do} r={r} shift={shift}")
+    p = inp.draw_projection(f"sat_{act}", T, di, do, r, dt, seed=515, bias_std=0.5)
+    two = noble.two_layers(act)
+    k = "phi2" if two else "phi1"
+    sat = np.arange(r) % 2 == 0
+    sign = np.where(np.arange(r) % 4 == 0, 1.0, -1.0) if act.startswith("tanh") else 1.0
+    p.arrays[k] = np.where(sat, sign * shift, p.arrays[k]).astype(np.float32)
+    mix = _mix_round(act, dt)
+    ref = oracle_outputs(p, activation=act, mix_round=mix)
+    got = _run(p, act).outputs()
+    a = {n: np.asarray(v, dtype=np.float64) for n, v in p.arrays.items() if v is not None}
+    terms = np.abs(a["dy"][0])[None, :] * np.abs(a["W_up"])
+    dC = a["W_up"] @ a["dy"][0]
+    keep = sat & (terms.sum(axis=1) < 1e3 * np.abs(dC))
+    assert keep.sum() >= r // 4
+    want, have = ref["d" + k][keep], np.asarray(got["d" + k], dtype=np.float64)[keep]
+    rel = np.abs(have - want) / np.abs(want)
+    _say(f"  {keep.sum()} saturated columns, |slope dC| from {np.abs(want).min():.2e}, max rel err {rel.max():.2e}")
+    assert np.all(np.abs(want) > 0)
+    assert rel.max() <= {"bf16": 1e-2, "f32": 1e-4}[dt], rel.max()

@@ -42,7 +42,9 @@ MUTATIONS = {
     "gelu_slope_missing_density": ("return _phi_cdf(a) + a * np.exp(-0.5 * a * a) / np.sqrt(2.0 * np.pi)",
                                    "return _phi_cdf(a)"),
     "gelu_value_is_cdf": ("return a * _phi_cdf(a)", "return _phi_cdf(a)"),
-    "gelu_cdf_unscaled": ("return 0.5 * (1.0 + erf(a / np.sqrt(2.0)))", "return 0.5 * (1.0 + erf(a))"),
+    "gelu_cdf_unscaled": ("return 0.5 * erfc(-a / np.sqrt(2.0))", "return 0.5 * erfc(-a)"),
+    "gelu_cdf_through_erf": ("return 0.5 * erfc(-a / np.sqrt(2.0))",
+                             "from scipy.special import erf\n    return 0.5 * (1.0 + erf(a / np.sqrt(2.0)))"),
     "one_layer_chain_mixes": ("        dC1 = dC2                                    # C2 = C1",
                               "        dC1 = 2.0 * dC2"),
     # rounding of the mixing operand
@@ -133,7 +135,7 @@ def _battery_passes(mod):
                 fd = (loss(qp) - loss(qm)) / 2e-6
                 if abs(fd - g[gn][idx]) > 1e-6 * max(1.0, abs(g[gn][idx])):
                     return False
-    return _mix_round_pin(mod) and _grouped_pin(mod)
+    return _mix_round_pin(mod) and _grouped_pin(mod) and _tail_pin(mod)
 
 
 def _grouped_pin(mod):
@@ -161,6 +163,20 @@ def _grouped_pin(mod):
         if not np.allclose(gg["dM"][g], gs["dM"][g * r:(g + 1) * r, g * r:(g + 1) * r], rtol=0, atol=1e-12):
             return False
     return True
+
+
+def _tail_pin(mod):
+    """GELU's value and slope in the lower tail lie inside the Mills-ratio
+    bounds of the normal distribution function, and tanh's slope equals
+    1 / cosh^2 where tanh saturates."""
+    a = np.array([-6.0, -8.0, -10.0, -20.0])
+    dens = np.exp(-0.5 * a * a) / math.sqrt(2.0 * math.pi)
+    lo, hi = dens / np.abs(a) * (1.0 - 1.0 / (a * a)), dens / np.abs(a)
+    cdf = mod.activation_value("gelu", a) / a
+    d = mod.activation_slope("gelu", a)
+    t = np.array([5.0, 9.5, -12.0])
+    return bool(np.all(lo < cdf) and np.all(cdf < hi) and np.all(lo + a * dens < d) and np.all(d < hi + a * dens)
+                and np.allclose(mod.activation_slope("tanh", t), np.cosh(t) ** -2.0, rtol=1e-5, atol=0))
 
 
 def _mix_round_pin(mod):

@@ -463,6 +463,25 @@ def test_gelu_tends_to_identity_and_zero():
     np.testing.assert_allclose(_fwd_a(q, "gelu")[0] - base, 0.0, rtol=0, atol=1e-12)
 
 
+
+def test_slopes_keep_relative_accuracy_in_the_tails():
+    """Where tanh saturates and in GELU's lower tail the slopes are tiny, and
+    a saturated unit's gradient is that tiny number times dC.  Pinned against
+    bounds from analysis rather than a second evaluation of the same formula:
+    1 - tanh(a)^2 = 1 / cosh(a)^2, and the Mills-ratio bounds of the normal
+    tail, phi(a) / |a| (1 - 1 / a^2) < Phi(a) < phi(a) / |a| for a < 0, which
+    bracket GELU = a Phi(a) and its slope Phi(a) + a phi(a)."""
+    a = np.array([2.0, 5.0, 8.0, 9.5, 12.0])
+    for s in (1.0, -1.0):
+        np.testing.assert_allclose(oracle.activation_slope("tanh", s * a), np.cosh(a) ** -2.0, rtol=1e-5, atol=0)
+    a = np.array([-4.0, -6.0, -8.0, -10.0, -20.0])
+    dens = np.exp(-0.5 * a * a) / math.sqrt(2.0 * math.pi)
+    lo, hi = dens / np.abs(a) * (1.0 - 1.0 / (a * a)), dens / np.abs(a)
+    cdf = oracle.activation_value("gelu", a) / a
+    assert np.all(lo < cdf) and np.all(cdf < hi), (lo, cdf, hi)
+    d = oracle.activation_slope("gelu", a)
+    assert np.all(lo + a * dens < d) and np.all(d < hi + a * dens)
+
 # ------------------------------------------------- mixing-operand rounding --
 
 def _coarse(a):
