@@ -68,17 +68,24 @@ def kink_margin(p, activation, mix_round=None, rel=1e-5):
     """Smallest |A| / band over the pre-activations A1 (and A2) of the
     LeakyReLU forms, band = rel * (|w| max_t |h| + |p|) per rank column (h the
     column that w scales).  Below 1 an element sits where float32 and float64
-    can take different branches of the kink; a parity case needs > 1."""
-    a = {k: np.asarray(v, dtype=np.float64) for k, v in p.arrays.items()}
+    can take different branches of the kink; a parity case needs > 1.
+    Grouped layers are checked group by group."""
+    a = {k: (None if v is None else np.asarray(v, dtype=np.float64)) for k, v in p.arrays.items()}
+    G = getattr(p, "groups", 1)
+    r = p.r
     H = a["x"] @ a["W_down"]
-    fw = oracle.branch_forward(H, activation, a["omega1"], a["phi1"], a["M"], a["omega2"], a["phi2"],
-                               mix_round=mix_round)
 
     def margin(A, h, w, ph):
         band = rel * (np.abs(w) * np.max(np.abs(h), axis=0) + np.abs(ph))
         return float(np.min(np.abs(A) / band))
 
-    m = margin(fw["A1"], H, a["omega1"], a["phi1"])
-    if "A2" in fw:
-        m = min(m, margin(fw["A2"], fw["H2"], a["omega2"], a["phi2"]))
+    m = np.inf
+    for g in range(G):
+        cs = slice(g * r, (g + 1) * r)
+        Mg = a["M"] if G == 1 else a["M"][g]
+        fw = oracle.branch_forward(H[:, cs], activation, a["omega1"][cs], a["phi1"][cs], Mg, a["omega2"][cs],
+                                   a["phi2"][cs], mix_round=mix_round)
+        m = min(m, margin(fw["A1"], H[:, cs], a["omega1"][cs], a["phi1"][cs]))
+        if "A2" in fw:
+            m = min(m, margin(fw["A2"], fw["H2"], a["omega2"][cs], a["phi2"][cs]))
     return m
