@@ -27,6 +27,8 @@ LIB_PATH = os.path.join(PKG_DIR, "libnoble.so")
 
 NOBLE_BF16 = 0
 NOBLE_F32 = 1
+# NOBLE_ABI_VERSION of include/noble.h that the structures below mirror
+ABI_VERSION = 3
 
 STATUS = {
     0: "NOBLE_OK",
@@ -113,6 +115,9 @@ def lib() -> ctypes.CDLL:
         L.noble_status_string.argtypes = [ctypes.c_int]
         L.noble_abi_version.restype = ctypes.c_int
         L.noble_abi_version.argtypes = []
+        if L.noble_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has C ABI version {L.noble_abi_version()}, the binding expects "
+                               f"{ABI_VERSION}: rebuild it")
         L.noble_linear_workspace_size.restype = ctypes.c_int
         L.noble_linear_workspace_size.argtypes = [ctypes.POINTER(noble_linear_desc),
                                                   ctypes.POINTER(ctypes.c_size_t),

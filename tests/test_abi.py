@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
     L = noble.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.noble_abi_version() == 3
+    assert L.noble_abi_version() == 3 == noble.ABI_VERSION
 
 
 def test_status_strings():
