@@ -255,7 +255,7 @@ int choose_split_partials(int tiles, int nk, int64_t MN) {
     constexpr double kBytesPerUs = 5.0e6;     // HBM rate of the partials
     double best = 0;
     int bs = 1;
-    for (int s = 1; s <= 16; s *= 2) {
+    for (int s = 1; s <= kMaxReduceSlices; s *= 2) {   // reduce_kernel sums at most that many
         if (s > 1 && s * 8 > nk) break;
         const double waves = (double)((int64_t)tiles * s + 255) / 256;
         const double cost = (int)waves * ((double)nk / s) * kChunkUs + (s > 1 ? (2.0 * s + 1) * MN * 4 / kBytesPerUs : 0);
@@ -271,13 +271,19 @@ int choose_split_partials(int tiles, int nk, int64_t MN) {
 // pieces add atomically into zeroed outputs of at most a few MB.  They share
 // a launch with dW (dw_wgs workgroups of dw_chunks K chunks each, launched
 // first); one factor for all of them, the one that minimises the launch's
-// makespan under the list-scheduling model above, with at least 8 K chunks
-// per piece.  rank_tiles: the rank problems' 256 x 256 tile count.
-int choose_rank_split(int dw_wgs, int dw_chunks, int rank_tiles, int nk) {
+// makespan under the list-scheduling model above plus the float atomics of
+// the pieces (split x rank_bytes of output at about 1 MB per us), with at
+// least 8 K chunks per piece.  Candidates are 2^a 3^b: the model is flat near
+// its optimum, and a coarse set keeps its choice off near-ties.
+// rank_tiles: the rank problems' 256 x 256 tile count.
+int choose_rank_split(int dw_wgs, int dw_chunks, int rank_tiles, int nk, int64_t rank_bytes) {
+    constexpr double kAtomicBytesPerUs = 1.0e6;
     int best = 1;
     double best_t = 0.0;
-    for (int s = 1; s <= 16 && (s == 1 || s * 8 <= nk); s *= 2) {
-        const double t = launch_makespan({{dw_wgs, dw_chunks}, {rank_tiles * s, cdiv(nk, s)}});
+    for (int s : {1, 2, 3, 4, 6, 8, 12, 16}) {
+        if (s > 1 && s * 8 > nk) break;
+        const double t = launch_makespan({{dw_wgs, dw_chunks}, {rank_tiles * s, cdiv(nk, s)}}) +
+                         (double)s * (double)rank_bytes / kAtomicBytesPerUs;
         if (s == 1 || t < best_t) {
             best_t = t;
             best = s;
@@ -644,8 +650,9 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         if (r > 0) {
             const int rank_tiles = cdiv(din, kBM) * cdiv(R, kBN) +
                                    G * (cdiv(r, kBM) * cdiv(dog, kBN) + (two ? cdiv(r, kBM) * cdiv(r, kBN) : 0));
+            const int64_t rank_bytes = 4 * (din * R + G * (r * dog + (two ? r * r : 0)));
             const int rs = choose_rank_split(cdiv(din, kBM) * cdiv(dout, kBN) * wp.split, cdiv(nkT, wp.split),
-                                             rank_tiles, nkT);
+                                             rank_tiles, nkT, rank_bytes);
             bt.add(xT, operand1(seg(dHs, R, T), R), (int)din, (int)R, nkT, dWd, R, true, nullptr, nullptr, rs);
             for (int g = 0; g < G; ++g) {
                 const int64_t c0 = g * r;
@@ -663,6 +670,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         // One reduction pass: the split-K partials of dW, and the copies of
         // the frequency / phase gradients.
         ReduceList red{};
+        static_assert(kChainCopies <= kMaxReduceSlices, "copies exceed the reduction's slices");
         auto reduce = [&](const float* part, float* out, int64_t n, int S) {
             red.part[red.count] = part;
             red.out[red.count] = out;
@@ -681,8 +689,11 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             }
         }
         if (red.count > 0) {
-            const int blocks = wp.split > 1 ? 1024 : std::max(1, cdiv(R, 4 * 256));
-            hipLaunchKernelGGL(reduce_kernel, dim3(blocks), dim3(256), 0, st, red);
+            // up to 1024 blocks of 256 threads per array, four floats per thread
+            red.first[0] = 0;
+            for (int a = 0; a < red.count; ++a)
+                red.first[a + 1] = red.first[a] + (int)std::min<int64_t>(1024, std::max<int64_t>(1, cdiv(red.n[a], 4 * 256)));
+            hipLaunchKernelGGL(reduce_kernel, dim3(red.first[red.count]), dim3(256), 0, st, red);
             NOBLE_TRY(last_launch());
         }
     }

@@ -58,28 +58,48 @@ struct ReduceList {
     float* out[kMaxZero];
     int64_t n[kMaxZero];
     int S[kMaxZero];
+    int first[kMaxZero + 1];   // array s owns blocks first[s] .. first[s + 1] - 1
     int count;
 };
 
+constexpr int kMaxReduceSlices = 16;
+
+// out[i] = part[i] + part[n + i] + ... + part[(S - 1) n + i] for each array,
+// every array on its own range of blocks.  The S loads of an element are
+// issued together (S is at most kMaxReduceSlices) and added in slice order:
+// a loop that waits on each slice in turn makes the few-element arrays
+// (the frequency / phase copies) a chain of dependent L2 round trips.
 __global__ __launch_bounds__(256) void reduce_kernel(ReduceList z) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    for (int s = 0; s < z.count; ++s) {
-        const float* p = z.part[s];
-        float* o = z.out[s];
-        const int64_t n = z.n[s];
-        const int S = z.S[s];
-        const int64_t n4 = n >> 2;
-        for (int64_t i = gid; i < n4; i += stride) {
-            f32x4 acc = reinterpret_cast<const f32x4*>(p)[i];
-            for (int q = 1; q < S; ++q) acc += reinterpret_cast<const f32x4*>(p + q * n)[i];
-            reinterpret_cast<f32x4*>(o)[i] = acc;
-        }
-        for (int64_t i = (n4 << 2) + gid; i < n; i += stride) {
-            float acc = p[i];
-            for (int q = 1; q < S; ++q) acc += p[q * n + i];
-            o[i] = acc;
-        }
+    int s = 0;
+    while (s + 1 < z.count && (int)blockIdx.x >= z.first[s + 1]) ++s;
+    const float* p = z.part[s];
+    float* o = z.out[s];
+    const int64_t n = z.n[s];
+    const int S = z.S[s];
+    const int64_t stride = (int64_t)(z.first[s + 1] - z.first[s]) * blockDim.x;
+    const int64_t gid = (int64_t)(blockIdx.x - z.first[s]) * blockDim.x + threadIdx.x;
+    const int64_t n4 = n >> 2;
+    for (int64_t i = gid; i < n4; i += stride) {
+        f32x4 v[kMaxReduceSlices];
+#pragma unroll
+        for (int q = 0; q < kMaxReduceSlices; ++q)
+            if (q < S) v[q] = reinterpret_cast<const f32x4*>(p + q * n)[i];
+        f32x4 acc = v[0];
+#pragma unroll
+        for (int q = 1; q < kMaxReduceSlices; ++q)
+            if (q < S) acc += v[q];
+        reinterpret_cast<f32x4*>(o)[i] = acc;
+    }
+    for (int64_t i = (n4 << 2) + gid; i < n; i += stride) {
+        float v[kMaxReduceSlices];
+#pragma unroll
+        for (int q = 0; q < kMaxReduceSlices; ++q)
+            if (q < S) v[q] = p[q * n + i];
+        float acc = v[0];
+#pragma unroll
+        for (int q = 1; q < kMaxReduceSlices; ++q)
+            if (q < S) acc += v[q];
+        o[i] = acc;
     }
 }
 
