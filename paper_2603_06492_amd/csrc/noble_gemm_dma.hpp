@@ -189,8 +189,38 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
     // The wave index is uniform; say so, so DMA offsets and LDS bases stay
     // in SGPRs.
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm0 = (wave / kDmaWN) * WTM, wn0 = (wave % kDmaWN) * WTN;
+    // Wave w takes M half w / 4 and N quarter (w % 4) ^ 2 (w / 4).  Waves w and
+    // w + 4 share a SIMD, and this way they differ in both the M half and the
+    // N half: a tile that is only half inside M or N (the rank-r products,
+    // r <= 128) leaves every SIMD one live wave instead of idling two SIMDs.
+    const int wm0 = (wave / kDmaWN) * WTM, wn0 = ((wave % kDmaWN) ^ ((wave / kDmaWN) * (kDmaWN / 2))) * WTN;
+    static_assert(kDmaWM == 2, "the N-quarter swizzle pairs two M halves");
     const int r32 = lane & 31, h = lane >> 5;
+
+    // A wave whose block lies wholly outside the problem only loads its share
+    // of the operand tiles and meets the barriers: the same stages and the
+    // same barrier sequence (one after the first chunk's loads, one per chunk)
+    // as the loop below, without fragment reads, MFMAs or stores.  Kept apart
+    // from that loop: a test inside it slowed the full tiles by 2-4%.
+    if (m0 + wm0 >= P.M || n0 + wn0 >= P.N) {
+        if (kc0 < kc1) {
+            const Operand opA = P.A, opB = P.B;
+            dma_tile<AK, NW>(opA, m0, kc0, lds0, wave, lane);
+            dma_tile<BKM, NW>(opB, n0, kc0, lds0 + TILE, wave, lane);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            for (int kc = kc0; kc < kc1; ++kc) {
+                char* nxt = ((kc - kc0) & 1) ? lds0 : lds1;
+                if (kc + 1 < kc1) {
+                    dma_tile<AK, NW>(opA, m0, kc + 1, nxt, wave, lane);
+                    dma_tile<BKM, NW>(opB, n0, kc + 1, nxt + TILE, wave, lane);
+                }
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                __syncthreads();
+            }
+        }
+        return;
+    }
 
     f32x16 acc[TM][TN];
 #pragma unroll
