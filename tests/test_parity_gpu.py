@@ -44,6 +44,11 @@ SMALL = [
     ("bf16_r64_T1", 1, 256, 128, 64, "bf16", 0.5),
     ("bf16_r32_T127", 127, 128, 128, 32, "bf16", 0.0),
     ("bf16_r64_T2500_splitK", 2500, 1024, 256, 64, "bf16", 0.5),
+    # narrow layers over many tokens: dW split into 16 and 8 K pieces whose
+    # float32 partials the reduction sums
+    ("bf16_r32_T8192_dW16", 8192, 256, 264, 32, "bf16", 0.5),
+    ("bf16_r64_T4096_dW8", 4096, 256, 256, 64, "bf16", 0.5),
+    ("f32_r24_T4096_dW16", 4096, 128, 136, 24, "f32", 0.5),
     ("f32_ragged_r24", 333, 96, 136, 24, "f32", 0.5),
     ("f32_r128", 200, 160, 96, 128, "f32", 0.5),
     ("f32_r72", 65, 40, 48, 72, "f32", 0.5),
