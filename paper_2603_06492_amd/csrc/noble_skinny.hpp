@@ -413,9 +413,17 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
     const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * R + col) * 2) : kOOB;
     auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * R * es); };
     const bool keep_h = a.H != nullptr;   // NULL: inference-only forward
+    // Stores count in vmcnt: in the two-application form H is stored after
+    // the barrier, whose wait for M would otherwise also wait for them.
+    auto store_h = [&]() {
+        if (keep_h)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), 0);
+    };
+    if constexpr (!L2) store_h();
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-        if (keep_h) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), 0);
         const float c1 = cv ? act_value<F, true>(acc[v] * w1 + p1) : 0.f;
         if constexpr (L2) {
             const int row = 8 * (v >> 2) + 4 * h + (v & 3);
@@ -428,6 +436,7 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
         const float w2 = cv ? a.w2[q.c0 + col] : 0.f, p2 = cv ? a.p2[q.c0 + col] : 0.f;
         wait_vmcnt<0>();   // this wave's part of M has landed
         __syncthreads();   // C1 tile and M complete
+        store_h();
 
         f32x16 h2;
 #pragma unroll
@@ -501,18 +510,22 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     } else {
         const float w2 = cv ? a.w2[gc] : 0.f, p2 = cv ? a.p2[gc] : 0.f;
         const __amdgpu_buffer_rsrc_t rc1 = group_rsrc(a.C1s, a, q, 2), rdh2 = group_rsrc(a.dH2s, a, q, 2);
+        uint16_t c1[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int row = 8 * (v >> 2) + 4 * h + (v & 3);
             float f = 0.f, d = 0.f;
             if (cv) act_value_slope<F, true>(hr[v] * w1 + p1, f, d);
             d1[v] = d;
-            const uint16_t c1 = (uint16_t)f2bf(f);
-            *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = c1;
-            __builtin_amdgcn_raw_buffer_store_b16(c1, rc1, vo2, soff(v, 2), 0);
+            c1[v] = (uint16_t)f2bf(f);
+            *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = c1[v];
         }
         wait_vmcnt<0>();   // this wave's part of M has landed
         __syncthreads();   // C1 tile and M complete
+        // C1 to scratch after the barrier: stores count in vmcnt, and the
+        // wait above is for M only
+#pragma unroll
+        for (int v = 0; v < 16; ++v) __builtin_amdgcn_raw_buffer_store_b16(c1[v], rc1, vo2, soff(v, 2), 0);
 
         f32x16 h2;
 #pragma unroll
