@@ -192,12 +192,21 @@ Operand operand2(Seg s0, Seg s1, int nk1, int64_t rows) {
     return o;
 }
 
-// Tile shape of the large products.
-constexpr int kBM = 256, kBN = 256;
+// Square output tile of the large products: 256 on the bf16 path; 128 on
+// the float32 path, which serves small layers (a 256 tile of a 64 x 64
+// output would leave one wave doing 16 times the needed work on one CU).
+template <typename E>
+constexpr int gemm_tile() {
+    return sizeof(E) == 2 ? 256 : 128;
+}
+int gemm_tile_of(const noble_linear_desc* d) {
+    return d->dtype == NOBLE_BF16 ? gemm_tile<uint16_t>() : gemm_tile<float>();
+}
 
 struct Batch {
     GemmBatch b{};
     int blocks = 0;
+    int tile = 256;   // square output tile
     // split > 1: pieces add atomically into C, or, when `partials` is given,
     // each stores its float32 partial [M][ldc] at partials + piece * M * ldc.
     void add(const Operand& A, const Operand& B, int M, int N, int nk, void* C, int64_t ldc, bool out_f32,
@@ -214,8 +223,8 @@ struct Batch {
         p.N = N;
         p.nk = nk;
         p.split = split;
-        p.tiles_m = cdiv(M, kBM);
-        p.tiles_n = cdiv(N, kBN);
+        p.tiles_m = cdiv(M, tile);
+        p.tiles_n = cdiv(N, tile);
         p.tile_begin = blocks;
         p.nblocks = p.tiles_m * p.tiles_n * split;
         p.out_f32 = out_f32 ? 1 : 0;
@@ -299,17 +308,19 @@ struct WgradPlan {
     size_t bytes;   // dW partials
 };
 
-WgradPlan plan_wgrad(int64_t T, int64_t din, int64_t dout, int bk) {
+WgradPlan plan_wgrad(int64_t T, int64_t din, int64_t dout, int bk, int tile) {
     WgradPlan w{1, 0};
     const int nkT = T > 0 ? cdiv(T, bk) : 0;
     if (nkT == 0) return w;
-    w.split = choose_split_partials(cdiv(din, kBM) * cdiv(dout, kBN), nkT, din * dout);
+    w.split = choose_split_partials(cdiv(din, tile) * cdiv(dout, tile), nkT, din * dout);
     w.bytes = w.split > 1 ? align_up((size_t)w.split * din * dout * 4) : 0;
     return w;
 }
 
 size_t wgrad_need(const noble_linear_desc* d) {
-    return plan_wgrad(d->T, d->d_in, d->d_out, d->dtype == NOBLE_BF16 ? Elt<uint16_t>::BK : Elt<float>::BK).bytes;
+    return plan_wgrad(d->T, d->d_in, d->d_out, d->dtype == NOBLE_BF16 ? Elt<uint16_t>::BK : Elt<float>::BK,
+                      gemm_tile_of(d))
+        .bytes;
 }
 
 // `plain`: the r = 0 forward, launched under its own kernel symbol so that
@@ -325,7 +336,8 @@ noble_status launch_gemm(const Batch& bt, hipStream_t st, bool plain = false) {
             hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKM, !AK && !BKM, 0>), dim3(bt.blocks), dim3(kDmaThreads), 0,
                                st, bt.b);
     } else
-        hipLaunchKernelGGL((gemm_kernel<E, kBM, kBN, AK, BKM, !AK && !BKM>), dim3(bt.blocks), dim3(kThreads), 0,
+        hipLaunchKernelGGL((gemm_kernel<E, gemm_tile<E>(), gemm_tile<E>(), AK, BKM, !AK && !BKM>), dim3(bt.blocks),
+                           dim3(kThreads), 0,
                            st, bt.b);
     return last_launch();
 }
@@ -515,6 +527,7 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
     const int nk1 = cdiv(din, GBK);
     const int nk = nk1 + (r > 0 ? cdiv(r, GBK) : 0);
     Batch bt;
+    bt.tile = gemm_tile<E>();
     for (int g = 0; g < G; ++g) {
         const E* Wg = static_cast<const E*>(W) + g * dog;
         const char* C2g = C2s + g * r * (int64_t)ES;
@@ -551,7 +564,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     // and dp2 (when given).
     constexpr int GBK = gemm_bk<E>();
     const int nkT = cdiv(T, GBK);
-    const WgradPlan wp = plan_wgrad(T, din, dout, GBK);
+    const WgradPlan wp = plan_wgrad(T, din, dout, GBK, gemm_tile<E>());
     float* copies = copies_need(d) ? reinterpret_cast<float*>(base + 4 * reg + partial_need(d)) : nullptr;
     float* wpart = reinterpret_cast<float*>(base + (r > 0 ? 4 * reg + partial_need(d) + copies_need(d) : 0));
 
@@ -632,6 +645,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         const int nk1 = cdiv(dout, GBK);
         const int nk = nk1 + (r > 0 ? cdiv(R, GBK) : 0);
         Batch bt;
+        bt.tile = gemm_tile<E>();
         bt.add(operand2(seg(dy, dout, dout), seg(dHs, R, R), nk1, T), operand2(seg(W, dout, dout), seg(Wd, R, R), nk1, din),
                (int)T, (int)din, nk, dx, din, sizeof(E) == 4, nullptr, nullptr, 1);
         NOBLE_TRY((launch_gemm<E, true, true>(bt, st)));
@@ -643,15 +657,17 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     // stores partials that reduce_kernel then sums into dW.
     {
         Batch bt;
+        bt.tile = gemm_tile<E>();
         const Operand xT = operand1(seg(x, din, T), din);
         const Operand dyN = operand1(seg(dy, dout, T), dout);
         bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split,
                wp.split > 1 ? wpart : nullptr);
         if (r > 0) {
-            const int rank_tiles = cdiv(din, kBM) * cdiv(R, kBN) +
-                                   G * (cdiv(r, kBM) * cdiv(dog, kBN) + (two ? cdiv(r, kBM) * cdiv(r, kBN) : 0));
+            constexpr int TL = gemm_tile<E>();
+            const int rank_tiles = cdiv(din, TL) * cdiv(R, TL) +
+                                   G * (cdiv(r, TL) * cdiv(dog, TL) + (two ? cdiv(r, TL) * cdiv(r, TL) : 0));
             const int64_t rank_bytes = 4 * (din * R + G * (r * dog + (two ? r * r : 0)));
-            const int rs = choose_rank_split(cdiv(din, kBM) * cdiv(dout, kBN) * wp.split, cdiv(nkT, wp.split),
+            const int rs = choose_rank_split(cdiv(din, TL) * cdiv(dout, TL) * wp.split, cdiv(nkT, wp.split),
                                              rank_tiles, nkT, rank_bytes);
             bt.add(xT, operand1(seg(dHs, R, T), R), (int)din, (int)R, nkT, dWd, R, true, nullptr, nullptr, rs);
             for (int g = 0; g < G; ++g) {

@@ -86,13 +86,14 @@ def _copies(R):
     return _align(4 * 8 * R * 4)
 
 
-def _wgrad_bytes(T, di, do, r, bk):
+def _wgrad_bytes(T, di, do, r, bk, tile=256):
     """dW partials: only dW stores partials (the rank gradients add
-    atomically)."""
+    atomically).  Output tiles are 256 square on the bf16 path, 128 on the
+    float32 path."""
     nk = -(-T // bk) if T > 0 else 0
     if nk == 0:
         return 0
-    sp = _split_partials(-(-di // 256) * -(-do // 256), nk, di * do)
+    sp = _split_partials(-(-di // tile) * -(-do // tile), nk, di * do)
     return _align(sp * di * do * 4) if sp > 1 else 0
 
 
@@ -115,6 +116,11 @@ def test_workspace_sizes():
     assert S == 4 and st == OK and scr == 4 * _align(300 * 40 * 2) + _align(S * 300 * 40 * 4) + _copies(40)
     st, res, scr = _ws(256, 64, 64, 8, noble.NOBLE_F32)
     assert st == OK and res == 4 * 256 * 8 and scr == 4 * 256 * 8 * 4
+    # float32 tiles are 128 square: 64 tiles of 1024 x 1024 split dW in 4
+    # (with 256 tiles it would be 16)
+    st, res, scr = _ws(8192, 1024, 1024, 0, noble.NOBLE_F32)
+    assert _wgrad_bytes(8192, 1024, 1024, 0, 32, tile=256) == 16 * 1024 * 1024 * 4
+    assert st == OK and scr == _wgrad_bytes(8192, 1024, 1024, 0, 32, tile=128) == 4 * 1024 * 1024 * 4
     st, res, scr = _ws(1000, 64, 64, 0, noble.NOBLE_BF16)
     assert st == OK and res == 0 and scr == _wgrad_bytes(1000, 64, 64, 0, 64) == 2 * 64 * 64 * 4
     st, res, scr = _ws(200, 64, 64, 0, noble.NOBLE_BF16)
