@@ -239,3 +239,36 @@ def test_full_size_workloads(wl, idx):
     for k, e in rep.items():
         assert e <= TOL["bf16"], (k, e)
     assert ok
+
+
+def test_buffers_past_2gib():
+    """x and dx of 2.16 GB (T = 2^20 + 4133 tokens, d_in = 1024): every
+    device offset past the 2^31-byte mark is formed in 64 bits before it
+    reaches a 32-bit buffer offset.  x and dy repeat a seeded block of 65537
+    rows (drawing 10^9 values would take minutes); 2^20 is not a multiple of
+    65537, so a read wrapped by 2^31 bytes (2^20 rows) would land on a
+    different row.  Rows on both sides of byte 2^31 of x and dx are compared
+    with the oracle, with dW on sampled columns and the rank gradients in
+    full."""
+    T, di, do, r, period = (1 << 20) + 4133, 1024, 256, 64, 65537
+    base = inp.draw_projection("bf16_past_2gib", period, di, do, r, "bf16", seed=131, bias_std=0.5)
+    arrays = dict(base.arrays)
+    for k in ("x", "dy"):
+        arrays[k] = np.resize(base.arrays[k], (T, base.arrays[k].shape[1]))   # row t = block row t % period
+    p = inp.Projection("bf16_past_2gib", T, di, do, r, "bf16", arrays)
+    assert p.arrays["x"].size * 2 > (1 << 31)
+    _say(f"[parity] past 2 GiB: T={T} d_in={di} d_out={do} r={r}")
+    edge = 1 << 20
+    rows = np.unique(np.concatenate([_sample(T, 16, 3), np.arange(edge - 3, edge + 3)]))
+    dw_rows = _sample(di, 8, 4)
+    dp = _run(p)
+    got = dp.outputs(rows=rows, dw_rows=dw_rows)
+    ok = dp.guards_intact()
+    del dp
+    ref = oracle_outputs(p, rows=rows, dw_rows=dw_rows)
+    rep = parity_report(got, ref)
+    _say(rep)
+    assert set(rep) == set(OUTPUTS)
+    for k, e in rep.items():
+        assert e <= TOL["bf16"], (k, e)
+    assert ok
