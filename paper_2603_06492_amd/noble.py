@@ -174,7 +174,7 @@ def _dtype_code(t) -> int:
     raise TypeError(f"storage tensors must be bfloat16 or float32, got {t.dtype}")
 
 
-def _ptr(t, name: str, dtype=None, shape=None) -> Optional[int]:
+def _ptr(t, name: str, dtype=None, shape=None, device=None) -> Optional[int]:
     if t is None:
         return None
     torch = _torch()
@@ -182,6 +182,8 @@ def _ptr(t, name: str, dtype=None, shape=None) -> Optional[int]:
         raise TypeError(f"{name} must be a torch.Tensor")
     if t.device.type != "cuda":
         raise ValueError(f"{name} must be on the GPU (got {t.device})")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the call runs on {device}: all tensors must share one device")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:
@@ -191,10 +193,20 @@ def _ptr(t, name: str, dtype=None, shape=None) -> Optional[int]:
     return t.data_ptr() or None
 
 
-def _stream(stream) -> Optional[int]:
+def _stream(stream, device) -> Optional[int]:
+    """The stream handle of ``stream`` (default: torch's current stream of
+    ``device``), which must belong to ``device``."""
     torch = _torch()
-    s = torch.cuda.current_stream() if stream is None else stream
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    if s.device != device:
+        raise ValueError(f"stream belongs to {s.device}, the tensors to {device}")
     return s.cuda_stream or None
+
+
+def _on(device):
+    """Context making ``device`` current: the library launches on the
+    current HIP device."""
+    return _torch().cuda.device(device)
 
 
 def _branch_shapes(d_in, d_out, R, groups):
@@ -228,15 +240,18 @@ def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, re
     sd = x.dtype
     f32 = torch.float32
     d = make_desc(T, d_in, d_out, r, dt, activation, groups)
+    dev = x.device
     args = [
-        _ptr(x, "x", sd, (T, d_in)), _ptr(W, "W", sd, (d_in, d_out)), _ptr(b, "b", f32, (d_out,)),
-        _ptr(W_down, "W_down", sd, sh["W_down"]), _ptr(omega1, "omega1", f32, sh["vec"]),
-        _ptr(phi1, "phi1", f32, sh["vec"]), _ptr(M, "M", sd, sh["M"]), _ptr(omega2, "omega2", f32, sh["vec"]),
-        _ptr(phi2, "phi2", f32, sh["vec"]), _ptr(W_up, "W_up", sd, sh["W_up"]), _ptr(y, "y", sd, (T, d_out)),
-        _ptr(reserve, "reserve"), _ptr(scratch, "scratch"),
+        _ptr(x, "x", sd, (T, d_in), dev), _ptr(W, "W", sd, (d_in, d_out), dev), _ptr(b, "b", f32, (d_out,), dev),
+        _ptr(W_down, "W_down", sd, sh["W_down"], dev), _ptr(omega1, "omega1", f32, sh["vec"], dev),
+        _ptr(phi1, "phi1", f32, sh["vec"], dev), _ptr(M, "M", sd, sh["M"], dev),
+        _ptr(omega2, "omega2", f32, sh["vec"], dev), _ptr(phi2, "phi2", f32, sh["vec"], dev),
+        _ptr(W_up, "W_up", sd, sh["W_up"], dev), _ptr(y, "y", sd, (T, d_out), dev),
+        _ptr(reserve, "reserve", device=dev), _ptr(scratch, "scratch", device=dev),
     ]
     nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
-    st = lib().noble_linear_fwd(ctypes.byref(d), *args, nbytes, _stream(stream))
+    with _on(dev):
+        st = lib().noble_linear_fwd(ctypes.byref(d), *args, nbytes, _stream(stream, dev))
     if st != 0:
         raise NobleError(st, "noble_linear_fwd")
 
@@ -261,20 +276,24 @@ def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, rese
     f32 = torch.float32
     d = make_desc(T, d_in, d_out, r, dt, activation, groups)
     v = sh["vec"]
+    dev = x.device
     args = [
-        _ptr(dy, "dy", sd, (T, d_out)), _ptr(x, "x", sd, (T, d_in)), _ptr(W, "W", sd, (d_in, d_out)),
-        _ptr(W_down, "W_down", sd, sh["W_down"]), _ptr(omega1, "omega1", f32, v), _ptr(phi1, "phi1", f32, v),
-        _ptr(M, "M", sd, sh["M"]), _ptr(omega2, "omega2", f32, v), _ptr(phi2, "phi2", f32, v),
-        _ptr(W_up, "W_up", sd, sh["W_up"]), _ptr(reserve, "reserve"),
-        _ptr(dx, "dx", sd, (T, d_in)), _ptr(dW, "dW", f32, (d_in, d_out)), _ptr(db, "db", f32, (d_out,)),
-        _ptr(dW_down, "dW_down", f32, sh["W_down"]), _ptr(dM, "dM", f32, sh["M"]),
-        _ptr(dW_up, "dW_up", f32, sh["W_up"]),
-        _ptr(domega1, "domega1", f32, v), _ptr(dphi1, "dphi1", f32, v),
-        _ptr(domega2, "domega2", f32, v), _ptr(dphi2, "dphi2", f32, v),
-        _ptr(scratch, "scratch"),
+        _ptr(dy, "dy", sd, (T, d_out), dev), _ptr(x, "x", sd, (T, d_in), dev), _ptr(W, "W", sd, (d_in, d_out), dev),
+        _ptr(W_down, "W_down", sd, sh["W_down"], dev), _ptr(omega1, "omega1", f32, v, dev),
+        _ptr(phi1, "phi1", f32, v, dev), _ptr(M, "M", sd, sh["M"], dev), _ptr(omega2, "omega2", f32, v, dev),
+        _ptr(phi2, "phi2", f32, v, dev), _ptr(W_up, "W_up", sd, sh["W_up"], dev),
+        _ptr(reserve, "reserve", device=dev),
+        _ptr(dx, "dx", sd, (T, d_in), dev), _ptr(dW, "dW", f32, (d_in, d_out), dev),
+        _ptr(db, "db", f32, (d_out,), dev),
+        _ptr(dW_down, "dW_down", f32, sh["W_down"], dev), _ptr(dM, "dM", f32, sh["M"], dev),
+        _ptr(dW_up, "dW_up", f32, sh["W_up"], dev),
+        _ptr(domega1, "domega1", f32, v, dev), _ptr(dphi1, "dphi1", f32, v, dev),
+        _ptr(domega2, "domega2", f32, v, dev), _ptr(dphi2, "dphi2", f32, v, dev),
+        _ptr(scratch, "scratch", device=dev),
     ]
     nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
-    st = lib().noble_linear_bwd(ctypes.byref(d), *args, nbytes, _stream(stream))
+    with _on(dev):
+        st = lib().noble_linear_bwd(ctypes.byref(d), *args, nbytes, _stream(stream, dev))
     if st != 0:
         raise NobleError(st, "noble_linear_bwd")
 
@@ -323,11 +342,14 @@ def noble_init_params(W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, seed: i
     sd, f32 = W.dtype, torch.float32
     d = make_desc(0, d_in, d_out, r, dt, 0, groups)
     v = sh["vec"]
-    args = [_ptr(W, "W", sd, (d_in, d_out)), _ptr(b, "b", f32, (d_out,)), _ptr(W_down, "W_down", sd, sh["W_down"]),
-            _ptr(omega1, "omega1", f32, v), _ptr(phi1, "phi1", f32, v), _ptr(M, "M", sd, sh["M"]),
-            _ptr(omega2, "omega2", f32, v), _ptr(phi2, "phi2", f32, v), _ptr(W_up, "W_up", sd, sh["W_up"])]
-    st = lib().noble_init_params(ctypes.byref(d), ctypes.byref(rc), int(seed) & (2 ** 64 - 1), *args,
-                                 _stream(stream))
+    dev = W.device
+    args = [_ptr(W, "W", sd, (d_in, d_out), dev), _ptr(b, "b", f32, (d_out,), dev),
+            _ptr(W_down, "W_down", sd, sh["W_down"], dev), _ptr(omega1, "omega1", f32, v, dev),
+            _ptr(phi1, "phi1", f32, v, dev), _ptr(M, "M", sd, sh["M"], dev), _ptr(omega2, "omega2", f32, v, dev),
+            _ptr(phi2, "phi2", f32, v, dev), _ptr(W_up, "W_up", sd, sh["W_up"], dev)]
+    with _on(dev):
+        st = lib().noble_init_params(ctypes.byref(d), ctypes.byref(rc), int(seed) & (2 ** 64 - 1), *args,
+                                     _stream(stream, dev))
     if st != 0:
         raise NobleError(st, "noble_init_params")
 
