@@ -3,7 +3,7 @@
 // Host side: argument validation (complete before any HIP call), workspace
 // layout, launch planning (tile choice, split-K) and kernel launches on the
 // caller's stream.  The library is stateless apart from a per-device cache of
-// the architecture check.
+// the architecture check and a per-thread cache of weight-gradient plans.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -11,7 +11,7 @@
 #include <cmath>
 #include <cstring>
 #include <functional>
-#include <queue>
+#include <map>
 #include <vector>
 
 #include "noble.h"
@@ -241,16 +241,24 @@ struct Batch {
 // epilogue stores and ramp are about 12 us per tile, a chunk 1.45 us).
 double launch_makespan(const std::vector<std::pair<int, int>>& wgs) {
     constexpr double kWgFixed = 12.0, kWgChunk = 1.45;
-    std::priority_queue<double, std::vector<double>, std::greater<double>> cu;
-    for (int i = 0; i < 256; ++i) cu.push(0.0);
+    // CU free times with their multiplicities.  The workgroups of one group
+    // are identical, so handing all the CUs that free first to as many of
+    // them at once gives the same schedule as one at a time, in a handful of
+    // steps: the planner runs on every call.
+    std::map<double, int> free_at{{0.0, 256}};
     double end = 0.0;
-    for (const auto& g : wgs)
-        for (int i = 0; i < g.first; ++i) {
-            const double t = cu.top() + kWgFixed + kWgChunk * g.second;
-            cu.pop();
-            cu.push(t);
-            end = std::max(end, t);
+    for (const auto& g : wgs) {
+        const double d = kWgFixed + kWgChunk * g.second;
+        for (int n = g.first; n > 0;) {
+            const auto it = free_at.begin();
+            const double t = it->first;
+            const int k = std::min(n, it->second);
+            if ((it->second -= k) == 0) free_at.erase(it);
+            free_at[t + d] += k;
+            end = std::max(end, t + d);
+            n -= k;
         }
+    }
     return end;
 }
 
@@ -276,52 +284,89 @@ int choose_split_partials(int tiles, int nk, int64_t MN) {
     return bs;
 }
 
-// Split-K factor of the rank-gradient products (dW_down, dW_up, dM), whose
-// pieces add atomically into zeroed outputs of at most a few MB.  They share
-// a launch with dW (dw_wgs workgroups of dw_chunks K chunks each, launched
-// first); one factor for all of them, the one that minimises the launch's
-// makespan under the list-scheduling model above plus the float atomics of
-// the pieces (split x rank_bytes of output at about 1 MB per us), with at
-// least 8 K chunks per piece.  Candidates are 2^a 3^b: the model is flat near
-// its optimum, and a coarse set keeps its choice off near-ties.
-// rank_tiles: the rank problems' 256 x 256 tile count.
-int choose_rank_split(int dw_wgs, int dw_chunks, int rank_tiles, int nk, int64_t rank_bytes) {
-    constexpr double kAtomicBytesPerUs = 1.0e6;
-    int best = 1;
-    double best_t = 0.0;
-    for (int s : {1, 2, 3, 4, 6, 8, 12, 16}) {
-        if (s > 1 && s * 8 > nk) break;
-        const double t = launch_makespan({{dw_wgs, dw_chunks}, {rank_tiles * s, cdiv(nk, s)}}) +
-                         (double)s * (double)rank_bytes / kAtomicBytesPerUs;
-        if (s == 1 || t < best_t) {
-            best_t = t;
-            best = s;
-        }
-    }
-    return best;
-}
-
-// Split of dW over K = T: its pieces store float32 partials in the scratch
-// that reduce_kernel sums.
+// K splits of the weight-gradient launch (K = T tokens).  dW's pieces store
+// float32 partials that reduce_kernel sums; the rank products (dW_down,
+// dW_up, dM; outputs of a few MB) add their pieces atomically.
+//  - r = 0: dW alone, choose_split_partials.
+//  - r > 0: both splits together (the rank problems share dW's launch and
+//    can fill the CUs that a smaller dW split leaves), minimising the
+//    launch's makespan under the list-scheduling model above plus the dW
+//    partial traffic ((2 S + 1) d_in d_out 4 bytes at 5 MB per us) and the
+//    rank atomics (S x their output bytes at 1 MB per us, fitted on the
+//    square projection).  Candidates are 2^a 3^b up to 16 with at least 8 K
+//    chunks per piece: the model is flat near its optimum, and a coarse set
+//    keeps its choice off near-ties.  dM is counted whatever the activation,
+//    so that the workspace does not depend on it.
 struct WgradPlan {
     int split;      // K pieces of dW
+    int rank;       // K pieces of the rank products
     size_t bytes;   // dW partials
 };
 
-WgradPlan plan_wgrad(int64_t T, int64_t din, int64_t dout, int bk, int tile) {
-    WgradPlan w{1, 0};
+WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
+    WgradPlan w{1, 1, 0};
+    const bool bf = d->dtype == NOBLE_BF16;
+    const int bk = bf ? Elt<uint16_t>::BK : Elt<float>::BK, tile = gemm_tile_of(d);
+    const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
     const int nkT = T > 0 ? cdiv(T, bk) : 0;
     if (nkT == 0) return w;
-    w.split = choose_split_partials(cdiv(din, tile) * cdiv(dout, tile), nkT, din * dout);
-    w.bytes = w.split > 1 ? align_up((size_t)w.split * din * dout * 4) : 0;
+    const int tiles = cdiv(din, tile) * cdiv(dout, tile);
+    const int64_t MN = din * dout;
+    if (r == 0) {
+        w.split = choose_split_partials(tiles, nkT, MN);
+    } else {
+        constexpr double kPartialBytesPerUs = 5.0e6, kAtomicBytesPerUs = 1.0e6;
+        const int64_t R = rank_total(d), dog = group_dout(d);
+        const int G = ngroups(d);
+        const int rank_tiles =
+            cdiv(din, tile) * cdiv(R, tile) + G * (cdiv(r, tile) * cdiv(dog, tile) + cdiv(r, tile) * cdiv(r, tile));
+        const double rank_bytes = 4.0 * (double)(din * R + G * (r * dog + r * r));
+        double best = -1.0;
+        for (int sw : {1, 2, 3, 4, 6, 8, 12, 16}) {
+            if (sw > 1 && sw * 8 > nkT) break;
+            for (int sr : {1, 2, 3, 4, 6, 8, 12, 16}) {
+                if (sr > 1 && sr * 8 > nkT) break;
+                const double t = launch_makespan({{tiles * sw, cdiv(nkT, sw)}, {rank_tiles * sr, cdiv(nkT, sr)}}) +
+                                 (sw > 1 ? (2.0 * sw + 1) * (double)MN * 4 / kPartialBytesPerUs : 0.0) +
+                                 sr * rank_bytes / kAtomicBytesPerUs;
+                if (best < 0 || t < best) {
+                    best = t;
+                    w.split = sw;
+                    w.rank = sr;
+                }
+            }
+        }
+    }
+    w.bytes = w.split > 1 ? align_up((size_t)w.split * MN * 4) : 0;
     return w;
 }
 
-size_t wgrad_need(const noble_linear_desc* d) {
-    return plan_wgrad(d->T, d->d_in, d->d_out, d->dtype == NOBLE_BF16 ? Elt<uint16_t>::BK : Elt<float>::BK,
-                      gemm_tile_of(d))
-        .bytes;
+// The plan depends only on the shape, and the search costs 10-20 us, paid by
+// the workspace query, the forward's size check and the backward: the last
+// eight plans are kept per thread.
+WgradPlan plan_wgrad(const noble_linear_desc* d) {
+    struct Entry {
+        int64_t T, d_in, d_out, r;
+        int32_t dtype, groups;
+        WgradPlan w;
+    };
+    thread_local Entry cache[8];
+    thread_local int used = 0, next = 0;
+    const int32_t G = ngroups(d);
+    for (int i = 0; i < used; ++i) {
+        const Entry& e = cache[i];
+        if (e.T == d->T && e.d_in == d->d_in && e.d_out == d->d_out && e.r == d->r && e.dtype == d->dtype &&
+            e.groups == G)
+            return e.w;
+    }
+    const WgradPlan w = plan_wgrad_uncached(d);
+    cache[next] = Entry{d->T, d->d_in, d->d_out, d->r, d->dtype, G, w};
+    next = (next + 1) % 8;
+    used = std::min(used + 1, 8);
+    return w;
 }
+
+size_t wgrad_need(const noble_linear_desc* d) { return plan_wgrad(d).bytes; }
 
 // `plain`: the r = 0 forward, launched under its own kernel symbol so that
 // profiles can tell it from the K-extended forward.
@@ -564,7 +609,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     // and dp2 (when given).
     constexpr int GBK = gemm_bk<E>();
     const int nkT = cdiv(T, GBK);
-    const WgradPlan wp = plan_wgrad(T, din, dout, GBK, gemm_tile<E>());
+    const WgradPlan wp = plan_wgrad(d);
     float* copies = copies_need(d) ? reinterpret_cast<float*>(base + 4 * reg + partial_need(d)) : nullptr;
     float* wpart = reinterpret_cast<float*>(base + (r > 0 ? 4 * reg + partial_need(d) + copies_need(d) : 0));
 
@@ -663,12 +708,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split,
                wp.split > 1 ? wpart : nullptr);
         if (r > 0) {
-            constexpr int TL = gemm_tile<E>();
-            const int rank_tiles = cdiv(din, TL) * cdiv(R, TL) +
-                                   G * (cdiv(r, TL) * cdiv(dog, TL) + (two ? cdiv(r, TL) * cdiv(r, TL) : 0));
-            const int64_t rank_bytes = 4 * (din * R + G * (r * dog + (two ? r * r : 0)));
-            const int rs = choose_rank_split(cdiv(din, TL) * cdiv(dout, TL) * wp.split, cdiv(nkT, wp.split),
-                                             rank_tiles, nkT, rank_bytes);
+            const int rs = wp.rank;
             bt.add(xT, operand1(seg(dHs, R, T), R), (int)din, (int)R, nkT, dWd, R, true, nullptr, nullptr, rs);
             for (int g = 0; g < G; ++g) {
                 const int64_t c0 = g * r;

@@ -86,14 +86,56 @@ def _copies(R):
     return _align(4 * 8 * R * 4)
 
 
-def _wgrad_bytes(T, di, do, r, bk, tile=256):
+def _makespan(groups):
+    """List scheduling of (count, K chunks) workgroup groups, in launch order,
+    on 256 CUs: each workgroup costs 12 + 1.45 x chunks, dispatched one at a
+    time to the CU that frees first."""
+    import heapq
+    cu, end = [0.0] * 256, 0.0
+    for n, ch in groups:
+        for _ in range(n):
+            t = heapq.heappop(cu) + 12.0 + 1.45 * ch
+            heapq.heappush(cu, t)
+            end = max(end, t)
+    return end
+
+
+def _wgrad_split(T, di, do, r, bk, tile=256, groups=1):
+    """K pieces of dW in the weight-gradient launch.  r = 0: dW alone
+    (_split_partials).  r > 0: dW and the rank products (dW_down, dW_up and
+    dM, counted whatever the activation) together, minimising the makespan
+    plus the dW partial traffic at 5 MB/us and the rank atomics at 1 MB/us;
+    both splits from 2^a 3^b up to 16 with at least 8 K chunks per piece."""
+    nk = -(-T // bk) if T > 0 else 0
+    if nk == 0:
+        return 1
+    cd = lambda a, b: -(-a // b)
+    tiles = cd(di, tile) * cd(do, tile)
+    if r == 0:
+        return _split_partials(tiles, nk, di * do)
+    G, R, dog = groups, groups * r, do // groups
+    rank_tiles = cd(di, tile) * cd(R, tile) + G * (cd(r, tile) * cd(dog, tile) + cd(r, tile) * cd(r, tile))
+    rank_bytes = 4.0 * (di * R + G * (r * dog + r * r))
+    best, pick = None, 1
+    cands = (1, 2, 3, 4, 6, 8, 12, 16)
+    for sw in cands:
+        if sw > 1 and sw * 8 > nk:
+            break
+        for sr in cands:
+            if sr > 1 and sr * 8 > nk:
+                break
+            t = (_makespan([(tiles * sw, cd(nk, sw)), (rank_tiles * sr, cd(nk, sr))])
+                 + ((2.0 * sw + 1) * di * do * 4 / 5.0e6 if sw > 1 else 0.0) + sr * rank_bytes / 1.0e6)
+            if best is None or t < best:
+                best, pick = t, sw
+    return pick
+
+
+def _wgrad_bytes(T, di, do, r, bk, tile=256, groups=1):
     """dW partials: only dW stores partials (the rank gradients add
     atomically).  Output tiles are 256 square on the bf16 path, 128 on the
     float32 path."""
-    nk = -(-T // bk) if T > 0 else 0
-    if nk == 0:
-        return 0
-    sp = _split_partials(-(-di // tile) * -(-do // tile), nk, di * do)
+    sp = _wgrad_split(T, di, do, r, bk, tile, groups)
     return _align(sp * di * do * 4) if sp > 1 else 0
 
 
@@ -103,8 +145,9 @@ def test_workspace_sizes():
     # float32 split-K partials of the weight-gradient products
     st, res, scr = _ws(8192, 2048, 2048, 128, noble.NOBLE_BF16)
     assert _proj_split(8192, 2048) == 4
-    # square 2048 projection: dW in 4 pieces
-    wg = 4 * 2048 * 2048 * 4
+    # square 2048 projection with a branch: dW in 3 pieces (192 workgroups),
+    # the rank problems in 3 pieces on the other 64 CUs of the same wave
+    wg = 3 * 2048 * 2048 * 4
     assert _wgrad_bytes(8192, 2048, 2048, 128, 64) == wg
     assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + _copies(128) + wg
     st, res, scr = _ws(8192, 2048, 8192, 128, noble.NOBLE_BF16)
