@@ -179,6 +179,29 @@ def test_workspace_sizes():
     assert noble.lib().noble_linear_workspace_size(None, None, None) == NULL
 
 
+
+@pytest.mark.parametrize("di,do,r,G,split", [
+    (2048, 6144, 128, 1, 1),   # QKV: 192 dW tiles, the rank problems fill the other 64 CUs
+    (2048, 2048, 128, 1, 3),   # square: 3 dW pieces and 3 rank pieces in one wave
+    (2048, 8192, 128, 1, 1),   # FFN up: one wave of dW, the rank problems split 6 ways after it
+    (8192, 2048, 128, 1, 1),   # FFN down
+    (2048, 6144, 128, 3, 1),   # grouped Q/K/V
+    (2048, 2048, 0, 1, 4),     # the plain square layer: dW alone, 4 pieces
+])
+def test_weight_gradient_plan_of_the_block(di, do, r, G, split):
+    """The dW split the library plans at T = 8192 (visible in the scratch
+    size) matches the independent one-at-a-time scheduler of _wgrad_split."""
+    T = 8192
+    assert _wgrad_split(T, di, do, r, 64, 256, G) == split
+    st, _, scr = _ws(T, di, do, r, noble.NOBLE_BF16, G)
+    R = G * r
+    branch = 0
+    if r > 0:
+        J = G * -(-r // 128)
+        S = max(_proj_split(T, di, J), _proj_split(T, do // G, J))
+        branch = 4 * _align(T * R * 2) + _align(S * T * R * 4) + _copies(R)
+    assert st == OK and scr == branch + _wgrad_bytes(T, di, do, r, 64, 256, G)
+
 def test_workspace_sizes_grouped_and_rank_256():
     """Grouped layers size every rank-side region by R = G r, and the
     projection's split counts one job per (group, 128-rank block)."""
