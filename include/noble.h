@@ -32,10 +32,15 @@
  *    (cosine arguments, cos and sin in float32; C1, C2, dH and the mixing
  *    gradients are rounded to bf16 only where they feed a matrix product),
  *    float32 throughout on the f32 path.
- *  - Shapes: T >= 0 (any value); d_in, d_out >= 8 and multiples of 8;
- *    r = 0 (plain linear: every branch pointer is ignored and may be NULL) or
- *    8 <= r <= 256 (bf16) / 128 (f32) with r a multiple of 8.  Every pointer
- *    must be 16-byte aligned.  Outputs must not alias inputs or each other.
+ *  - Shapes: 0 <= T <= 2^31 - 4096; 8 <= d_in, d_out <= 2^20, multiples of
+ *    8; r = 0 (plain linear: every branch pointer is ignored and may be NULL)
+ *    or 8 <= r <= 256 (bf16) / 128 (f32) with r a multiple of 8.  Each
+ *    matrix product of a call must also fit one dispatch (2^32 - 1
+ *    work-items): at most 8388607 output tiles of 256 x 256 (bf16) or
+ *    16777215 of 128 x 128 (f32) in y = x W, dx and dW (plus, for dW, the
+ *    rank gradients' tiles), which only layers far beyond a GPU's memory
+ *    exceed.  Every pointer must be 16-byte aligned.  Outputs must not alias
+ *    inputs or each other.
  *  - Groups (desc->groups = G, 1 to 4; 0 means 1): the d_out output columns
  *    form G equal blocks that share x, each with its own branch of rank r
  *    (Q, K and V of an attention block, each with its own CosNet,

@@ -164,6 +164,11 @@ noble_status last_launch() { return hipGetLastError() == hipSuccess ? NOBLE_OK :
 
 int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
+// Grid of a launch of n workgroups on rows of kGridRow (see flat_block).
+dim3 flat_grid(int64_t n) {
+    return n <= kGridRow ? dim3((unsigned)n) : dim3(kGridRow, (unsigned)((n + kGridRow - 1) / kGridRow));
+}
+
 Seg seg(const void* p, int64_t ld, int64_t klen) {
     Seg s;
     s.ptr = static_cast<const char*>(p);
@@ -201,6 +206,12 @@ constexpr int gemm_tile() {
 }
 int gemm_tile_of(const noble_linear_desc* d) {
     return d->dtype == NOBLE_BF16 ? gemm_tile<uint16_t>() : gemm_tile<float>();
+}
+
+// Largest workgroup count of one GEMM launch: a dispatch counts its
+// work-items in 32 bits.
+int64_t max_gemm_blocks(const noble_linear_desc* d) {
+    return (int64_t)UINT32_MAX / (d->dtype == NOBLE_BF16 ? kDmaThreads : kThreads);
 }
 
 struct Batch {
@@ -266,14 +277,14 @@ double launch_makespan(const std::vector<std::pair<int, int>>& wgs) {
 // float32 partials that a reduction sums afterwards.  Cost model: the longest
 // CU's share of 64-element K chunks (waves of 256 workgroups) plus the partial
 // traffic (S writes, S reads, one result write).  A split must beat the
-// unsplit cost by 3%.
-int choose_split_partials(int tiles, int nk, int64_t MN) {
+// unsplit cost by 3% and keep the launch within `cap` workgroups.
+int choose_split_partials(int tiles, int nk, int64_t MN, int64_t cap) {
     constexpr double kChunkUs = 1.7;          // one K chunk of a 256 x 256 tile
     constexpr double kBytesPerUs = 5.0e6;     // HBM rate of the partials
     double best = 0;
     int bs = 1;
     for (int s = 1; s <= kMaxReduceSlices; s *= 2) {   // reduce_kernel sums at most that many
-        if (s > 1 && s * 8 > nk) break;
+        if (s > 1 && (s * 8 > nk || (int64_t)tiles * s > cap)) break;
         const double waves = (double)((int64_t)tiles * s + 255) / 256;
         const double cost = (int)waves * ((double)nk / s) * kChunkUs + (s > 1 ? (2.0 * s + 1) * MN * 4 / kBytesPerUs : 0);
         if (s == 1 || cost < best * 0.97) {
@@ -313,7 +324,7 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
     const int tiles = cdiv(din, tile) * cdiv(dout, tile);
     const int64_t MN = din * dout;
     if (r == 0) {
-        w.split = choose_split_partials(tiles, nkT, MN);
+        w.split = choose_split_partials(tiles, nkT, MN, max_gemm_blocks(d));
     } else {
         constexpr double kPartialBytesPerUs = 5.0e6, kAtomicBytesPerUs = 1.0e6;
         const int64_t R = rank_total(d), dog = group_dout(d);
@@ -326,6 +337,7 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
             if (sw > 1 && sw * 8 > nkT) break;
             for (int sr : {1, 2, 3, 4, 6, 8, 12, 16}) {
                 if (sr > 1 && sr * 8 > nkT) break;
+                if ((int64_t)tiles * sw + (int64_t)rank_tiles * sr > max_gemm_blocks(d)) continue;
                 const double t = launch_makespan({{tiles * sw, cdiv(nkT, sw)}, {rank_tiles * sr, cdiv(nkT, sr)}}) +
                                  (sw > 1 ? (2.0 * sw + 1) * (double)MN * 4 / kPartialBytesPerUs : 0.0) +
                                  sr * rank_bytes / kAtomicBytesPerUs;
@@ -368,6 +380,18 @@ WgradPlan plan_wgrad(const noble_linear_desc* d) {
 
 size_t wgrad_need(const noble_linear_desc* d) { return plan_wgrad(d).bytes; }
 
+// Every GEMM launch of the call, unsplit, within max_gemm_blocks (the
+// planner's splits stay within it too).  Only layers far beyond a GPU's
+// memory come near: at the largest T the forward reaches it at d_out > 256.
+noble_status check_grids(const noble_linear_desc* d) {
+    const int64_t tile = gemm_tile_of(d), T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
+    const int64_t G = ngroups(d), dog = group_dout(d), R = rank_total(d);
+    auto tiles = [tile](int64_t m, int64_t n) { return ((m + tile - 1) / tile) * ((n + tile - 1) / tile); };
+    const int64_t fwd = G * tiles(T, dog), dx = tiles(T, din);
+    const int64_t wgrad = tiles(din, dout) + (r > 0 ? tiles(din, R) + G * (tiles(r, dog) + tiles(r, r)) : 0);
+    return std::max({fwd, dx, wgrad}) <= max_gemm_blocks(d) ? NOBLE_OK : NOBLE_ERR_BAD_SHAPE;
+}
+
 // `plain`: the r = 0 forward, launched under its own kernel symbol so that
 // profiles can tell it from the K-extended forward.
 template <typename E, bool AK, bool BKM>
@@ -390,7 +414,7 @@ noble_status launch_gemm(const Batch& bt, hipStream_t st, bool plain = false) {
 // float32 path: chain kernels with their own rank projection, one launch per
 // group (the arguments already point at the group's operands and columns).
 noble_status launch_chain(bool fwd, int RP, int act, const ChainArgs& a, int T, hipStream_t st) {
-    const dim3 grid(cdiv(T, kChainRows)), block(kThreads);
+    const dim3 grid = flat_grid(cdiv(T, kChainRows)), block(kThreads);
     return with_act(act, [&]<Act F, bool L2>() -> noble_status {
 #define NOBLE_CHAIN(RPV)                                                                    \
     if (RP == RPV) {                                                                        \
@@ -438,7 +462,7 @@ noble_status launch_proj(bool fwd, const noble_linear_desc* d, const void* A, co
     a.T = (int)T;
     a.nk = cdiv(fwd ? din : dog, 64);
     a.S = S;
-    const dim3 grid(cdiv(T, kPjRows) * S * a.J), block(kPjThreads);
+    const dim3 grid = flat_grid((int64_t)cdiv(T, kPjRows) * S * a.J), block(kPjThreads);
     if (fwd)
         hipLaunchKernelGGL(proj_kernel<false>, grid, block, 0, st, a);
     else
@@ -474,7 +498,7 @@ noble_status launch_branch(bool fwd, const noble_linear_desc* d, const ChainArgs
     a.G = ngroups(d);
     a.R = (int)rank_total(d);
     const int NT = rank_blocks(d);
-    const dim3 grid(cdiv(d->T, kSkRows) * a.G), block(kThreads * NT);
+    const dim3 grid = flat_grid((int64_t)cdiv(d->T, kSkRows) * a.G), block(kThreads * NT);
     return with_act(d->activation, [&]<Act F, bool L2>() -> noble_status {
         if (NT == 1) {
             if (fwd)
@@ -780,6 +804,7 @@ const char* noble_status_string(int status) {
 noble_status noble_linear_workspace_size(const noble_linear_desc* desc, size_t* reserve_bytes,
                                          size_t* scratch_bytes) {
     NOBLE_TRY(check_desc(desc));
+    NOBLE_TRY(check_grids(desc));
     if (reserve_bytes) *reserve_bytes = reserve_need(desc);
     if (scratch_bytes) *scratch_bytes = scratch_need(desc);
     return NOBLE_OK;
@@ -790,6 +815,7 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, cons
                               const float* omega2, const float* phi2, const void* W_up, void* y, void* reserve,
                               void* scratch, size_t scratch_bytes, void* stream) {
     NOBLE_TRY(check_desc(desc));
+    NOBLE_TRY(check_grids(desc));
     const bool rows = desc->T > 0, br = desc->r > 0;
     NOBLE_TRY(need(x, rows));
     NOBLE_TRY(need(W, true));
@@ -823,6 +849,7 @@ noble_status noble_linear_bwd(const noble_linear_desc* desc, const void* dy, con
                               float* dphi1, float* domega2, float* dphi2, void* scratch, size_t scratch_bytes,
                               void* stream) {
     NOBLE_TRY(check_desc(desc));
+    NOBLE_TRY(check_grids(desc));
     const bool rows = desc->T > 0, br = desc->r > 0;
     NOBLE_TRY(need(dy, rows));
     NOBLE_TRY(need(x, rows));

@@ -29,6 +29,16 @@
 
 namespace noble {
 
+// ------------------------------------------------------------- launch grids --
+
+// A dispatch counts its work-items in 32 bits per grid dimension.  The
+// launches whose workgroup count grows with T (the chain, projection and
+// branch kernels: up to 2^28 workgroups at the largest T) therefore run on
+// rows of kGridRow workgroups: workgroup b sits at (b % kGridRow, b /
+// kGridRow), and the surplus of the last row exits on entry.
+constexpr int kGridRow = 65536;
+__device__ __forceinline__ int64_t flat_block() { return (int64_t)blockIdx.y * gridDim.x + blockIdx.x; }
+
 // ---------------------------------------------------------------- zero fill --
 
 constexpr int kMaxZero = 10;
@@ -183,7 +193,9 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r16 = lane & 15, g = lane >> 4;
     const int wm0 = (wave >> 1) * 16, wn0 = (wave & 1) * (RP / 2);
-    const int m0 = blockIdx.x * kChainRows;
+    const int64_t wg = flat_block();
+    if (wg * kChainRows >= a.T) return;
+    const int m0 = (int)wg * kChainRows;
     const int r = a.r;
 
     f32x4 acc[1][TN];
@@ -250,7 +262,9 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r16 = lane & 15, g = lane >> 4;
     const int wm0 = (wave >> 1) * 16, wn0 = (wave & 1) * (RP / 2);
-    const int m0 = blockIdx.x * kChainRows;
+    const int64_t wg = flat_block();
+    if (wg * kChainRows >= a.T) return;
+    const int m0 = (int)wg * kChainRows;
     const int r = a.r;
 
     // dC2 = dy W_up^T

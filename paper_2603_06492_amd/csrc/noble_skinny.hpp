@@ -249,8 +249,10 @@ __global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
     const int blocks = (a.T + kPjRows - 1) / kPjRows;
-    const int ji = blockIdx.x / (blocks * a.S);
-    const int rem = blockIdx.x - ji * blocks * a.S;
+    const int64_t wg = flat_block(), nb = (int64_t)blocks * a.S * a.J;
+    if (wg >= nb) return;
+    const int ji = (int)(wg / (blocks * a.S));
+    const int rem = (int)(wg - (int64_t)ji * blocks * a.S);
     const int piece = rem / blocks;
     const int row0 = (rem - piece * blocks) * kPjRows;
     const ProjJob& jb = a.job[ji];
@@ -281,8 +283,8 @@ __global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
     // The zeroing rides on the projection: every workgroup clears a strided
     // share while its first loads are in flight.
     {
-        const int64_t stride = (int64_t)gridDim.x * kPjThreads;
-        const int64_t gid = (int64_t)blockIdx.x * kPjThreads + tid;
+        const int64_t stride = nb * kPjThreads;
+        const int64_t gid = wg * kPjThreads + tid;
         for (int s = 0; s < a.z.count; ++s) {
             float* p = a.z.ptr[s];
             const int64_t cnt = a.z.n[s];
@@ -374,9 +376,14 @@ struct ChainPos {
     int row0, g, c0;
 };
 __device__ __forceinline__ ChainPos chain_pos(const BranchArgs& a) {
-    const int tb = blockIdx.x / a.G;
-    const int g = blockIdx.x - tb * a.G;
+    const int64_t wg = flat_block();
+    const int tb = (int)(wg / a.G);
+    const int g = (int)(wg - (int64_t)tb * a.G);
     return ChainPos{tb * kSkRows, g, g * a.r};
+}
+// False for the surplus workgroups of the last grid row.
+__device__ __forceinline__ bool chain_live(const BranchArgs& a) {
+    return flat_block() < (int64_t)((a.T + kSkRows - 1) / kSkRows) * a.G;
 }
 
 // Buffer resource over the group's columns of a [T, R] array from token row0
@@ -396,6 +403,7 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
     char* ct = mt + NT * NT * kSkM;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
+    if (!chain_live(a)) return;
     const ChainPos q = chain_pos(a);
     const int r = a.r, R = a.R;
 
@@ -458,6 +466,7 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     char* ct = mt + NT * NT * kSkM;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
+    if (!chain_live(a)) return;
     const ChainPos q = chain_pos(a);
     const int r = a.r, R = a.R;
     // targets of the frequency / phase gradient sums
@@ -466,7 +475,7 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     float* gw2 = a.dw2;
     float* gp2 = a.dp2;
     if (a.copies) {
-        float* c = a.copies + (int64_t)(blockIdx.x % kChainCopies) * R;
+        float* c = a.copies + (flat_block() % kChainCopies) * R;
         const int64_t arr = (int64_t)kChainCopies * R;
         gw1 = c;
         gp1 = c + arr;

@@ -235,6 +235,33 @@ def test_f32_rank_limit():
     assert _ws(16, 64, 64, 136, noble.NOBLE_F32)[0] == SHAPE
 
 
+TMAX = (1 << 31) - 4096
+
+
+@pytest.mark.parametrize("shape,dtype,code", [
+    # the forward at the largest T: 8388592 token tiles of 256 (bf16, 512
+    # threads each) fit one dispatch once, not twice; float32 tiles of 128
+    # (256 threads) likewise
+    ((TMAX, 8, 256, 8), noble.NOBLE_BF16, OK), ((TMAX, 8, 264, 8), noble.NOBLE_BF16, SHAPE),
+    ((TMAX + 1, 8, 8, 0), noble.NOBLE_BF16, SHAPE),
+    ((TMAX, 8, 128, 8), noble.NOBLE_F32, OK), ((TMAX, 8, 136, 8), noble.NOBLE_F32, SHAPE),
+    ((TMAX, 264, 8, 8), noble.NOBLE_BF16, SHAPE),   # dx
+    # dW: 2^20 x (2^19 - 256) is 8384512 tiles, 2^20 x 2^19 is 8388608
+    ((1, 1 << 20, (1 << 19) - 256, 0), noble.NOBLE_BF16, OK),
+    ((1, 1 << 20, 1 << 19, 0), noble.NOBLE_BF16, SHAPE),
+    ((0, 1 << 20, 1 << 20, 0), noble.NOBLE_BF16, SHAPE),
+    ((16, 1 << 20, 1 << 20, 0), noble.NOBLE_F32, SHAPE),
+    ((16, 1 << 20, (1 << 18) - 128, 0), noble.NOBLE_F32, OK),   # 16769024 tiles of 128
+    ((16, 1 << 20, 1 << 18, 0), noble.NOBLE_F32, SHAPE),          # 16777216
+])
+def test_launch_grid_limits(shape, dtype, code):
+    """A dispatch counts its work-items in 32 bits: a call whose GEMM
+    launch would pass 2^32 - 1 is rejected (only layers far beyond a GPU's
+    memory come near).  The rank-side launches, whose workgroup count grows
+    with T, run on two-dimensional grids and set no limit of their own."""
+    assert _ws(*shape, dtype)[0] == code
+
+
 @pytest.mark.parametrize("do,groups,code", [
     (96, 3, OK), (96, 4, OK), (104, 4, SHAPE), (128, 4, OK), (64, 0, OK), (64, 1, OK), (80, 5, SHAPE),
     (64, -1, SHAPE), (72, 3, OK), (64, 3, SHAPE),

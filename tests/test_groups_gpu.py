@@ -105,3 +105,31 @@ def test_full_size_grouped_and_r256(shape):
     for k, e in rep.items():
         assert e <= TOL["bf16"], (k, e)
     assert ok
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_two_dimensional_grids(dt):
+    """T = 2^21 + 4133 tokens, four groups of r = 8: the launches whose
+    workgroup count grows with T pass the 65536 workgroups of one grid row
+    (bf16: 65668 projection workgroups and 262664 branch workgroups; f32:
+    65666 chain workgroups per group), so workgroups past the first row, and
+    the surplus of the last one, are exercised.  y and dx on sampled rows
+    (both ends and the first row boundaries), every weight gradient in full."""
+    T, di, do, r, G = (1 << 21) + 4133, 32, 64, 8, 4
+    name = f"{dt}_g4_r8_T{T}"
+    _say(f"[groups] {name}: T={T} d_in={di} d_out={do} r={r} groups={G} {dt}")
+    p = inp.draw_projection(name, T, di, do, r, dt, seed=305, bias_std=0.5, groups=G)
+    # first tokens of the second grid row: branch (32-token blocks x G),
+    # f32 chain (32-token blocks), projection (128-token blocks x G jobs)
+    edges = np.array([32 * 65536 // G, 32 * 65536, 65536 % -(-T // 128) * 128])
+    rows = np.unique(np.concatenate([_sample(T, 24, 5), edges - 1, edges]))
+    dp = _run(p)
+    got = dp.outputs(rows=rows)
+    ok = dp.guards_intact()
+    del dp
+    rep = parity_report(got, oracle_outputs(p, rows=rows))
+    _say(rep)
+    assert set(rep) == set(OUTPUTS)
+    for k, e in rep.items():
+        assert e <= TOL[dt], (k, e)
+    assert ok
