@@ -489,6 +489,17 @@ def _make_module():
         def reset_parameters(self, seed=0):
             noble_init_params(self.W, self.b, *self._branch(), seed=seed, recipe=self.recipe, groups=self.groups)
 
+        def _infer(self, x2):
+            # Nothing to differentiate: the forward without the reserve, so H
+            # is neither written nor kept.
+            T = x2.shape[0]
+            _, scratch = alloc_workspace(T, self.d_in, self.d_out, self.r, _dtype_code(x2), x2.device,
+                                         groups=self.groups)
+            y = torch.empty((T, self.d_out), dtype=x2.dtype, device=x2.device)
+            noble_linear_fwd(x2, self.W, self.b, *self._branch(), y, None, scratch,
+                             activation=activation_code(self.activation), groups=self.groups)
+            return y
+
         def param_groups(self, lr):
             """Optimizer parameter groups with the layer's learning-rate
             multipliers (Sec. 3.3 Eqs. 3-4, App. A)."""
@@ -500,6 +511,8 @@ def _make_module():
         def forward(self, x):
             lead = x.shape[:-1]
             x2 = x.reshape(-1, self.d_in).contiguous()
+            if not torch.is_grad_enabled() or not (x2.requires_grad or any(p.requires_grad for p in self.parameters())):
+                return self._infer(x2).reshape(*lead, self.d_out)
             if self.r == 0:
                 # plain layer: the same library call with no branch
                 y = Function.apply(x2, self.W, self.b, torch.empty((self.d_in, 0), dtype=x.dtype, device=x.device),

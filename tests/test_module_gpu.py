@@ -79,6 +79,32 @@ def test_module_matches_oracle(act, G, r):
         assert e <= TOL["bf16"], (k, e)
 
 
+@pytest.mark.parametrize("act,G,r", [("cosnet", 1, 40), ("tanh", 2, 24), ("cosnet", 1, 0)])
+def test_module_inference_forward(act, G, r):
+    """Under no_grad (or with nothing requiring a gradient) the module runs
+    the forward without the reserve: y is bit for bit the y of the forward
+    that records the graph."""
+    import torch
+    print(f"[module] inference {act} groups={G} r={r}", flush=True)
+    m = noble.NobleLinear(136, 144, r, activation=act, groups=G, seed=13)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    if r > 0:
+        with torch.no_grad():
+            m.W_up.copy_(torch.randn(m.W_up.shape, device="cuda", generator=g) / np.sqrt(r))
+    x = torch.randn(3, 41, 136, device="cuda", generator=g).to(torch.bfloat16)
+    y_grad = m(x)
+    assert y_grad.requires_grad
+    with torch.no_grad():
+        y_nograd = m(x)
+    m.requires_grad_(False)
+    y_frozen = m(x)
+    torch.cuda.synchronize()
+    assert not y_nograd.requires_grad and not y_frozen.requires_grad
+    assert y_nograd.shape == (3, 41, 144)
+    for y in (y_nograd, y_frozen):
+        assert bool((y.view(torch.int16) == y_grad.detach().view(torch.int16)).all())
+
+
 def test_module_param_groups_and_training_steps():
     import torch
     d_in, d_out, r = 256, 256, 32
