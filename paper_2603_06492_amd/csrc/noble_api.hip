@@ -160,7 +160,16 @@ noble_status check_device() {
     return s == 1 ? NOBLE_OK : NOBLE_ERR_UNSUPPORTED_DEVICE;
 }
 
-noble_status last_launch() { return hipGetLastError() == hipSuccess ? NOBLE_OK : NOBLE_ERR_HIP; }
+// Launch of a kernel that takes one argument struct, with the status of this
+// launch itself (the thread's last-error state would also carry, and clear,
+// an earlier failure of the caller's).
+template <typename Arg>
+noble_status launch(void (*kernel)(Arg), dim3 grid, dim3 block, hipStream_t st, const Arg& arg) {
+    void* argv[] = {const_cast<Arg*>(&arg)};
+    return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, 0, st) == hipSuccess
+               ? NOBLE_OK
+               : NOBLE_ERR_HIP;
+}
 
 int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
@@ -399,16 +408,12 @@ noble_status launch_gemm(const Batch& bt, hipStream_t st, bool plain = false) {
     if (bt.blocks == 0) return NOBLE_OK;
     if constexpr (sizeof(E) == 2) {
         if (AK && !BKM && plain)
-            hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKM, false, 1>), dim3(bt.blocks), dim3(kDmaThreads), 0, st,
-                               bt.b);
-        else
-            hipLaunchKernelGGL((gemm_bf16_kernel<AK, BKM, !AK && !BKM, 0>), dim3(bt.blocks), dim3(kDmaThreads), 0,
-                               st, bt.b);
-    } else
-        hipLaunchKernelGGL((gemm_kernel<E, gemm_tile<E>(), gemm_tile<E>(), AK, BKM, !AK && !BKM>), dim3(bt.blocks),
-                           dim3(kThreads), 0,
-                           st, bt.b);
-    return last_launch();
+            return launch(gemm_bf16_kernel<AK, BKM, false, 1>, dim3(bt.blocks), dim3(kDmaThreads), st, bt.b);
+        return launch(gemm_bf16_kernel<AK, BKM, !AK && !BKM, 0>, dim3(bt.blocks), dim3(kDmaThreads), st, bt.b);
+    } else {
+        return launch(gemm_kernel<E, gemm_tile<E>(), gemm_tile<E>(), AK, BKM, !AK && !BKM>, dim3(bt.blocks),
+                      dim3(kThreads), st, bt.b);
+    }
 }
 
 // float32 path: chain kernels with their own rank projection, one launch per
@@ -416,14 +421,10 @@ noble_status launch_gemm(const Batch& bt, hipStream_t st, bool plain = false) {
 noble_status launch_chain(bool fwd, int RP, int act, const ChainArgs& a, int T, hipStream_t st) {
     const dim3 grid = flat_grid(cdiv(T, kChainRows)), block(kThreads);
     return with_act(act, [&]<Act F, bool L2>() -> noble_status {
-#define NOBLE_CHAIN(RPV)                                                                    \
-    if (RP == RPV) {                                                                        \
-        if (fwd)                                                                            \
-            hipLaunchKernelGGL((fwd_chain_kernel<float, RPV, F, L2>), grid, block, 0, st, a); \
-        else                                                                                \
-            hipLaunchKernelGGL((bwd_chain_kernel<float, RPV, F, L2>), grid, block, 0, st, a); \
-        return last_launch();                                                               \
-    }
+#define NOBLE_CHAIN(RPV)                                                                       \
+    if (RP == RPV)                                                                             \
+        return fwd ? launch(fwd_chain_kernel<float, RPV, F, L2>, grid, block, st, a)           \
+                   : launch(bwd_chain_kernel<float, RPV, F, L2>, grid, block, st, a);
         NOBLE_CHAIN(32)
         NOBLE_CHAIN(64)
         NOBLE_CHAIN(128)
@@ -463,11 +464,7 @@ noble_status launch_proj(bool fwd, const noble_linear_desc* d, const void* A, co
     a.nk = cdiv(fwd ? din : dog, 64);
     a.S = S;
     const dim3 grid = flat_grid((int64_t)cdiv(T, kPjRows) * S * a.J), block(kPjThreads);
-    if (fwd)
-        hipLaunchKernelGGL(proj_kernel<false>, grid, block, 0, st, a);
-    else
-        hipLaunchKernelGGL(proj_kernel<true>, grid, block, 0, st, a);
-    return last_launch();
+    return fwd ? launch(proj_kernel<false>, grid, block, st, a) : launch(proj_kernel<true>, grid, block, st, a);
 }
 
 // bf16 path, step 2: the branch nonlinearity (forward or backward) from the
@@ -500,18 +497,11 @@ noble_status launch_branch(bool fwd, const noble_linear_desc* d, const ChainArgs
     const int NT = rank_blocks(d);
     const dim3 grid = flat_grid((int64_t)cdiv(d->T, kSkRows) * a.G), block(kThreads * NT);
     return with_act(d->activation, [&]<Act F, bool L2>() -> noble_status {
-        if (NT == 1) {
-            if (fwd)
-                hipLaunchKernelGGL((branch_fwd_kernel<F, L2, 1>), grid, block, 0, st, a);
-            else
-                hipLaunchKernelGGL((branch_bwd_kernel<F, L2, 1>), grid, block, 0, st, a);
-        } else {
-            if (fwd)
-                hipLaunchKernelGGL((branch_fwd_kernel<F, L2, 2>), grid, block, 0, st, a);
-            else
-                hipLaunchKernelGGL((branch_bwd_kernel<F, L2, 2>), grid, block, 0, st, a);
-        }
-        return last_launch();
+        if (NT == 1)
+            return fwd ? launch(branch_fwd_kernel<F, L2, 1>, grid, block, st, a)
+                       : launch(branch_bwd_kernel<F, L2, 1>, grid, block, st, a);
+        return fwd ? launch(branch_fwd_kernel<F, L2, 2>, grid, block, st, a)
+                   : launch(branch_bwd_kernel<F, L2, 2>, grid, block, st, a);
     });
 }
 
@@ -668,8 +658,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     // On the bf16 path with a branch, the projection kernel does the zeroing.
     const bool zero_in_proj = sizeof(E) == 2 && r > 0 && T > 0;
     if (z.count > 0 && !zero_in_proj) {
-        hipLaunchKernelGGL(zero_kernel, dim3(512), dim3(256), 0, st, z);
-        NOBLE_TRY(last_launch());
+        NOBLE_TRY(launch(zero_kernel, dim3(512), dim3(256), st, z));
     }
     if (T == 0) return NOBLE_OK;
 
@@ -773,8 +762,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             red.first[0] = 0;
             for (int a = 0; a < red.count; ++a)
                 red.first[a + 1] = red.first[a] + (int)std::min<int64_t>(1024, std::max<int64_t>(1, cdiv(red.n[a], 4 * 256)));
-            hipLaunchKernelGGL(reduce_kernel, dim3(red.first[red.count]), dim3(256), 0, st, red);
-            NOBLE_TRY(last_launch());
+            NOBLE_TRY(launch(reduce_kernel, dim3(red.first[red.count]), dim3(256), st, red));
         }
     }
     return NOBLE_OK;
@@ -958,8 +946,7 @@ noble_status noble_init_params(const noble_linear_desc* desc, const noble_recipe
     }
     if (L.count == 0) return NOBLE_OK;
     NOBLE_TRY(check_device());
-    hipLaunchKernelGGL(init_kernel, dim3(1024), dim3(256), 0, static_cast<hipStream_t>(stream), L);
-    return last_launch();
+    return launch(init_kernel, dim3(1024), dim3(256), static_cast<hipStream_t>(stream), L);
 }
 
 }  // extern "C"

@@ -196,6 +196,29 @@ def test_backward_repeatable():
         assert e <= TOL["bf16"] / 10, (k, e)
 
 
+def test_pending_hip_error_of_the_caller():
+    """A failed HIP call of the caller's, pending in the thread's last-error
+    state, is not taken for a failure of the library's launches: the calls
+    succeed, and y, dx and dW are bit for bit those of a clean run."""
+    import ctypes
+    _torch_gpu()
+    hip = ctypes.CDLL("libamdhip64.so")
+    p = inp.draw_projection("pending", 300, 256, 264, 40, "bf16", seed=14, bias_std=0.5)
+    _say("[parity] pending caller error")
+    dp = _run(p)
+    clean = dp.outputs()
+    assert hip.hipGetLastError() == 0
+    assert hip.hipSetDevice(ctypes.c_int(1 << 20)) != 0   # an ordinal no box has
+    try:
+        dp.fwd()
+        dp.bwd()
+    finally:
+        hip.hipGetLastError()   # clear it: torch checks the state after its own launches
+    again = dp.outputs()
+    for k in ("y", "dx", "dW"):
+        assert np.array_equal(clean[k], again[k]), k
+
+
 def test_autograd_function():
     torch = _torch_gpu()
     from paper_2603_06492_amd.noble import NobleLinearFunction
