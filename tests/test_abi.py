@@ -7,6 +7,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 from paper_2603_06492_amd import noble
@@ -444,3 +445,24 @@ def test_reserved_field_must_be_zero():
     a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
     assert noble.lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(a), ctypes.byref(b)) == SHAPE
     assert _fwd(d, FAKE[:13], 1 << 30) == SHAPE
+
+
+def test_workspace_queries_from_many_threads():
+    """The weight-gradient plan behind the scratch size is cached per thread
+    (eight entries): many threads querying more shapes than a cache holds,
+    in different orders, get the single-threaded answers."""
+    from concurrent.futures import ThreadPoolExecutor
+    shapes = [(T, di, do, r, G) for T in (1000, 8192, 40000) for (di, do, r, G) in
+              ((2048, 6144, 128, 3), (2048, 2048, 128, 1), (8192, 2048, 64, 1), (512, 384, 0, 1))]
+    want = {s: _ws(*s[:4], noble.NOBLE_BF16, s[4]) for s in shapes}
+
+    def worker(seed):
+        rng = np.random.default_rng(seed)
+        bad = 0
+        for _ in range(300):
+            s = shapes[rng.integers(len(shapes))]
+            bad += _ws(*s[:4], noble.NOBLE_BF16, s[4]) != want[s]
+        return bad
+
+    with ThreadPoolExecutor(8) as ex:
+        assert sum(ex.map(worker, range(16))) == 0
