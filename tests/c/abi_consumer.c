@@ -74,6 +74,11 @@ int main(void) {
     bad = desc(64, 64, 64, 8, NOBLE_BF16);
     bad.activation = 8;
     CHECK(noble_linear_workspace_size(&bad, &reserve, &scratch) == NOBLE_ERR_BAD_ACTIVATION);
+    /* a forward product past one dispatch: 8388592 token tiles x 2 column tiles */
+    bad = desc(2147483648LL - 4096, 8, 264, 8, NOBLE_BF16);
+    CHECK(noble_linear_workspace_size(&bad, &reserve, &scratch) == NOBLE_ERR_BAD_SHAPE);
+    bad = desc(2147483648LL - 4096, 8, 256, 8, NOBLE_BF16);
+    CHECK(noble_linear_workspace_size(&bad, &reserve, &scratch) == NOBLE_OK);
 
     /* the compute calls reject a bad descriptor before any HIP call */
     bad = desc(64, 60, 64, 8, NOBLE_BF16);
