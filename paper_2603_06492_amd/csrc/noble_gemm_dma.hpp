@@ -151,6 +151,14 @@ struct FragAddr {
 
 constexpr int kDmaWM = 2, kDmaWN = 4, kDmaThreads = 64 * kDmaWM * kDmaWN;
 
+// Cache policy of the epilogue's plain stores: non-temporal (the NT bit of
+// the buffer instruction's cache-policy operand).  The product is bound by
+// the MFMAs, so its output can go to HBM while it runs; stored with the
+// default policy it stays dirty in the memory-side cache and is written back
+// while the next kernel, often a bandwidth-bound rank projection, reads its
+// own operand.  Measured on the 1.5B-style block step: 3-4% less time.
+constexpr int kStoreNT = 2;
+
 // TAG only separates launch sites in profiles (1: the plain r = 0 forward);
 // the code is the same.
 template <bool AK, bool BKM, bool HAS_BSUM, int TAG>
@@ -355,11 +363,11 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
         });
     else if (P.out_f32)
         epilogue([&](float val, uint32_t vo, uint32_t so) {
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), rc, vo, so, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), rc, vo, so, kStoreNT);
         });
     else
         epilogue([&](float val, uint32_t vo, uint32_t so) {
-            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(val), rc, vo, so, 0);
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(val), rc, vo, so, kStoreNT);
         });
 }
 
