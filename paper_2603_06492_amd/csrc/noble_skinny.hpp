@@ -343,20 +343,35 @@ __global__ __launch_bounds__(kPjThreads, 1) void proj_kernel(ProjArgs a) {
 }
 
 // acc[v] = sum over the S partials of token row0 + 8(v/4) + 4h + v%4, rank
-// column c0 + col of the group (zero past T or past the group's r).
+// column c0 + col of the group (zero past T or past the group's r).  The
+// partials are loaded four at a time, all loads of a batch issued before any
+// is used, so S <= 4 costs one memory round trip; the sum keeps the order
+// partial 0, 1, 2, ...  Slots past S read through a zero-length buffer (no
+// memory access, value 0), which leaves the sum unchanged.
 __device__ __forceinline__ void sum_partials(const BranchArgs& a, int row0, int c0, int col, int h, f32x16& acc) {
+    constexpr int kBatch = 4;
     const int R = a.R;
     const uint32_t vo = col < a.r ? (uint32_t)(((4 * h) * R + col) * 4) : kOOB;
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-    for (int s = 0; s < a.S; ++s) {
-        const __amdgpu_buffer_rsrc_t rp =
-            make_rsrc(reinterpret_cast<const char*>(a.P + s * a.pstride + c0) + (int64_t)row0 * R * 4,
-                      (int64_t)(a.T - row0) * R * 4);
+    for (int s0 = 0; s0 < a.S; s0 += kBatch) {
+        float x[kBatch][16];
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-            acc[v] += __uint_as_float(
-                __builtin_amdgcn_raw_buffer_load_b32(rp, vo, (uint32_t)((8 * (v >> 2) + (v & 3)) * R * 4), 0));
+        for (int i = 0; i < kBatch; ++i) {
+            const bool live = s0 + i < a.S;
+            const __amdgpu_buffer_rsrc_t rp =
+                make_rsrc(reinterpret_cast<const char*>(a.P + (live ? (s0 + i) * a.pstride : 0) + c0) +
+                              (int64_t)row0 * R * 4,
+                          live ? (int64_t)(a.T - row0) * R * 4 : 0);
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                x[i][v] = __uint_as_float(
+                    __builtin_amdgcn_raw_buffer_load_b32(rp, vo, (uint32_t)((8 * (v >> 2) + (v & 3)) * R * 4), 0));
+        }
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[v] += x[i][v];
     }
 }
 
@@ -485,12 +500,8 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
 
     if constexpr (L2) m_dma<NT>(a.M + (int64_t)q.g * r * r, r, mt, wave, lane);
     const int col = 32 * wave + r32;
-    f32x16 dc2;
-    sum_partials(a, q.row0, q.c0, col, h, dc2);   // dC2 = dy W_up^T
-
     const bool cv = col < r;
     const int gc = q.c0 + col;   // column of the [R] vectors
-    const float w1 = cv ? a.w1[gc] : 0.f, p1 = cv ? a.p1[gc] : 0.f;
     const int64_t rows_left = a.T - q.row0;
     const __amdgpu_buffer_rsrc_t rh = group_rsrc(a.H, a, q, 4);
     const __amdgpu_buffer_rsrc_t rc2 = group_rsrc(a.C2s, a, q, 2), rdh = group_rsrc(a.dHs, a, q, 2);
@@ -498,12 +509,16 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * R + col) * 2) : kOOB;
     auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * R * es); };
 
-    // H from the reserve (rows past T and columns past r read as zero);
-    // A1 = H w1 + p1, keep f'(A1)
+    // H from the reserve (rows past T and columns past r read as zero),
+    // issued before the partial sums so that both arrive in one round trip
     float hr[16], d1[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v)
         hr[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rh, vo4, soff(v, 4), 0));
+    f32x16 dc2;
+    sum_partials(a, q.row0, q.c0, col, h, dc2);   // dC2 = dy W_up^T
+    // A1 = H w1 + p1, keep f'(A1)
+    const float w1 = cv ? a.w1[gc] : 0.f, p1 = cv ? a.p1[gc] : 0.f;
 
     // dC1: dC2 itself (one application) or dH2 M^T (two)
     f32x16 dc1;
