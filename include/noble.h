@@ -154,11 +154,11 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc,
  *   dx [T, d_in] (storage dtype), dW [d_in, d_out], db [d_out] (nullable =
  *   not computed), dW_down [d_in, r], dM [r, r], dW_up [r, d_out],
  *   domega1, dphi1, domega2, dphi2 [r]  (all float32).
- * With T = 0 the parameter gradients are set to zero.  db, the four
- * omega / phi gradients and the rank gradients dW_down, dM and dW_up are
- * summed over tokens with float atomics (the rank gradients when their
- * token sum is split into pieces), so they may differ in the last bits
- * between runs; dx and dW are reproducible.  scratch (>= scratch_bytes) may be NULL only when
+ * With T = 0 the parameter gradients are set to zero.  db and the four
+ * omega / phi gradients are summed over tokens with float atomics, so they
+ * may differ in the last bits between runs; dx, dW, dW_down, dM and dW_up
+ * are reproducible (a token sum split into pieces stores per-piece partials
+ * that are added in a fixed order).  scratch (>= scratch_bytes) may be NULL only when
  * scratch_bytes is 0 or T is 0.  With a one-application activation, M,
  * omega2 and phi2 are not read, and dM, domega2, dphi2 may be NULL; when
  * given they are set to zero (the function does not depend on them). */

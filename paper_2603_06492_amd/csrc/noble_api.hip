@@ -304,27 +304,29 @@ int choose_split_partials(int tiles, int nk, int64_t MN, int64_t cap) {
     return bs;
 }
 
-// K splits of the weight-gradient launch (K = T tokens).  dW's pieces store
-// float32 partials that reduce_kernel sums; the rank products (dW_down,
-// dW_up, dM; outputs of a few MB) add their pieces atomically.
+// K splits of the weight-gradient launch (K = T tokens).  The pieces of
+// every product (dW, and the rank products dW_down, dW_up, dM) store float32
+// partials that reduce_kernel sums in piece order.  Float atomics were used
+// for the rank products before: they are device-scope, so the eight XCDs'
+// adds meet beyond their L2s, and they cost about 1 MB of output per us.
 //  - r = 0: dW alone, choose_split_partials.
 //  - r > 0: both splits together (the rank problems share dW's launch and
 //    can fill the CUs that a smaller dW split leaves), minimising the
 //    launch's makespan under the list-scheduling model above plus the dW
-//    partial traffic ((2 S + 1) d_in d_out 4 bytes at 5 MB per us) and the
-//    rank atomics (S x their output bytes at 1 MB per us, fitted on the
-//    square projection).  Candidates are 2^a 3^b up to 16 with at least 8 K
+//    partial traffic of both products ((2 S + 1) x their output bytes at
+//    5 MB per us).  Candidates are 2^a 3^b up to 16 with at least 8 K
 //    chunks per piece: the model is flat near its optimum, and a coarse set
 //    keeps its choice off near-ties.  dM is counted whatever the activation,
 //    so that the workspace does not depend on it.
 struct WgradPlan {
     int split;      // K pieces of dW
     int rank;       // K pieces of the rank products
-    size_t bytes;   // dW partials
+    size_t bytes;        // dW partials
+    size_t rank_bytes;   // rank-product partials, [rank][d_in R], then per group [rank][r d_out/G], [rank][r r]
 };
 
 WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
-    WgradPlan w{1, 1, 0};
+    WgradPlan w{1, 1, 0, 0};
     const bool bf = d->dtype == NOBLE_BF16;
     const int bk = bf ? Elt<uint16_t>::BK : Elt<float>::BK, tile = gemm_tile_of(d);
     const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
@@ -335,7 +337,7 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
     if (r == 0) {
         w.split = choose_split_partials(tiles, nkT, MN, max_gemm_blocks(d));
     } else {
-        constexpr double kPartialBytesPerUs = 5.0e6, kAtomicBytesPerUs = 1.0e6;
+        constexpr double kPartialBytesPerUs = 5.0e6;
         const int64_t R = rank_total(d), dog = group_dout(d);
         const int G = ngroups(d);
         const int rank_tiles =
@@ -349,7 +351,7 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
                 if ((int64_t)tiles * sw + (int64_t)rank_tiles * sr > max_gemm_blocks(d)) continue;
                 const double t = launch_makespan({{tiles * sw, cdiv(nkT, sw)}, {rank_tiles * sr, cdiv(nkT, sr)}}) +
                                  (sw > 1 ? (2.0 * sw + 1) * (double)MN * 4 / kPartialBytesPerUs : 0.0) +
-                                 sr * rank_bytes / kAtomicBytesPerUs;
+                                 (sr > 1 ? (2.0 * sr + 1) * rank_bytes / kPartialBytesPerUs : 0.0);
                 if (best < 0 || t < best) {
                     best = t;
                     w.split = sw;
@@ -359,6 +361,10 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
         }
     }
     w.bytes = w.split > 1 ? align_up((size_t)w.split * MN * 4) : 0;
+    if (r > 0 && w.rank > 1) {
+        const int64_t G = ngroups(d), rr = r, R = rank_total(d), dog = group_dout(d);
+        w.rank_bytes = align_up((size_t)w.rank * (size_t)(din * R + G * (rr * dog + rr * rr)) * 4);
+    }
     return w;
 }
 
@@ -387,7 +393,10 @@ WgradPlan plan_wgrad(const noble_linear_desc* d) {
     return w;
 }
 
-size_t wgrad_need(const noble_linear_desc* d) { return plan_wgrad(d).bytes; }
+size_t wgrad_need(const noble_linear_desc* d) {
+    const WgradPlan w = plan_wgrad(d);
+    return w.bytes + w.rank_bytes;
+}
 
 // Every GEMM launch of the call, unsplit, within max_gemm_blocks (the
 // planner's splits stay within it too).  Only layers far beyond a GPU's
@@ -616,8 +625,8 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     char* dH2s = base + 2 * reg;
     char* dHs = base + 3 * reg;
 
-    // dW is overwritten by its product (or by the sum of its split-K
-    // partials); db, dW_down, dW_up, dM and the dw / dp vectors are
+    // dW, dW_down, dW_up and dM are overwritten by their products (or by
+    // the sums of their split-K partials); db and the dw / dp vectors are
     // accumulated atomically and start from zero.  T = 0 zeroes every
     // gradient; so does a one-application activation for the unused dM, dw2
     // and dp2 (when given).
@@ -626,6 +635,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     const WgradPlan wp = plan_wgrad(d);
     float* copies = copies_need(d) ? reinterpret_cast<float*>(base + 4 * reg + partial_need(d)) : nullptr;
     float* wpart = reinterpret_cast<float*>(base + (r > 0 ? 4 * reg + partial_need(d) + copies_need(d) : 0));
+    float* rpart = reinterpret_cast<float*>(reinterpret_cast<char*>(wpart) + wp.bytes);
 
     ZeroList z{};
     auto zero = [&](float* p, int64_t n) {
@@ -638,9 +648,11 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     if (T == 0) zero(dW, din * dout);
     zero(db, dout);
     if (r > 0) {
-        zero(dWd, din * R);
-        zero(dM, G * r * r);
-        zero(dWu, R * dog);
+        if (T == 0) {
+            zero(dWd, din * R);
+            zero(dWu, R * dog);
+        }
+        if (T == 0 || !two) zero(dM, G * r * r);
         if (copies && T > 0) {
             // the reduction of the copies overwrites dw1, dp1 (and dw2, dp2)
             zero(copies, (int64_t)4 * kChainCopies * R);
@@ -711,35 +723,13 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
 
     // Weight gradients, reduced over tokens (K = T), A and B both MN-major, in
     // one grouped launch: the rank-r gradients (dW_down, and dW_up, dM per
-    // group) add atomically and fill the CUs that dW leaves idle; a split dW
-    // stores partials that reduce_kernel then sums into dW.
+    // group) fill the CUs that dW leaves idle.  A split product stores its
+    // partials, and one reduction pass sums them, with the copies of the
+    // frequency / phase gradients.
     {
-        Batch bt;
-        bt.tile = gemm_tile<E>();
-        const Operand xT = operand1(seg(x, din, T), din);
-        const Operand dyN = operand1(seg(dy, dout, T), dout);
-        bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split,
-               wp.split > 1 ? wpart : nullptr);
-        if (r > 0) {
-            const int rs = wp.rank;
-            bt.add(xT, operand1(seg(dHs, R, T), R), (int)din, (int)R, nkT, dWd, R, true, nullptr, nullptr, rs);
-            for (int g = 0; g < G; ++g) {
-                const int64_t c0 = g * r;
-                const Operand C2T = operand1(seg(C2s + c0 * (int64_t)ES, R, T), r);
-                const Operand dyg = operand1(seg(static_cast<const E*>(dy) + g * dog, dout, T), dog);
-                bt.add(C2T, dyg, (int)r, (int)dog, nkT, dWu + c0 * dog, dog, true, nullptr, nullptr, rs);
-                if (two) {
-                    const Operand C1T = operand1(seg(C1s + c0 * (int64_t)ES, R, T), r);
-                    const Operand dH2N = operand1(seg(dH2s + c0 * (int64_t)ES, R, T), r);
-                    bt.add(C1T, dH2N, (int)r, (int)r, nkT, dM + g * r * r, r, true, nullptr, nullptr, rs);
-                }
-            }
-        }
-        NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
-        // One reduction pass: the split-K partials of dW, and the copies of
-        // the frequency / phase gradients.
         ReduceList red{};
         static_assert(kChainCopies <= kMaxReduceSlices, "copies exceed the reduction's slices");
+        static_assert(kMaxZero >= kMaxProblems + 4, "the reduction list holds every product and four copies");
         auto reduce = [&](const float* part, float* out, int64_t n, int S) {
             red.part[red.count] = part;
             red.out[red.count] = out;
@@ -747,7 +737,38 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             red.S[red.count] = S;
             ++red.count;
         };
+        Batch bt;
+        bt.tile = gemm_tile<E>();
+        const Operand xT = operand1(seg(x, din, T), din);
+        const Operand dyN = operand1(seg(dy, dout, T), dout);
+        bt.add(xT, dyN, (int)din, (int)dout, nkT, dW, dout, true, nullptr, db, wp.split,
+               wp.split > 1 ? wpart : nullptr);
         if (wp.split > 1) reduce(wpart, dW, din * dout, wp.split);
+        if (r > 0) {
+            const int rs = wp.rank;
+            float* rp = rs > 1 ? rpart : nullptr;
+            // one rank product: split pieces go to the next partial slots
+            auto rank = [&](const Operand& A, const Operand& B, int64_t m, int64_t n, float* out) {
+                bt.add(A, B, (int)m, (int)n, nkT, out, n, true, nullptr, nullptr, rs, rp);
+                if (rp) {
+                    reduce(rp, out, m * n, rs);
+                    rp += (int64_t)rs * m * n;
+                }
+            };
+            rank(xT, operand1(seg(dHs, R, T), R), din, R, dWd);
+            for (int g = 0; g < G; ++g) {
+                const int64_t c0 = g * r;
+                const Operand C2T = operand1(seg(C2s + c0 * (int64_t)ES, R, T), r);
+                const Operand dyg = operand1(seg(static_cast<const E*>(dy) + g * dog, dout, T), dog);
+                rank(C2T, dyg, r, dog, dWu + c0 * dog);
+                if (two) {
+                    const Operand C1T = operand1(seg(C1s + c0 * (int64_t)ES, R, T), r);
+                    const Operand dH2N = operand1(seg(dH2s + c0 * (int64_t)ES, R, T), r);
+                    rank(C1T, dH2N, r, r, dM + g * r * r);
+                }
+            }
+        }
+        NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
         if (copies) {
             const int64_t arr = (int64_t)kChainCopies * R;
             reduce(copies, dw1, R, kChainCopies);

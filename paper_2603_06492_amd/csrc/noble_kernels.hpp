@@ -41,7 +41,7 @@ __device__ __forceinline__ int64_t flat_block() { return (int64_t)blockIdx.y * g
 
 // ---------------------------------------------------------------- zero fill --
 
-constexpr int kMaxZero = 10;
+constexpr int kMaxZero = 16;
 struct ZeroList {
     float* ptr[kMaxZero];
     int64_t n[kMaxZero];

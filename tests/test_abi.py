@@ -105,19 +105,20 @@ def _wgrad_split(T, di, do, r, bk, tile=256, groups=1):
     """K pieces of dW in the weight-gradient launch.  r = 0: dW alone
     (_split_partials).  r > 0: dW and the rank products (dW_down, dW_up and
     dM, counted whatever the activation) together, minimising the makespan
-    plus the dW partial traffic at 5 MB/us and the rank atomics at 1 MB/us;
-    both splits from 2^a 3^b up to 16 with at least 8 K chunks per piece."""
+    plus the partial traffic of both at 5 MB/us ((2 S + 1) x the output
+    bytes of a split product); both splits from 2^a 3^b up to 16 with at
+    least 8 K chunks per piece.  Returns (dW split, rank split)."""
     nk = -(-T // bk) if T > 0 else 0
     if nk == 0:
-        return 1
+        return 1, 1
     cd = lambda a, b: -(-a // b)
     tiles = cd(di, tile) * cd(do, tile)
     if r == 0:
-        return _split_partials(tiles, nk, di * do)
+        return _split_partials(tiles, nk, di * do), 1
     G, R, dog = groups, groups * r, do // groups
     rank_tiles = cd(di, tile) * cd(R, tile) + G * (cd(r, tile) * cd(dog, tile) + cd(r, tile) * cd(r, tile))
     rank_bytes = 4.0 * (di * R + G * (r * dog + r * r))
-    best, pick = None, 1
+    best, pick = None, (1, 1)
     cands = (1, 2, 3, 4, 6, 8, 12, 16)
     for sw in cands:
         if sw > 1 and sw * 8 > nk:
@@ -126,18 +127,22 @@ def _wgrad_split(T, di, do, r, bk, tile=256, groups=1):
             if sr > 1 and sr * 8 > nk:
                 break
             t = (_makespan([(tiles * sw, cd(nk, sw)), (rank_tiles * sr, cd(nk, sr))])
-                 + ((2.0 * sw + 1) * di * do * 4 / 5.0e6 if sw > 1 else 0.0) + sr * rank_bytes / 1.0e6)
+                 + ((2.0 * sw + 1) * di * do * 4 / 5.0e6 if sw > 1 else 0.0)
+                 + ((2.0 * sr + 1) * rank_bytes / 5.0e6 if sr > 1 else 0.0))
             if best is None or t < best:
-                best, pick = t, sw
+                best, pick = t, (sw, sr)
     return pick
 
 
 def _wgrad_bytes(T, di, do, r, bk, tile=256, groups=1):
-    """dW partials: only dW stores partials (the rank gradients add
-    atomically).  Output tiles are 256 square on the bf16 path, 128 on the
-    float32 path."""
-    sp = _wgrad_split(T, di, do, r, bk, tile, groups)
-    return _align(sp * di * do * 4) if sp > 1 else 0
+    """Split-K partials of the weight gradients: dW's region, then one
+    region for the rank products (dW_down [d_in, G r], and per group dW_up
+    [r, d_out / G] and dM [r, r], counted whatever the activation).  Output
+    tiles are 256 square on the bf16 path, 128 on the float32 path."""
+    sw, sr = _wgrad_split(T, di, do, r, bk, tile, groups)
+    R, dog = groups * r, do // groups
+    rank = di * R + groups * (r * dog + r * r)
+    return (_align(sw * di * do * 4) if sw > 1 else 0) + (_align(sr * rank * 4) if r > 0 and sr > 1 else 0)
 
 
 def test_workspace_sizes():
@@ -147,8 +152,9 @@ def test_workspace_sizes():
     st, res, scr = _ws(8192, 2048, 2048, 128, noble.NOBLE_BF16)
     assert _proj_split(8192, 2048) == 4
     # square 2048 projection with a branch: dW in 3 pieces (192 workgroups),
-    # the rank problems in 3 pieces on the other 64 CUs of the same wave
-    wg = 3 * 2048 * 2048 * 4
+    # the rank problems in 3 pieces on the other 64 CUs of the same wave;
+    # both store float32 partials
+    wg = 3 * 2048 * 2048 * 4 + _align(3 * (2048 * 128 + 128 * 2048 + 128 * 128) * 4)
     assert _wgrad_bytes(8192, 2048, 2048, 128, 64) == wg
     assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + _copies(128) + wg
     st, res, scr = _ws(8192, 2048, 8192, 128, noble.NOBLE_BF16)
@@ -182,16 +188,17 @@ def test_workspace_sizes():
 
 
 @pytest.mark.parametrize("di,do,r,G,split", [
-    (2048, 6144, 128, 1, 1),   # QKV: 192 dW tiles, the rank problems fill the other 64 CUs
-    (2048, 2048, 128, 1, 3),   # square: 3 dW pieces and 3 rank pieces in one wave
-    (2048, 8192, 128, 1, 1),   # FFN up: one wave of dW, the rank problems split 6 ways after it
-    (8192, 2048, 128, 1, 1),   # FFN down
-    (2048, 6144, 128, 3, 1),   # grouped Q/K/V
-    (2048, 2048, 0, 1, 4),     # the plain square layer: dW alone, 4 pieces
+    (2048, 6144, 128, 1, (1, 1)),   # QKV: 192 dW tiles, the rank problems fill the other 64 CUs
+    (2048, 2048, 128, 1, (3, 3)),   # square: 3 dW pieces and 3 rank pieces in one wave
+    (2048, 8192, 128, 1, (1, 6)),   # FFN up: one wave of dW, the rank problems split 6 ways after it
+    (8192, 2048, 128, 1, (1, 6)),   # FFN down
+    (2048, 6144, 128, 3, (1, 1)),   # grouped Q/K/V
+    (2048, 2048, 0, 1, (4, 1)),     # the plain square layer: dW alone, 4 pieces
 ])
 def test_weight_gradient_plan_of_the_block(di, do, r, G, split):
-    """The dW split the library plans at T = 8192 (visible in the scratch
-    size) matches the independent one-at-a-time scheduler of _wgrad_split."""
+    """The dW and rank splits the library plans at T = 8192 (visible in the
+    scratch size, which holds both products' partials) match the independent
+    one-at-a-time scheduler of _wgrad_split."""
     T = 8192
     assert _wgrad_split(T, di, do, r, 64, 256, G) == split
     st, _, scr = _ws(T, di, do, r, noble.NOBLE_BF16, G)

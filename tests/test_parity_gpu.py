@@ -177,9 +177,10 @@ def test_degenerate_chain(which):
 
 
 def test_backward_repeatable():
-    """y, dx and dW are reproducible bit for bit: no float atomics in their
-    paths; a split dW sums its partials in a fixed order.  db, the rank
-    gradients and the frequency / phase gradients are summed with float
+    """y, dx, dW and the rank gradients dW_down, dM, dW_up are reproducible
+    bit for bit: no float atomics in their paths; a split product (here dW
+    and the rank products, both in two pieces) sums its partials in a fixed
+    order.  db and the frequency / phase gradients are summed with float
     atomics in a varying order: two runs must agree far inside the
     tolerance."""
     p = inp.draw_projection("rep", 1000, 512, 256, 64, "bf16", seed=12, bias_std=0.5)
@@ -189,7 +190,7 @@ def test_backward_repeatable():
     dp.fwd()
     dp.bwd()
     second = dp.outputs()
-    for k in ("y", "dx", "dW"):
+    for k in ("y", "dx", "dW", "dW_down", "dM", "dW_up"):
         assert np.array_equal(first[k], second[k]), k
     rep = parity_report(second, first)
     for k, e in rep.items():
