@@ -436,13 +436,16 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
     const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * R + col) * 2) : kOOB;
     auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * R * es); };
     const bool keep_h = a.H != nullptr;   // NULL: inference-only forward
+    // H is read again only by the backward, after every other projection's
+    // forward: it is stored non-temporal, so that it does not linger dirty in
+    // the memory-side cache.
     // Stores count in vmcnt: in the two-application form H is stored after
     // the barrier, whose wait for M would otherwise also wait for them.
     auto store_h = [&]() {
         if (keep_h)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), 0);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), kStoreNT);
     };
     if constexpr (!L2) store_h();
 #pragma unroll
