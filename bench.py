@@ -108,13 +108,7 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0, activ
     from paper_2603_06492_amd import inputs as inp
     from paper_2603_06492_amd import noble
     mixing = noble.two_layers(activation)
-    # the variants' two-application forms are compared with the mixing
-    # operand C1 rounded to bf16 as the kernels round it (a sign decision of
-    # LeakyReLU and GELU's conditioning depend on it)
-    mix = None
-    if mixing and activation != "cosnet":
-        mix = lambda a: inp.round_bf16(np.asarray(a, dtype=np.float32)).astype(np.float64)
-    kw = dict(activation=activation, mix_round=mix)
+    kw = dict(activation=activation)
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])

@@ -29,9 +29,13 @@
  *  - desc->dtype is the storage type of x, W, W_down, M, W_up, y, dy and dx.
  *    b, omega1, phi1, omega2, phi2 and every parameter gradient are float32.
  *    Arithmetic: bf16 operands with float32 accumulation on the bf16 path
- *    (cosine arguments, cos and sin in float32; C1, C2, dH and the mixing
- *    gradients are rounded to bf16 only where they feed a matrix product),
- *    float32 throughout on the f32 path.
+ *    (cosine arguments, cos and sin in float32).  Of the branch's
+ *    intermediates, C2 is rounded to bf16 where it feeds y and dW_up, and
+ *    dH where it feeds dx; the mixing products (C1 M, dH2 M^T) and the
+ *    gradient products dW_down = x^T dH and dM = C1^T dH2 take C1, dH2 and
+ *    dH as a pair of bf16 values whose sum carries about 16 significant
+ *    bits, so that those products are float32-accurate.  float32
+ *    throughout on the f32 path.
  *  - Shapes: 0 <= T <= 2^31 - 4096; 8 <= d_in, d_out <= 2^20, multiples of
  *    8; r = 0 (plain linear: every branch pointer is ignored and may be NULL)
  *    or 8 <= r <= 256 (bf16) / 128 (f32) with r a multiple of 8.  Each
@@ -126,13 +130,21 @@ noble_status noble_linear_workspace_size(const noble_linear_desc* desc,
                                          size_t* reserve_bytes,
                                          size_t* scratch_bytes);
 
+/* Scratch bytes the forward alone needs (at most the scratch_bytes of
+ * noble_linear_workspace_size, which covers both calls): a forward-only or
+ * inference caller may pass a buffer of this size to noble_linear_fwd.
+ * Same errors as noble_linear_workspace_size; makes no HIP call. */
+noble_status noble_linear_fwd_scratch_size(const noble_linear_desc* desc,
+                                           size_t* scratch_bytes);
+
 /* Forward, Eq. 1 with the CosNet of Eq. 2:
  *   y = x W + b + cos(omega2 (.) (cos(omega1 (.) (x W_down) + phi1) M) + phi2) W_up
  * Inputs : x [T, d_in], W [d_in, d_out], b [d_out] f32 (nullable = no bias),
  *          W_down [d_in, r], omega1/phi1/omega2/phi2 [r] f32, M [r, r],
  *          W_up [r, d_out].
  * Outputs: y [T, d_out]; reserve (>= reserve_bytes) receives H for the
- *          backward.  scratch must hold scratch_bytes.
+ *          backward.  scratch must hold the bytes noble_linear_fwd_scratch_size
+ *          gives (a buffer sized for both calls also serves).
  * reserve may be NULL: an inference-only forward that keeps no H (the
  * branch's permanent inference cost, Sec. 6); no backward can follow it.
  * With a one-application activation, M, omega2 and phi2 are not read and
@@ -245,7 +257,7 @@ const char* noble_status_string(int status);
 /* ABI version of this header (bumped on incompatible changes). */
 int noble_abi_version(void);
 
-#define NOBLE_ABI_VERSION 3
+#define NOBLE_ABI_VERSION 4
 
 #ifdef __cplusplus
 }

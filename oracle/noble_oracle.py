@@ -33,13 +33,6 @@ Everything is evaluated in float64 on whatever values it is handed; callers pass
 the exact values the device sees (bf16-rounded storage tensors upcast to
 float64).  There is no blocking, fusion or reordering beyond the equations.
 
-``mix_round`` (optional, default exact): an elementwise map applied to C1
-where it enters the mixing product, H2 = mix_round(C1) M, with its derivative
-taken as the identity (so dM = mix_round(C1)^T dH2 and dC1 = dH2 M^T).  With
-bf16 rounding this is the operand rounding of the bf16 mixed precision the
-paper trains in (§3.4); callers use it where a later decision (the sign that
-picks LeakyReLU's slope) must be taken from the same operand values a bf16
-implementation sees.
 """
 
 from __future__ import annotations
@@ -124,13 +117,12 @@ def activation_slope(f, a):
     raise ValueError(f"unknown activation {f!r}")
 
 
-def branch_forward(H, activation, omega1, phi1, M=None, omega2=None, phi2=None, mix_round=None):
+def branch_forward(H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
     """The bottleneck nonlinearity sigma applied to every row of ``H: [T, r]``.
 
     2-layer forms (Eq. (2) for cosine):  A1 = w1 (.) H + p1, C1 = f(A1),
     H2 = C1 M, A2 = w2 (.) H2 + p2, C2 = f(A2).  1-layer forms stop at
-    C2 = C1 = f(A1) and ignore M, w2, p2.  Returns the intermediates by name
-    (C1m: the mixing operand, C1 or mix_round(C1)).
+    C2 = C1 = f(A1) and ignore M, w2, p2.  Returns the intermediates by name.
     """
     f, layers = ACTIVATIONS[activation]
     H = _f64(H)
@@ -138,11 +130,10 @@ def branch_forward(H, activation, omega1, phi1, M=None, omega2=None, phi2=None, 
     C1 = activation_value(f, A1)                 # h1 = f(.)
     if layers == 1:
         return {"A1": A1, "C1": C1, "C2": C1}
-    C1m = C1 if mix_round is None else _f64(mix_round(C1))
-    H2 = C1m @ _f64(M)                           # h2 = h1 mixed by M (row form)
+    H2 = C1 @ _f64(M)                            # h2 = h1 mixed by M (row form)
     A2 = H2 * _f64(omega2) + _f64(phi2)          # w2 (.) h2 + p2
     C2 = activation_value(f, A2)                 # sigma(h) = f(.)
-    return {"A1": A1, "C1": C1, "C1m": C1m, "H2": H2, "A2": A2, "C2": C2}
+    return {"A1": A1, "C1": C1, "H2": H2, "A2": A2, "C2": C2}
 
 
 def cosnet_forward(H, omega1, phi1, M, omega2, phi2):
@@ -153,7 +144,7 @@ def cosnet_forward(H, omega1, phi1, M, omega2, phi2):
     return branch_forward(H, "cosnet", omega1, phi1, M, omega2, phi2)
 
 
-def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="cosnet", mix_round=None):
+def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="cosnet"):
     """Eq. (1) with sigma = the named bottleneck activation (CosNet by
     default).  Rows of ``x`` are independent tokens, so passing a subset of
     rows of ``x`` yields exactly those rows of ``Y``.
@@ -162,14 +153,14 @@ def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="co
     """
     x = _f64(x)
     H = x @ _f64(W_down)
-    C2 = branch_forward(H, activation, omega1, phi1, M, omega2, phi2, mix_round)["C2"]
+    C2 = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)["C2"]
     Y = x @ _f64(W) + C2 @ _f64(W_up)
     if b is not None:
         Y = Y + _f64(b)
     return Y, H
 
 
-def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=None, mix_round=None):
+def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
     """Chain rule through sigma for ``L`` with ``dL/dC2 = dC2`` (rows = tokens).
 
     Recomputes the forward chain from ``H``.  Returns dH, domega1, dphi1, the
@@ -179,14 +170,14 @@ def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=
     dC2 = _f64(dC2)
     H = _f64(H)
     w1 = _f64(omega1)
-    fw = branch_forward(H, activation, omega1, phi1, M, omega2, phi2, mix_round)
+    fw = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)
     out = {"dM": None, "domega2": None, "dphi2": None, "C2": fw["C2"]}
     if layers == 2:
         dA2 = activation_slope(f, fw["A2"]) * dC2    # C2 = f(A2)
         out["domega2"] = np.sum(dA2 * fw["H2"], axis=0)   # A2 = w2 (.) H2 + p2
         out["dphi2"] = np.sum(dA2, axis=0)
         dH2 = dA2 * _f64(omega2)
-        out["dM"] = fw["C1m"].T @ dH2                # H2 = C1m @ M
+        out["dM"] = fw["C1"].T @ dH2                 # H2 = C1 @ M
         dC1 = dH2 @ _f64(M).T
     else:
         dC1 = dC2                                    # C2 = C1
@@ -207,7 +198,7 @@ def cosnet_backward(dC2, H, omega1, phi1, M, omega2, phi2):
 
 
 def backward(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up,
-             dx_rows=None, dW_rows=None, activation="cosnet", mix_round=None):
+             dx_rows=None, dW_rows=None, activation="cosnet"):
     """Gradients of ``L = sum(dy * Y)`` with respect to every input of Eq. (1).
 
     Returns a dict with dx, dW, db, dW_down, dM, dW_up, domega1, dphi1,
@@ -223,7 +214,7 @@ def backward(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up,
     U = _f64(W_up)
     H = x @ D
     dC2 = dy @ U.T                               # Y = ... + C2 @ W_up
-    cb = branch_backward(dC2, H, activation, omega1, phi1, M, omega2, phi2, mix_round)
+    cb = branch_backward(dC2, H, activation, omega1, phi1, M, omega2, phi2)
     dH = cb["dH"]
     out = {
         "dW_up": cb["C2"].T @ dy,
@@ -280,7 +271,7 @@ def _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g):
 
 
 def forward_grouped(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, groups,
-                    activation="cosnet", mix_round=None):
+                    activation="cosnet"):
     """Eq. (1) for each of ``groups`` column blocks sharing x.  Returns
     ``(Y, H)`` with H = x W_down ([T, G r])."""
     W = _f64(W)
@@ -289,13 +280,13 @@ def forward_grouped(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, groups
     for g in range(G):
         cs, Dg, w1, p1, Mg, w2, p2, Ug = _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g)
         Y, _ = forward(x, W[:, cs], None if b is None else _f64(b)[cs], Dg, w1, p1, Mg, w2, p2, Ug,
-                       activation=activation, mix_round=mix_round)
+                       activation=activation)
         Ys.append(Y)
     return np.concatenate(Ys, axis=1), _f64(x) @ _f64(W_down)
 
 
 def backward_grouped(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, groups,
-                     dx_rows=None, dW_rows=None, activation="cosnet", mix_round=None):
+                     dx_rows=None, dW_rows=None, activation="cosnet"):
     """Gradients of L = sum(dy * Y) for the grouped layer: each block's
     backward on its columns of dy; dx, which every block reaches through x,
     is the sum of the blocks' dx, every other gradient is the blocks'
@@ -306,7 +297,7 @@ def backward_grouped(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, grou
     for g in range(G):
         cs, Dg, w1, p1, Mg, w2, p2, Ug = _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g)
         parts.append(backward(dy[:, cs], x, W[:, cs], Dg, w1, p1, Mg, w2, p2, Ug, dx_rows=dx_rows,
-                              dW_rows=dW_rows, activation=activation, mix_round=mix_round))
+                              dW_rows=dW_rows, activation=activation))
     cat = lambda k, ax: None if parts[0][k] is None else np.concatenate([q[k] for q in parts], axis=ax)
     out = {"dx": sum(q["dx"] for q in parts), "dW": cat("dW", 1), "db": cat("db", 0),
            "dW_down": cat("dW_down", 1), "dW_up": cat("dW_up", 0)}

@@ -103,14 +103,23 @@ int proj_split(int64_t T, int64_t K, int J) {
 }
 int proj_jobs(const noble_linear_desc* d) { return ngroups(d) * rank_blocks(d); }
 
-// Scratch layout, each part 256-byte aligned: four [T, R] storage-type
-// regions C1, C2, dH2, dH (the forward uses only C2); on the bf16 path the
-// float32 projection partials [S][T][R] for the larger split of the forward
-// and backward projections and the copies of the frequency / phase gradients
-// (backward); then the float32 split-K partials of the weight-gradient
-// products (backward only).
+// Scratch layout, each part 256-byte aligned.  The forward's part comes
+// first, so that a forward-only call needs just that prefix:
+//  - C2 [T, R] storage type;
+//  - bf16: the float32 projection partials [S][T][R] for the larger split of
+//    the forward and backward projections;
+// then the backward's:
+//  - C1, dH2, dH [T, hl R] storage type, hl = 2 on the bf16 path (each value
+//    as a high + low bf16 pair, see branch_bwd_kernel), 1 on the float32
+//    path;
+//  - bf16: the copies of the frequency / phase gradients;
+//  - the float32 split-K partials of the weight-gradient products.
+int hilo(const noble_linear_desc* d) { return d->dtype == NOBLE_BF16 ? 2 : 1; }
 size_t scratch_region(const noble_linear_desc* d) {
     return align_up((size_t)d->T * rank_total(d) * elt_size(d));
+}
+size_t scratch_region_w(const noble_linear_desc* d) {
+    return align_up((size_t)hilo(d) * d->T * rank_total(d) * elt_size(d));
 }
 size_t partial_need(const noble_linear_desc* d) {
     if (d->r == 0 || d->dtype != NOBLE_BF16) return 0;
@@ -125,8 +134,11 @@ size_t copies_need(const noble_linear_desc* d) {
     return align_up((size_t)4 * kChainCopies * rank_total(d) * 4);
 }
 size_t wgrad_need(const noble_linear_desc* d);
+size_t fwd_scratch_need(const noble_linear_desc* d) {
+    return d->r > 0 ? scratch_region(d) + partial_need(d) : 0;
+}
 size_t scratch_need(const noble_linear_desc* d) {
-    return (d->r > 0 ? 4 * scratch_region(d) + partial_need(d) + copies_need(d) : 0) + wgrad_need(d);
+    return (d->r > 0 ? fwd_scratch_need(d) + 3 * scratch_region_w(d) + copies_need(d) : 0) + wgrad_need(d);
 }
 size_t reserve_need(const noble_linear_desc* d) { return (size_t)d->T * rank_total(d) * 4; }
 
@@ -227,15 +239,16 @@ struct Batch {
     GemmBatch b{};
     int blocks = 0;
     int tile = 256;   // square output tile
-    // split > 1: pieces add atomically into C, or, when `partials` is given,
-    // each stores its float32 partial [M][ldc] at partials + piece * M * ldc.
+    // With `partials`, each of the `split` pieces stores its float32 partial
+    // [M][ldc] at partials + piece * M * ldc (also for split = 1); without,
+    // split > 1 pieces add atomically into C.
     void add(const Operand& A, const Operand& B, int M, int N, int nk, void* C, int64_t ldc, bool out_f32,
              const float* bias, float* bsum, int split, float* partials = nullptr) {
         GemmProblem& p = b.p[b.count++];
         p.A = A;
         p.B = B;
-        p.C = split > 1 && partials ? partials : C;
-        p.pstride = split > 1 && partials ? (int64_t)M * ldc : 0;
+        p.C = partials ? partials : C;
+        p.pstride = partials ? (int64_t)M * ldc : 0;
         p.ldc = ldc;
         p.bias = bias;
         p.bsum = bsum;
@@ -322,8 +335,26 @@ struct WgradPlan {
     int split;      // K pieces of dW
     int rank;       // K pieces of the rank products
     size_t bytes;        // dW partials
-    size_t rank_bytes;   // rank-product partials, [rank][d_in R], then per group [rank][r d_out/G], [rank][r r]
+    size_t rank_bytes;   // rank-product partials: [S][d_in][hl R] (dW_down), then per group
+                         // [S][r][d_out/G] (dW_up, only when split) and [S][hl r][hl r] (dM)
 };
+
+// Elements of one K piece of the rank products' float32 partials.  On the
+// bf16 path dW_down and dM are products over high + low bf16 operand pairs
+// (hl = 2): their partials are stored for any split, folded by the
+// reduction; dW_up is stored only when split.
+struct RankParts {
+    int64_t folded;     // dW_down and dM, per piece
+    int64_t unfolded;   // dW_up, per piece
+};
+RankParts rank_parts(const noble_linear_desc* d) {
+    const int64_t hl = hilo(d), G = ngroups(d), r = d->r, R = rank_total(d), dog = group_dout(d);
+    return RankParts{d->d_in * hl * R + G * hl * r * hl * r, G * r * dog};
+}
+// Pieces of partials stored for the folded and the unfolded rank products.
+int64_t rank_folded_pieces(const noble_linear_desc* d, int rank) {
+    return hilo(d) == 2 ? std::max(rank, 1) : (rank > 1 ? rank : 0);
+}
 
 WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
     WgradPlan w{1, 1, 0, 0};
@@ -338,20 +369,24 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
         w.split = choose_split_partials(tiles, nkT, MN, max_gemm_blocks(d));
     } else {
         constexpr double kPartialBytesPerUs = 5.0e6;
-        const int64_t R = rank_total(d), dog = group_dout(d);
+        const int64_t R = rank_total(d), dog = group_dout(d), hl = hilo(d);
         const int G = ngroups(d);
-        const int rank_tiles =
-            cdiv(din, tile) * cdiv(R, tile) + G * (cdiv(r, tile) * cdiv(dog, tile) + cdiv(r, tile) * cdiv(r, tile));
-        const double rank_bytes = 4.0 * (double)(din * R + G * (r * dog + r * r));
+        const int rank_tiles = cdiv(din, tile) * cdiv(hl * R, tile) +
+                               G * (cdiv(r, tile) * cdiv(dog, tile) + cdiv(hl * r, tile) * cdiv(hl * r, tile));
+        const RankParts rp = rank_parts(d);
         double best = -1.0;
         for (int sw : {1, 2, 3, 4, 6, 8, 12, 16}) {
             if (sw > 1 && sw * 8 > nkT) break;
             for (int sr : {1, 2, 3, 4, 6, 8, 12, 16}) {
                 if (sr > 1 && sr * 8 > nkT) break;
                 if ((int64_t)tiles * sw + (int64_t)rank_tiles * sr > max_gemm_blocks(d)) continue;
+                // partial traffic: S writes, S reads and one result write per stored product
+                const double fp = (double)rank_folded_pieces(d, sr), up = sr > 1 ? sr : 0;
+                const double rank_traffic = 4.0 * ((fp > 0 ? 2.0 * fp + 1 : 0) * rp.folded +
+                                                   (up > 0 ? 2.0 * up + 1 : 0) * rp.unfolded);
                 const double t = launch_makespan({{tiles * sw, cdiv(nkT, sw)}, {rank_tiles * sr, cdiv(nkT, sr)}}) +
                                  (sw > 1 ? (2.0 * sw + 1) * (double)MN * 4 / kPartialBytesPerUs : 0.0) +
-                                 (sr > 1 ? (2.0 * sr + 1) * rank_bytes / kPartialBytesPerUs : 0.0);
+                                 rank_traffic / kPartialBytesPerUs;
                 if (best < 0 || t < best) {
                     best = t;
                     w.split = sw;
@@ -361,9 +396,10 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
         }
     }
     w.bytes = w.split > 1 ? align_up((size_t)w.split * MN * 4) : 0;
-    if (r > 0 && w.rank > 1) {
-        const int64_t G = ngroups(d), rr = r, R = rank_total(d), dog = group_dout(d);
-        w.rank_bytes = align_up((size_t)w.rank * (size_t)(din * R + G * (rr * dog + rr * rr)) * 4);
+    if (r > 0) {
+        const RankParts rp = rank_parts(d);
+        const int64_t el = rank_folded_pieces(d, w.rank) * rp.folded + (w.rank > 1 ? w.rank * rp.unfolded : 0);
+        w.rank_bytes = el > 0 ? align_up((size_t)el * 4) : 0;
     }
     return w;
 }
@@ -406,7 +442,8 @@ noble_status check_grids(const noble_linear_desc* d) {
     const int64_t G = ngroups(d), dog = group_dout(d), R = rank_total(d);
     auto tiles = [tile](int64_t m, int64_t n) { return ((m + tile - 1) / tile) * ((n + tile - 1) / tile); };
     const int64_t fwd = G * tiles(T, dog), dx = tiles(T, din);
-    const int64_t wgrad = tiles(din, dout) + (r > 0 ? tiles(din, R) + G * (tiles(r, dog) + tiles(r, r)) : 0);
+    const int64_t hl = hilo(d);
+    const int64_t wgrad = tiles(din, dout) + (r > 0 ? tiles(din, hl * R) + G * (tiles(r, dog) + tiles(hl * r, hl * r)) : 0);
     return std::max({fwd, dx, wgrad}) <= max_gemm_blocks(d) ? NOBLE_OK : NOBLE_ERR_BAD_SHAPE;
 }
 
@@ -561,7 +598,7 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
     const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
     const int64_t R = rank_total(d), dog = group_dout(d);
     const int G = ngroups(d);
-    char* C2s = static_cast<char*>(scratch) + scratch_region(d);
+    char* C2s = static_cast<char*>(scratch);
     if (r > 0) {
         ChainArgs a{};
         a.M = static_cast<const char*>(M);
@@ -576,7 +613,7 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
         a.ldr = (int)R;
         a.nk = cdiv(din, BK);
         if constexpr (sizeof(E) == 2) {
-            float* P = reinterpret_cast<float*>(static_cast<char*>(scratch) + 4 * scratch_region(d));
+            float* P = reinterpret_cast<float*>(static_cast<char*>(scratch) + scratch_region(d));
             const int S = proj_split(T, din, proj_jobs(d));
             NOBLE_TRY(launch_proj(true, d, x, Wd, P, S, st));
             NOBLE_TRY(launch_branch(true, d, a, P, S, st));
@@ -618,12 +655,13 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     const int64_t R = rank_total(d), dog = group_dout(d);
     const int G = ngroups(d);
     const bool two = act_two_layers(d->activation);
-    const size_t reg = scratch_region(d);
+    const int64_t hl = hilo(d);   // C1, dH2, dH as high + low bf16 pairs on the bf16 path
+    const size_t regw = scratch_region_w(d);
     char* base = static_cast<char*>(scratch);
-    char* C1s = base;
-    char* C2s = base + reg;
-    char* dH2s = base + 2 * reg;
-    char* dHs = base + 3 * reg;
+    char* C2s = base;
+    char* C1s = base + fwd_scratch_need(d);
+    char* dH2s = C1s + regw;
+    char* dHs = dH2s + regw;
 
     // dW, dW_down, dW_up and dM are overwritten by their products (or by
     // the sums of their split-K partials); db and the dw / dp vectors are
@@ -633,8 +671,9 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     constexpr int GBK = gemm_bk<E>();
     const int nkT = cdiv(T, GBK);
     const WgradPlan wp = plan_wgrad(d);
-    float* copies = copies_need(d) ? reinterpret_cast<float*>(base + 4 * reg + partial_need(d)) : nullptr;
-    float* wpart = reinterpret_cast<float*>(base + (r > 0 ? 4 * reg + partial_need(d) + copies_need(d) : 0));
+    char* after_rank = r > 0 ? dHs + regw : base;
+    float* copies = copies_need(d) ? reinterpret_cast<float*>(after_rank) : nullptr;
+    float* wpart = reinterpret_cast<float*>(after_rank + copies_need(d));
     float* rpart = reinterpret_cast<float*>(reinterpret_cast<char*>(wpart) + wp.bytes);
 
     ZeroList z{};
@@ -695,7 +734,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         a.ldr = (int)R;
         a.nk = cdiv(dog, BK);
         if constexpr (sizeof(E) == 2) {
-            float* P = reinterpret_cast<float*>(base + 4 * reg);
+            float* P = reinterpret_cast<float*>(base + scratch_region(d));
             const int S = proj_split(T, dog, proj_jobs(d));
             NOBLE_TRY(launch_proj(false, d, dy, Wu, P, S, st, &z));
             NOBLE_TRY(launch_branch(false, d, a, P, S, st, copies));
@@ -710,13 +749,14 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         }
     }
 
-    // dx = [dy | dH] [W^T ; W_down^T]   (B(k, n) stored [n][k]: K-major)
+    // dx = [dy | dH] [W^T ; W_down^T]   (B(k, n) stored [n][k]: K-major); on
+    // the bf16 path the K-extension reads dH's high part (row stride 2 R)
     {
         const int nk1 = cdiv(dout, GBK);
         const int nk = nk1 + (r > 0 ? cdiv(R, GBK) : 0);
         Batch bt;
         bt.tile = gemm_tile<E>();
-        bt.add(operand2(seg(dy, dout, dout), seg(dHs, R, R), nk1, T), operand2(seg(W, dout, dout), seg(Wd, R, R), nk1, din),
+        bt.add(operand2(seg(dy, dout, dout), seg(dHs, hl * R, R), nk1, T), operand2(seg(W, dout, dout), seg(Wd, R, R), nk1, din),
                (int)T, (int)din, nk, dx, din, sizeof(E) == 4, nullptr, nullptr, 1);
         NOBLE_TRY((launch_gemm<E, true, true>(bt, st)));
     }
@@ -730,11 +770,13 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         ReduceList red{};
         static_assert(kChainCopies <= kMaxReduceSlices, "copies exceed the reduction's slices");
         static_assert(kMaxZero >= kMaxProblems + 4, "the reduction list holds every product and four copies");
-        auto reduce = [&](const float* part, float* out, int64_t n, int S) {
+        auto reduce = [&](const float* part, float* out, int64_t n, int S, int fw = 0, int fold = 0) {
             red.part[red.count] = part;
             red.out[red.count] = out;
             red.n[red.count] = n;
             red.S[red.count] = S;
+            red.fw[red.count] = fw;
+            red.fold[red.count] = fold;
             ++red.count;
         };
         Batch bt;
@@ -746,25 +788,33 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         if (wp.split > 1) reduce(wpart, dW, din * dout, wp.split);
         if (r > 0) {
             const int rs = wp.rank;
-            float* rp = rs > 1 ? rpart : nullptr;
-            // one rank product: split pieces go to the next partial slots
-            auto rank = [&](const Operand& A, const Operand& B, int64_t m, int64_t n, float* out) {
-                bt.add(A, B, (int)m, (int)n, nkT, out, n, true, nullptr, nullptr, rs, rp);
-                if (rp) {
-                    reduce(rp, out, m * n, rs);
+            float* rp = rpart;
+            // One rank product [m, n]: a split product stores its pieces in the
+            // next partial slots, as does (for any split) a product over high +
+            // low operand pairs, whose output [m, n] the reduction folds into
+            // `out` ([m / 2, n] or [m, n / 2] per the fold bits; F = its width).
+            auto rank = [&](const Operand& A, const Operand& B, int64_t m, int64_t n, float* out, int fold, int64_t F) {
+                const bool parts = fold != 0 || rs > 1;
+                bt.add(A, B, (int)m, (int)n, nkT, out, n, true, nullptr, nullptr, rs, parts ? rp : nullptr);
+                if (parts) {
+                    const int64_t outn = m * n / ((fold & 1 ? 2 : 1) * (fold & 2 ? 2 : 1));
+                    reduce(rp, out, outn, rs, fold ? (int)F : 0, fold);
                     rp += (int64_t)rs * m * n;
                 }
             };
-            rank(xT, operand1(seg(dHs, R, T), R), din, R, dWd);
+            // dW_down = x^T dH: on the bf16 path over [dH_hi | dH_lo] (N = 2 R)
+            rank(xT, operand1(seg(dHs, hl * R, T), hl * R), din, hl * R, dWd, hl == 2 ? 1 : 0, R);
             for (int g = 0; g < G; ++g) {
                 const int64_t c0 = g * r;
                 const Operand C2T = operand1(seg(C2s + c0 * (int64_t)ES, R, T), r);
                 const Operand dyg = operand1(seg(static_cast<const E*>(dy) + g * dog, dout, T), dog);
-                rank(C2T, dyg, r, dog, dWu + c0 * dog);
+                rank(C2T, dyg, r, dog, dWu + c0 * dog, 0, 0);
                 if (two) {
-                    const Operand C1T = operand1(seg(C1s + c0 * (int64_t)ES, R, T), r);
-                    const Operand dH2N = operand1(seg(dH2s + c0 * (int64_t)ES, R, T), r);
-                    rank(C1T, dH2N, r, r, dM + g * r * r);
+                    // dM_g = C1_g^T dH2_g: on the bf16 path over the group's
+                    // [hi | lo] column pairs of C1 and dH2 (2r x 2r, both folded)
+                    const Operand C1T = operand1(seg(C1s + hl * c0 * (int64_t)ES, hl * R, T), hl * r);
+                    const Operand dH2N = operand1(seg(dH2s + hl * c0 * (int64_t)ES, hl * R, T), hl * r);
+                    rank(C1T, dH2N, hl * r, hl * r, dM + g * r * r, hl == 2 ? 3 : 0, r);
                 }
             }
         }
@@ -819,6 +869,13 @@ noble_status noble_linear_workspace_size(const noble_linear_desc* desc, size_t* 
     return NOBLE_OK;
 }
 
+noble_status noble_linear_fwd_scratch_size(const noble_linear_desc* desc, size_t* scratch_bytes) {
+    NOBLE_TRY(check_desc(desc));
+    NOBLE_TRY(check_grids(desc));
+    if (scratch_bytes) *scratch_bytes = fwd_scratch_need(desc);
+    return NOBLE_OK;
+}
+
 noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, const void* W, const float* b,
                               const void* W_down, const float* omega1, const float* phi1, const void* M,
                               const float* omega2, const float* phi2, const void* W_up, void* y, void* reserve,
@@ -841,7 +898,7 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, cons
         NOBLE_TRY(need(W_up, true));
         NOBLE_TRY(optional(reserve));   // NULL: inference-only forward
         NOBLE_TRY(need(scratch, rows));
-        if (scratch_bytes < scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
+        if (scratch_bytes < fwd_scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
     }
     if (!rows) return NOBLE_OK;
     NOBLE_TRY(check_device());

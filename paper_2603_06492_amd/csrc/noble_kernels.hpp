@@ -62,12 +62,21 @@ __global__ __launch_bounds__(256) void zero_kernel(ZeroList z) {
 }
 
 // Split-K partial sums: out[i] = sum over p < S of part[p * n + i], for up to
-// kMaxZero float arrays.
+// kMaxZero float arrays.  A folded array sums, besides the slices, two or
+// four blocks of each slice: its partial products were computed over
+// operands split into high and low bf16 parts, laid side by side.  With
+// out = [rows][F] (F = fw[s]):
+//  - fold bit 0 (columns): a slice row holds 2F values, out[i][j] adds
+//    elements j and F + j of it;
+//  - fold bit 1 (rows): a slice holds 2 rows blocks, out[i][j] adds rows i
+//    and rows + i.
 struct ReduceList {
     const float* part[kMaxZero];
     float* out[kMaxZero];
     int64_t n[kMaxZero];
     int S[kMaxZero];
+    int fw[kMaxZero];          // folded arrays: the output row width F (a multiple of 4)
+    int fold[kMaxZero];        // 0, or the fold bits above
     int first[kMaxZero + 1];   // array s owns blocks first[s] .. first[s + 1] - 1
     int count;
 };
@@ -79,6 +88,8 @@ constexpr int kMaxReduceSlices = 16;
 // issued together (S is at most kMaxReduceSlices) and added in slice order:
 // a loop that waits on each slice in turn makes the few-element arrays
 // (the frequency / phase copies) a chain of dependent L2 round trips.
+// Folded arrays add, per slice, the fold blocks of the element in a fixed
+// order (high-high, high-low, low-high, low-low).
 __global__ __launch_bounds__(256) void reduce_kernel(ReduceList z) {
     int s = 0;
     while (s + 1 < z.count && (int)blockIdx.x >= z.first[s + 1]) ++s;
@@ -89,6 +100,32 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceList z) {
     const int64_t stride = (int64_t)(z.first[s + 1] - z.first[s]) * blockDim.x;
     const int64_t gid = (int64_t)(blockIdx.x - z.first[s]) * blockDim.x + threadIdx.x;
     const int64_t n4 = n >> 2;
+    const int fold = z.fold[s];
+    if (fold != 0) {
+        const int64_t F = z.fw[s], rows = n / F;
+        const int64_t pw = (fold & 1) ? 2 * F : F;                 // slice row width
+        const int64_t sstride = ((fold & 2) ? 2 * rows : rows) * pw;
+        const int64_t col_off = (fold & 1) ? F : 0, row_off = (fold & 2) ? rows * pw : 0;
+        for (int64_t i = gid; i < n4; i += stride) {
+            const int64_t e = 4 * i, row = e / F, col = e - row * F;
+            const float* q = p + row * pw + col;
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int sl = 0; sl < S; ++sl, q += sstride) {
+                f32x4 v[4];
+                v[0] = *reinterpret_cast<const f32x4*>(q);
+                v[1] = (fold & 1) ? *reinterpret_cast<const f32x4*>(q + col_off) : f32x4{0.f, 0.f, 0.f, 0.f};
+                v[2] = (fold & 2) ? *reinterpret_cast<const f32x4*>(q + row_off) : f32x4{0.f, 0.f, 0.f, 0.f};
+                v[3] = (fold == 3) ? *reinterpret_cast<const f32x4*>(q + row_off + col_off)
+                                   : f32x4{0.f, 0.f, 0.f, 0.f};
+                acc += v[0];
+                acc += v[1];
+                acc += v[2];
+                acc += v[3];
+            }
+            reinterpret_cast<f32x4*>(o)[i] = acc;
+        }
+        return;
+    }
     for (int64_t i = gid; i < n4; i += stride) {
         f32x4 v[kMaxReduceSlices];
 #pragma unroll

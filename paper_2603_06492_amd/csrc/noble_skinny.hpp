@@ -45,10 +45,38 @@ constexpr int kSkN = 128;       // rank columns of one M tile
 constexpr int kSkM = kSkN * kSkN * 2;     // one M tile, 128 x 128 bf16
 constexpr int kSkC = kSkRows * kSkN * 2;  // 32 x 128 bf16 of the C1 / dH2 operand tile
 constexpr int kSkMaxNT = 2;               // ranks up to 2 x 128 per group
-// LDS of a chain workgroup with NT x NT M tiles and a 32 x 128 NT operand tile
+// LDS of a chain workgroup with NT x NT M tiles and two 32 x 128 NT operand
+// tiles: the high and low bf16 parts of the mixing operand (C1 or dH2).
 template <int NT>
 constexpr int sk_lds() {
-    return NT * NT * kSkM + NT * kSkC;
+    return NT * NT * kSkM + 2 * NT * kSkC;
+}
+static_assert(sk_lds<kSkMaxNT>() <= 160 * 1024, "chain LDS exceeds a CU's 160 KB");
+
+// A float32 value as the sum of two bf16 values (round to nearest even
+// twice): hi carries the leading 8 significant bits, lo the next 8.  hi + lo
+// equals v to about 2^-17 relative, so an MFMA product over the pair is
+// float32-accurate where one bf16 operand would carry 2^-9.
+struct BfPair {
+    uint16_t hi, lo;
+};
+__device__ __forceinline__ BfPair bf_split(float v) {
+    const uint32_t hi = f2bf(v);
+    return BfPair{(uint16_t)hi, (uint16_t)f2bf(v - bf2f(hi))};
+}
+// Three parts: hi and mid as bf_split gives them (hi + mid is its pair), lo
+// the bf16 rounding of what remains.  hi + mid + lo equals v to about 2^-27
+// relative, below float32's own rounding, so a product over the three parts
+// is as accurate as a float32 product.  Each subtraction is exact in
+// float32 (the remainder has at most 16 significant bits).
+struct BfTriple {
+    uint16_t hi, mid, lo;
+};
+__device__ __forceinline__ BfTriple bf_split3(float v) {
+    const uint32_t hi = f2bf(v);
+    const float r1 = v - bf2f(hi);
+    const uint32_t mid = f2bf(r1);
+    return BfTriple{(uint16_t)hi, (uint16_t)mid, (uint16_t)f2bf(r1 - bf2f(mid))};
 }
 
 constexpr int kPjRows = 128;                 // tokens per projection workgroup
@@ -212,10 +240,13 @@ __device__ __forceinline__ int ctile_off(int row, int col) {
 }
 
 // acc (one 32x32 block per wave, columns 32 w .. of the 128 NT) over the K
-// steps of a [32 x 128 NT] tile in LDS (A, K-major) times M (TRANS_M = false:
+// steps of a [32 x 128 NT] operand held as two tiles in LDS (A, K-major: its
+// high bf16 part at `chi`, its low part at `clo`) times M (TRANS_M = false:
 // B(k, n) = M[k][n]) or M^T (B(k, n) = M[n][k]), M held as NT x NT tiles.
+// Each K step issues two MFMAs on the same M fragment, high part first.
 template <bool TRANS_M, int NT>
-__device__ __forceinline__ void mix_mma(const char* ctile, const char* mt, int wave, int lane, f32x16& acc) {
+__device__ __forceinline__ void mix_mma(const char* chi, const char* clo, const char* mt, int wave, int lane,
+                                        f32x16& acc) {
     const int r32 = lane & 31, h = lane >> 5;
     const int wl = wave & 3, nb = wave >> 2;   // 32-column block within tile column nb
     const uint32_t tb = tr_base(wl, lane);
@@ -227,7 +258,36 @@ __device__ __forceinline__ void mix_mma(const char* ctile, const char* mt, int w
         for (int s = 0; s < 8; ++s) {
             const int ql = 2 * s + h;     // 8-element K group of this lane within the tile
             const int q = 16 * kb + ql;   // ... within the whole rank
-            const u32x4 av = *reinterpret_cast<const u32x4*>(ctile + (q >> 3) * 4096 + r32 * 128 +
+            const uint32_t ao = (uint32_t)((q >> 3) * 4096 + r32 * 128 + ((((q & 7) ^ (r32 & 7) ^ (r32 >> 3))) << 4));
+            const u32x4 ah = *reinterpret_cast<const u32x4*>(chi + ao);
+            const u32x4 al = *reinterpret_cast<const u32x4*>(clo + ao);
+            u32x4 bv;
+            if constexpr (!TRANS_M)
+                bv = tr_read8(tile, tb, s);
+            else
+                bv = *reinterpret_cast<const u32x4*>(tile + p * 256 + ((ql ^ (4 * (p & 3))) << 4));
+            mma32<uint16_t>(acc, ah, bv);
+            mma32<uint16_t>(acc, al, bv);
+        }
+    }
+}
+
+// One more pass of the same product over a third operand tile `c` (the low
+// part of a three-part split), accumulated into acc.
+template <bool TRANS_M, int NT>
+__device__ __forceinline__ void mix_mma1(const char* c, const char* mt, int wave, int lane, f32x16& acc) {
+    const int r32 = lane & 31, h = lane >> 5;
+    const int wl = wave & 3, nb = wave >> 2;
+    const uint32_t tb = tr_base(wl, lane);
+    const int p = 32 * wl + r32;
+#pragma unroll
+    for (int kb = 0; kb < NT; ++kb) {
+        const char* tile = mt + (TRANS_M ? nb * NT + kb : kb * NT + nb) * kSkM;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            const int ql = 2 * s + h;
+            const int q = 16 * kb + ql;
+            const u32x4 av = *reinterpret_cast<const u32x4*>(c + (q >> 3) * 4096 + r32 * 128 +
                                                              ((((q & 7) ^ (r32 & 7) ^ (r32 >> 3))) << 4));
             u32x4 bv;
             if constexpr (!TRANS_M)
@@ -401,21 +461,32 @@ __device__ __forceinline__ bool chain_live(const BranchArgs& a) {
     return flat_block() < (int64_t)((a.T + kSkRows - 1) / kSkRows) * a.G;
 }
 
-// Buffer resource over the group's columns of a [T, R] array from token row0
-// (element size es): offsets (row * R + col) * es, col < r.
+// Buffer resource over a token-major array with row stride `ld` elements
+// (element size es), from token row0 and column c0: offsets (row * ld + col)
+// * es.  Rows past T fall past its end.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* base, int T, int row0, int64_t ld,
+                                                            int64_t c0, int es) {
+    return make_rsrc(reinterpret_cast<const char*>(base) + ((int64_t)row0 * ld + c0) * es,
+                     (int64_t)(T - row0) * ld * es);
+}
+// The group's columns of a [T, R] array.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t group_rsrc(const void* base, const BranchArgs& a, const ChainPos& q,
                                                              int es) {
-    return make_rsrc(reinterpret_cast<const char*>(base) + ((int64_t)q.row0 * a.R + q.c0) * es,
-                     (int64_t)(a.T - q.row0) * a.R * es);
+    return rows_rsrc(base, a.T, q.row0, a.R, q.c0, es);
 }
 
 // Forward chain.  L2: the two-application form with M (CosNet for F = Cos);
-// otherwise C2 = f(H w1 + p1) and M, w2, p2 are not read.
+// otherwise C2 = f(H w1 + p1) and M, w2, p2 are not read.  The mixing
+// operand C1 enters the MFMAs as three bf16 parts (bf_split3): the high and
+// middle parts from the two operand tiles, then the low part from the first
+// tile again, so H2 = C1 M is as accurate as a float32 product and A2 carries
+// float32 rounding only.
 template <Act F, bool L2, int NT>
 __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds[sk_lds<NT>()];
     char* mt = lds;
-    char* ct = mt + NT * NT * kSkM;
+    char* chi = mt + NT * NT * kSkM;
+    char* clo = chi + NT * kSkC;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
     if (!chain_live(a)) return;
@@ -448,12 +519,16 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), kStoreNT);
     };
     if constexpr (!L2) store_h();
+    uint16_t c1lo[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
         const float c1 = cv ? act_value<F, true>(acc[v] * w1 + p1) : 0.f;
         if constexpr (L2) {
             const int row = 8 * (v >> 2) + 4 * h + (v & 3);
-            *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = (uint16_t)f2bf(c1);
+            const BfTriple c = bf_split3(c1);
+            *reinterpret_cast<uint16_t*>(chi + ctile_off(row, col)) = c.hi;
+            *reinterpret_cast<uint16_t*>(clo + ctile_off(row, col)) = c.mid;
+            c1lo[v] = c.lo;
         } else {
             __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(c1), rc, vo2, soff(v, 2), 0);
         }
@@ -461,13 +536,19 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
     if constexpr (L2) {
         const float w2 = cv ? a.w2[q.c0 + col] : 0.f, p2 = cv ? a.p2[q.c0 + col] : 0.f;
         wait_vmcnt<0>();   // this wave's part of M has landed
-        __syncthreads();   // C1 tile and M complete
+        __syncthreads();   // C1 tiles and M complete
         store_h();
 
         f32x16 h2;
 #pragma unroll
         for (int v = 0; v < 16; ++v) h2[v] = 0.f;
-        mix_mma<false, NT>(ct, mt, wave, lane, h2);
+        mix_mma<false, NT>(chi, clo, mt, wave, lane, h2);
+        __syncthreads();   // every wave is done with the high part
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            *reinterpret_cast<uint16_t*>(chi + ctile_off(8 * (v >> 2) + 4 * h + (v & 3), col)) = c1lo[v];
+        __syncthreads();
+        mix_mma1<false, NT>(chi, mt, wave, lane, h2);
 #pragma unroll
         for (int v = 0; v < 16; ++v)
             __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(act_value<F, true>(h2[v] * w2 + p2)), rc, vo2,
@@ -477,11 +558,22 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
 
 // Backward chain, same forms as branch_fwd_kernel.  The one-application form
 // writes C2 and dH only (no C1, dH2 and no second frequency/phase).
+//
+// Scratch layouts (operands of the weight-gradient products, each a high +
+// low bf16 pair so that those products are float32-accurate):
+//  - C1 and dH2: [T][G][2 r], group g's high part in columns 2 g r .. 2 g r
+//    + r - 1 and its low part in the next r (row stride 2 R);
+//  - dH: [T][2 R], the high part of all groups in columns 0 .. R - 1, the
+//    low part in R .. 2 R - 1 (the dx product reads only the high part);
+//  - C2: [T][R], one bf16 value (the operand of y and dW_up).
+// Both mixing products (H2 = C1 M recomputed, dC1 = dH2 M^T) take their
+// operand as the same pair.
 template <Act F, bool L2, int NT>
 __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs a) {
     __shared__ __attribute__((aligned(1024))) char lds[sk_lds<NT>()];
     char* mt = lds;
-    char* ct = mt + NT * NT * kSkM;
+    char* chi = mt + NT * NT * kSkM;
+    char* clo = chi + NT * kSkC;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
     if (!chain_live(a)) return;
@@ -507,10 +599,14 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     const int gc = q.c0 + col;   // column of the [R] vectors
     const int64_t rows_left = a.T - q.row0;
     const __amdgpu_buffer_rsrc_t rh = group_rsrc(a.H, a, q, 4);
-    const __amdgpu_buffer_rsrc_t rc2 = group_rsrc(a.C2s, a, q, 2), rdh = group_rsrc(a.dHs, a, q, 2);
+    const __amdgpu_buffer_rsrc_t rc2 = group_rsrc(a.C2s, a, q, 2);
+    // dH [T][2R]: high part at column gc, low part at R + gc
+    const __amdgpu_buffer_rsrc_t rdh = rows_rsrc(a.dHs, a.T, q.row0, 2 * (int64_t)R, q.c0, 2);
     const uint32_t vo4 = cv ? (uint32_t)(((4 * h) * R + col) * 4) : kOOB;
     const uint32_t vo2 = cv ? (uint32_t)(((4 * h) * R + col) * 2) : kOOB;
+    const uint32_t vw2 = cv ? (uint32_t)(((4 * h) * 2 * R + col) * 2) : kOOB;   // row stride 2R
     auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * R * es); };
+    auto soffw = [&](int v) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * 2 * R * 2); };
 
     // H from the reserve (rows past T and columns past r read as zero),
     // issued before the partial sums so that both arrive in one round trip
@@ -536,29 +632,45 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
         }
     } else {
         const float w2 = cv ? a.w2[gc] : 0.f, p2 = cv ? a.p2[gc] : 0.f;
-        const __amdgpu_buffer_rsrc_t rc1 = group_rsrc(a.C1s, a, q, 2), rdh2 = group_rsrc(a.dH2s, a, q, 2);
-        uint16_t c1[16];
+        // C1 and dH2 [T][G][2r]: the group's pair starts at column 2 c0
+        const __amdgpu_buffer_rsrc_t rc1 = rows_rsrc(a.C1s, a.T, q.row0, 2 * (int64_t)R, 2 * (int64_t)q.c0, 2);
+        const __amdgpu_buffer_rsrc_t rdh2 = rows_rsrc(a.dH2s, a.T, q.row0, 2 * (int64_t)R, 2 * (int64_t)q.c0, 2);
+        const uint32_t lo_off = (uint32_t)r * 2;   // bytes from the high part to the low part
+        // C1 in three parts for the recomputed H2 (as in the forward, so that
+        // A2 is the forward's); its high and middle parts are the pair
+        // stored for dM
+        BfTriple c1[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int row = 8 * (v >> 2) + 4 * h + (v & 3);
             float f = 0.f, d = 0.f;
             if (cv) act_value_slope<F, true>(hr[v] * w1 + p1, f, d);
             d1[v] = d;
-            c1[v] = (uint16_t)f2bf(f);
-            *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = c1[v];
+            c1[v] = bf_split3(f);
+            *reinterpret_cast<uint16_t*>(chi + ctile_off(row, col)) = c1[v].hi;
+            *reinterpret_cast<uint16_t*>(clo + ctile_off(row, col)) = c1[v].mid;
         }
         wait_vmcnt<0>();   // this wave's part of M has landed
-        __syncthreads();   // C1 tile and M complete
+        __syncthreads();   // C1 tiles and M complete
         // C1 to scratch after the barrier: stores count in vmcnt, and the
         // wait above is for M only
 #pragma unroll
-        for (int v = 0; v < 16; ++v) __builtin_amdgcn_raw_buffer_store_b16(c1[v], rc1, vo2, soff(v, 2), 0);
+        for (int v = 0; v < 16; ++v) {
+            __builtin_amdgcn_raw_buffer_store_b16(c1[v].hi, rc1, vw2, soffw(v), 0);
+            __builtin_amdgcn_raw_buffer_store_b16(c1[v].mid, rc1, vw2 + lo_off, soffw(v), 0);
+        }
 
         f32x16 h2;
 #pragma unroll
         for (int v = 0; v < 16; ++v) h2[v] = 0.f;
-        mix_mma<false, NT>(ct, mt, wave, lane, h2);   // H2 = C1 M
-        __syncthreads();                               // done reading C1 from LDS
+        mix_mma<false, NT>(chi, clo, mt, wave, lane, h2);   // H2 = C1 M: high and middle parts
+        __syncthreads();                                     // every wave is done with the high part
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+            *reinterpret_cast<uint16_t*>(chi + ctile_off(8 * (v >> 2) + 4 * h + (v & 3), col)) = c1[v].lo;
+        __syncthreads();
+        mix_mma1<false, NT>(chi, mt, wave, lane, h2);       // ... and the low part
+        __syncthreads();                                     // done reading C1 from LDS
 
         // A2 = H2 w2 + p2, C2 = f(A2), dA2 = f'(A2) dC2, dH2 = dA2 w2
         float da2h2[16], da2[16];
@@ -572,9 +684,11 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
             const float g = ok ? d * dc2[v] : 0.f;
             da2[v] = g;
             da2h2[v] = g * h2[v];
-            const uint16_t dh2 = (uint16_t)f2bf(g * w2);
-            *reinterpret_cast<uint16_t*>(ct + ctile_off(row, col)) = dh2;
-            __builtin_amdgcn_raw_buffer_store_b16(dh2, rdh2, vo2, soff(v, 2), 0);
+            const BfPair dh2 = bf_split(g * w2);
+            *reinterpret_cast<uint16_t*>(chi + ctile_off(row, col)) = dh2.hi;
+            *reinterpret_cast<uint16_t*>(clo + ctile_off(row, col)) = dh2.lo;
+            __builtin_amdgcn_raw_buffer_store_b16(dh2.hi, rdh2, vw2, soffw(v), 0);
+            __builtin_amdgcn_raw_buffer_store_b16(dh2.lo, rdh2, vw2 + lo_off, soffw(v), 0);
         }
         {
             const float sw = block_colsum(da2h2), sp = block_colsum(da2);
@@ -583,15 +697,16 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
                 unsafeAtomicAdd(gp2 + gc, sp);
             }
         }
-        __syncthreads();   // dH2 tile complete
+        __syncthreads();   // dH2 tiles complete
 
 #pragma unroll
         for (int v = 0; v < 16; ++v) dc1[v] = 0.f;
-        mix_mma<true, NT>(ct, mt, wave, lane, dc1);   // dC1 = dH2 M^T
+        mix_mma<true, NT>(chi, clo, mt, wave, lane, dc1);   // dC1 = dH2 M^T
     }
 
     // dA1 = f'(A1) dC1; dw1 += dA1 H, dp1 += dA1; dH = dA1 w1
     float da1h[16], da1[16];
+    const uint32_t dh_lo = (uint32_t)R * 2;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
         const int row = 8 * (v >> 2) + 4 * h + (v & 3);
@@ -599,7 +714,9 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
         const float g = ok ? d1[v] * dc1[v] : 0.f;
         da1[v] = g;
         da1h[v] = g * hr[v];
-        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(g * w1), rdh, vo2, soff(v, 2), 0);
+        const BfPair dh = bf_split(g * w1);
+        __builtin_amdgcn_raw_buffer_store_b16(dh.hi, rdh, vw2, soffw(v), 0);
+        __builtin_amdgcn_raw_buffer_store_b16(dh.lo, rdh, vw2 + dh_lo, soffw(v), 0);
     }
     const float sw = block_colsum(da1h), sp = block_colsum(da1);
     if (h == 0 && cv) {

@@ -6,6 +6,7 @@ and turns status codes into exceptions.  There is no fallback: if the library
 is not built, or the device is not gfx950, calls raise.
 
 Functions keep the C names: ``noble_linear_workspace_size``,
+``noble_linear_fwd_scratch_size``,
 ``noble_linear_fwd``, ``noble_linear_bwd``, ``noble_status_string``, and the
 training-recipe calls ``noble_recipe_defaults``, ``noble_lr_multipliers``,
 ``noble_init_params`` (plus ``param_groups``, which only arranges the
@@ -28,7 +29,7 @@ LIB_PATH = os.path.join(PKG_DIR, "libnoble.so")
 NOBLE_BF16 = 0
 NOBLE_F32 = 1
 # NOBLE_ABI_VERSION of include/noble.h that the structures below mirror
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 STATUS = {
     0: "NOBLE_OK",
@@ -122,6 +123,9 @@ def lib() -> ctypes.CDLL:
         L.noble_linear_workspace_size.argtypes = [ctypes.POINTER(noble_linear_desc),
                                                   ctypes.POINTER(ctypes.c_size_t),
                                                   ctypes.POINTER(ctypes.c_size_t)]
+        L.noble_linear_fwd_scratch_size.restype = ctypes.c_int
+        L.noble_linear_fwd_scratch_size.argtypes = [ctypes.POINTER(noble_linear_desc),
+                                                    ctypes.POINTER(ctypes.c_size_t)]
         L.noble_linear_fwd.restype = ctypes.c_int
         L.noble_linear_fwd.argtypes = [ctypes.POINTER(noble_linear_desc)] + [_vp] * 13 + [ctypes.c_size_t, _vp]
         L.noble_linear_bwd.restype = ctypes.c_int
@@ -145,6 +149,17 @@ def noble_status_string(status: int) -> str:
 def make_desc(T: int, d_in: int, d_out: int, r: int, dtype: int, activation=0, groups: int = 1) -> noble_linear_desc:
     return noble_linear_desc(int(T), int(d_in), int(d_out), int(r), int(dtype), activation_code(activation),
                              int(groups), 0)
+
+
+def noble_linear_fwd_scratch_size(T: int, d_in: int, d_out: int, r: int, dtype: int,
+                                  activation=0, groups: int = 1) -> int:
+    """Scratch bytes of the forward alone (r: rank per group)."""
+    d = make_desc(T, d_in, d_out, r, dtype, activation, groups)
+    scr = ctypes.c_size_t(0)
+    st = lib().noble_linear_fwd_scratch_size(ctypes.byref(d), ctypes.byref(scr))
+    if st != 0:
+        raise NobleError(st, "noble_linear_fwd_scratch_size")
+    return scr.value
 
 
 def noble_linear_workspace_size(T: int, d_in: int, d_out: int, r: int, dtype: int,
@@ -376,10 +391,13 @@ def param_groups(params: dict, lr: float, d_in: int, d_out: int, r: int,
 
 # ------------------------------------------------------------ conveniences --
 
-def alloc_workspace(T, d_in, d_out, r, dtype_code, device="cuda", groups: int = 1):
-    """(reserve, scratch) uint8 tensors of the required sizes."""
+def alloc_workspace(T, d_in, d_out, r, dtype_code, device="cuda", groups: int = 1, forward_only=False):
+    """(reserve, scratch) uint8 tensors of the required sizes; with
+    ``forward_only`` the scratch covers the forward alone."""
     torch = _torch()
     res, scr = noble_linear_workspace_size(T, d_in, d_out, r, dtype_code, groups=groups)
+    if forward_only:
+        scr = noble_linear_fwd_scratch_size(T, d_in, d_out, r, dtype_code, groups=groups)
     return (torch.empty(max(res, 16), dtype=torch.uint8, device=device),
             torch.empty(max(scr, 16), dtype=torch.uint8, device=device))
 
@@ -401,7 +419,7 @@ def _make_function():
             r = R // groups
             dt = _dtype_code(x)
             act = activation_code(activation)
-            reserve, scratch = alloc_workspace(T, d_in, d_out, r, dt, x.device, groups=groups)
+            reserve, scratch = alloc_workspace(T, d_in, d_out, r, dt, x.device, groups=groups, forward_only=True)
             y = torch.empty((T, d_out), dtype=x.dtype, device=x.device)
             noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
                              activation=act, groups=groups)
@@ -494,7 +512,7 @@ def _make_module():
             # is neither written nor kept.
             T = x2.shape[0]
             _, scratch = alloc_workspace(T, self.d_in, self.d_out, self.r, _dtype_code(x2), x2.device,
-                                         groups=self.groups)
+                                         groups=self.groups, forward_only=True)
             y = torch.empty((T, self.d_out), dtype=x2.dtype, device=x2.device)
             noble_linear_fwd(x2, self.W, self.b, *self._branch(), y, None, scratch,
                              activation=activation_code(self.activation), groups=self.groups)

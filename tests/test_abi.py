@@ -30,13 +30,14 @@ def _declared_functions():
 
 def test_library_exports_every_declared_function():
     names = _declared_functions()
-    assert set(names) == {"noble_linear_workspace_size", "noble_linear_fwd", "noble_linear_bwd",
+    assert set(names) == {"noble_linear_workspace_size", "noble_linear_fwd_scratch_size", "noble_linear_fwd",
+                          "noble_linear_bwd",
                           "noble_status_string", "noble_abi_version", "noble_recipe_defaults",
                           "noble_lr_multipliers", "noble_init_params"}
     L = noble.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.noble_abi_version() == 3 == noble.ABI_VERSION
+    assert L.noble_abi_version() == 4 == noble.ABI_VERSION
 
 
 def test_status_strings():
@@ -101,13 +102,23 @@ def _makespan(groups):
     return end
 
 
-def _wgrad_split(T, di, do, r, bk, tile=256, groups=1):
+def _rank_parts(di, do, r, groups, hl):
+    """Float32 elements of one K piece of the rank products' partials:
+    (folded, unfolded).  On the bf16 path (hl = 2) dW_down = x^T [dH_hi |
+    dH_lo] ([d_in, 2 R]) and dM_g = [C1_hi | C1_lo]_g^T [dH2_hi | dH2_lo]_g
+    ([2 r, 2 r]) are stored for any split and folded by the reduction; dW_up
+    [r, d_out / G] per group is stored only when split."""
+    R, dog = groups * r, do // groups
+    return di * hl * R + groups * (hl * r) ** 2, groups * r * dog
+
+
+def _wgrad_split(T, di, do, r, bk, tile=256, groups=1, hl=2):
     """K pieces of dW in the weight-gradient launch.  r = 0: dW alone
     (_split_partials).  r > 0: dW and the rank products (dW_down, dW_up and
     dM, counted whatever the activation) together, minimising the makespan
-    plus the partial traffic of both at 5 MB/us ((2 S + 1) x the output
-    bytes of a split product); both splits from 2^a 3^b up to 16 with at
-    least 8 K chunks per piece.  Returns (dW split, rank split)."""
+    plus the partial traffic at 5 MB/us ((2 S + 1) x the output bytes of
+    each stored product, S its pieces); both splits from 2^a 3^b up to 16
+    with at least 8 K chunks per piece.  Returns (dW split, rank split)."""
     nk = -(-T // bk) if T > 0 else 0
     if nk == 0:
         return 1, 1
@@ -116,8 +127,8 @@ def _wgrad_split(T, di, do, r, bk, tile=256, groups=1):
     if r == 0:
         return _split_partials(tiles, nk, di * do), 1
     G, R, dog = groups, groups * r, do // groups
-    rank_tiles = cd(di, tile) * cd(R, tile) + G * (cd(r, tile) * cd(dog, tile) + cd(r, tile) * cd(r, tile))
-    rank_bytes = 4.0 * (di * R + G * (r * dog + r * r))
+    rank_tiles = cd(di, tile) * cd(hl * R, tile) + G * (cd(r, tile) * cd(dog, tile) + cd(hl * r, tile) ** 2)
+    folded, unfolded = _rank_parts(di, do, r, groups, hl)
     best, pick = None, (1, 1)
     cands = (1, 2, 3, 4, 6, 8, 12, 16)
     for sw in cands:
@@ -126,51 +137,69 @@ def _wgrad_split(T, di, do, r, bk, tile=256, groups=1):
         for sr in cands:
             if sr > 1 and sr * 8 > nk:
                 break
+            fp = (max(sr, 1) if hl == 2 else (sr if sr > 1 else 0))
+            up = sr if sr > 1 else 0
+            traffic = 4.0 * (((2.0 * fp + 1) * folded if fp else 0.0) + ((2.0 * up + 1) * unfolded if up else 0.0))
             t = (_makespan([(tiles * sw, cd(nk, sw)), (rank_tiles * sr, cd(nk, sr))])
                  + ((2.0 * sw + 1) * di * do * 4 / 5.0e6 if sw > 1 else 0.0)
-                 + ((2.0 * sr + 1) * rank_bytes / 5.0e6 if sr > 1 else 0.0))
+                 + traffic / 5.0e6)
             if best is None or t < best:
                 best, pick = t, (sw, sr)
     return pick
 
 
-def _wgrad_bytes(T, di, do, r, bk, tile=256, groups=1):
+def _wgrad_bytes(T, di, do, r, bk, tile=256, groups=1, hl=2):
     """Split-K partials of the weight gradients: dW's region, then one
-    region for the rank products (dW_down [d_in, G r], and per group dW_up
-    [r, d_out / G] and dM [r, r], counted whatever the activation).  Output
-    tiles are 256 square on the bf16 path, 128 on the float32 path."""
-    sw, sr = _wgrad_split(T, di, do, r, bk, tile, groups)
-    R, dog = groups * r, do // groups
-    rank = di * R + groups * (r * dog + r * r)
-    return (_align(sw * di * do * 4) if sw > 1 else 0) + (_align(sr * rank * 4) if r > 0 and sr > 1 else 0)
+    region for the rank products (see _rank_parts).  Output tiles are 256
+    square on the bf16 path (hl = 2), 128 on the float32 path (hl = 1)."""
+    sw, sr = _wgrad_split(T, di, do, r, bk, tile, groups, hl)
+    folded, unfolded = _rank_parts(di, do, r, groups, hl)
+    fp = max(sr, 1) if hl == 2 else (sr if sr > 1 else 0)
+    rank = fp * folded + (sr * unfolded if sr > 1 else 0)
+    return (_align(sw * di * do * 4) if sw > 1 else 0) + (_align(rank * 4) if r > 0 and T > 0 and rank else 0)
+
+
+def _branch_scratch(T, di, do, r, G=1, bf16=True):
+    """Rank-side scratch: C2 [T, R], the bf16 projection partials, then C1,
+    dH2, dH [T, hl R] and the bf16 copies of the frequency / phase
+    gradients."""
+    R, es, hl = G * r, (2 if bf16 else 4), (2 if bf16 else 1)
+    if r == 0:
+        return 0
+    part = 0
+    if bf16:
+        J = G * -(-r // 128)
+        S = max(_proj_split(T, di, J), _proj_split(T, do // G, J))
+        part = _align(S * T * R * 4)
+    return _align(T * R * es) + part + 3 * _align(hl * T * R * es) + (_copies(R) if bf16 else 0)
 
 
 def test_workspace_sizes():
-    # four storage-type [T, r] regions, then (bf16) the float32 projection
-    # partials of the larger of the forward and backward splits, then the
-    # float32 split-K partials of the weight-gradient products
+    # forward part first (C2, the bf16 projection partials), then C1, dH2 and
+    # dH as high + low bf16 pairs, the copies, and the float32 partials of the
+    # weight-gradient products
     st, res, scr = _ws(8192, 2048, 2048, 128, noble.NOBLE_BF16)
     assert _proj_split(8192, 2048) == 4
-    # square 2048 projection with a branch: dW in 3 pieces (192 workgroups),
-    # the rank problems in 3 pieces on the other 64 CUs of the same wave;
-    # both store float32 partials
-    wg = 3 * 2048 * 2048 * 4 + _align(3 * (2048 * 128 + 128 * 2048 + 128 * 128) * 4)
-    assert _wgrad_bytes(8192, 2048, 2048, 128, 64) == wg
-    assert st == OK and res == 4 * 8192 * 128 and scr == 4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + _copies(128) + wg
+    assert st == OK and res == 4 * 8192 * 128
+    assert scr == (8192 * 128 * 2 + 4 * 8192 * 128 * 4 + 3 * 2 * 8192 * 128 * 2 + _copies(128)
+                   + _wgrad_bytes(8192, 2048, 2048, 128, 64))
     st, res, scr = _ws(8192, 2048, 8192, 128, noble.NOBLE_BF16)
-    assert st == OK and scr == (4 * 8192 * 128 * 2 + 4 * 8192 * 128 * 4 + _copies(128)
-                                + _wgrad_bytes(8192, 2048, 8192, 128, 64))
+    assert st == OK and scr == _branch_scratch(8192, 2048, 8192, 128) + _wgrad_bytes(8192, 2048, 8192, 128, 64)
     st, res, scr = _ws(300, 64, 1024, 40, noble.NOBLE_BF16)
     S = max(_proj_split(300, 64), _proj_split(300, 1024))
-    assert _wgrad_bytes(300, 64, 1024, 40, 64) == 0   # 5 K chunks: no split
-    assert S == 4 and st == OK and scr == 4 * _align(300 * 40 * 2) + _align(S * 300 * 40 * 4) + _copies(40)
+    # 5 K chunks: no split, but dW_down and dM store their high + low products
+    assert _wgrad_split(300, 64, 1024, 40, 64) == (1, 1)
+    assert _wgrad_bytes(300, 64, 1024, 40, 64) == _align((64 * 80 + 80 * 80) * 4)
+    assert S == 4 and st == OK
+    assert scr == (_align(300 * 40 * 2) + _align(S * 300 * 40 * 4) + 3 * _align(2 * 300 * 40 * 2) + _copies(40)
+                   + _align((64 * 80 + 80 * 80) * 4))
     st, res, scr = _ws(256, 64, 64, 8, noble.NOBLE_F32)
     assert st == OK and res == 4 * 256 * 8 and scr == 4 * 256 * 8 * 4
     # float32 tiles are 128 square: 64 tiles of 1024 x 1024 split dW in 4
     # (with 256 tiles it would be 16)
     st, res, scr = _ws(8192, 1024, 1024, 0, noble.NOBLE_F32)
-    assert _wgrad_bytes(8192, 1024, 1024, 0, 32, tile=256) == 16 * 1024 * 1024 * 4
-    assert st == OK and scr == _wgrad_bytes(8192, 1024, 1024, 0, 32, tile=128) == 4 * 1024 * 1024 * 4
+    assert _wgrad_bytes(8192, 1024, 1024, 0, 32, tile=256, hl=1) == 16 * 1024 * 1024 * 4
+    assert st == OK and scr == _wgrad_bytes(8192, 1024, 1024, 0, 32, tile=128, hl=1) == 4 * 1024 * 1024 * 4
     st, res, scr = _ws(1000, 64, 64, 0, noble.NOBLE_BF16)
     assert st == OK and res == 0 and scr == _wgrad_bytes(1000, 64, 64, 0, 64) == 2 * 64 * 64 * 4
     st, res, scr = _ws(200, 64, 64, 0, noble.NOBLE_BF16)
@@ -182,9 +211,34 @@ def test_workspace_sizes():
     assert st == OK and res == 0
     # each region of the scratch is 256-byte aligned
     st, res, scr = _ws(3, 64, 64, 8, noble.NOBLE_BF16)
-    assert st == OK and scr == 4 * 256 + 256 + _copies(8)
+    assert st == OK and scr == 256 + 256 + 3 * 256 + _copies(8) + _align((64 * 16 + 16 * 16) * 4)
     assert noble.lib().noble_linear_workspace_size(None, None, None) == NULL
 
+
+def _fws(T, di, do, r, dt, groups=1):
+    d = noble.make_desc(T, di, do, r, dt, 0, groups)
+    b = ctypes.c_size_t(0)
+    st = noble.lib().noble_linear_fwd_scratch_size(ctypes.byref(d), ctypes.byref(b))
+    return st, b.value
+
+
+def test_forward_scratch_is_the_prefix():
+    """The forward needs only C2 and (bf16) the projection partials: the
+    prefix of the full scratch, tens of MB less at the block's shapes."""
+    for (T, di, do, r, G, dt) in ((8192, 2048, 2048, 128, 1, noble.NOBLE_BF16),
+                                  (8192, 2048, 6144, 128, 3, noble.NOBLE_BF16),
+                                  (256, 64, 64, 8, 1, noble.NOBLE_F32), (300, 64, 1024, 40, 1, noble.NOBLE_BF16)):
+        st, f = _fws(T, di, do, r, dt, G)
+        st2, _, full = _ws(T, di, do, r, dt, G)
+        R, bf = G * r, dt == noble.NOBLE_BF16
+        part = 0
+        if bf:
+            J = G * -(-r // 128)
+            part = _align(max(_proj_split(T, di, J), _proj_split(T, do // G, J)) * T * R * 4)
+        assert st == st2 == OK and f == _align(T * R * (2 if bf else 4)) + part and f < full
+    assert _fws(8192, 2048, 2048, 0, noble.NOBLE_BF16) == (OK, 0)
+    assert _fws(16, 12, 64, 8, noble.NOBLE_BF16)[0] == SHAPE
+    assert noble.lib().noble_linear_fwd_scratch_size(None, None) == NULL
 
 
 @pytest.mark.parametrize("di,do,r,G,split", [
@@ -202,13 +256,8 @@ def test_weight_gradient_plan_of_the_block(di, do, r, G, split):
     T = 8192
     assert _wgrad_split(T, di, do, r, 64, 256, G) == split
     st, _, scr = _ws(T, di, do, r, noble.NOBLE_BF16, G)
-    R = G * r
-    branch = 0
-    if r > 0:
-        J = G * -(-r // 128)
-        S = max(_proj_split(T, di, J), _proj_split(T, do // G, J))
-        branch = 4 * _align(T * R * 2) + _align(S * T * R * 4) + _copies(R)
-    assert st == OK and scr == branch + _wgrad_bytes(T, di, do, r, 64, 256, G)
+    assert st == OK and scr == _branch_scratch(T, di, do, r, G) + _wgrad_bytes(T, di, do, r, 64, 256, G)
+
 
 def test_workspace_sizes_grouped_and_rank_256():
     """Grouped layers size every rank-side region by R = G r, and the
@@ -219,12 +268,14 @@ def test_workspace_sizes_grouped_and_rank_256():
     S = max(_proj_split(T, di, G), _proj_split(T, do // G, G))
     assert S == 2   # 64 token blocks x 3 jobs = 192 < 256 workgroups: split K in two
     assert st == OK and res == 4 * T * R
-    assert scr == 4 * T * R * 2 + _align(S * T * R * 4) + _copies(R) + _wgrad_bytes(T, di, do, r, 64)
+    assert scr == (T * R * 2 + _align(S * T * R * 4) + 3 * 2 * T * R * 2 + _copies(R)
+                   + _wgrad_bytes(T, di, do, r, 64, groups=G))
     T, di, do, r = 300, 264, 200, 256
     st, res, scr = _ws(T, di, do, r, noble.NOBLE_BF16)
     S = max(_proj_split(T, di, 2), _proj_split(T, do, 2))
     assert st == OK and res == 4 * T * r
-    assert scr == 4 * _align(T * r * 2) + _align(S * T * r * 4) + _copies(r)
+    assert scr == (_align(T * r * 2) + _align(S * T * r * 4) + 3 * _align(2 * T * r * 2) + _copies(r)
+                   + _wgrad_bytes(T, di, do, r, 64))
 
 
 @pytest.mark.parametrize("shape,code", [
@@ -328,7 +379,9 @@ def test_bwd_rejects_null_and_misaligned(which):
 def test_workspace_too_small():
     d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_BF16)
     _, scr = noble.noble_linear_workspace_size(64, 64, 64, 16, noble.NOBLE_BF16)
-    assert _fwd(d, FAKE[:13], scr - 1) == WS
+    fscr = noble.noble_linear_fwd_scratch_size(64, 64, 64, 16, noble.NOBLE_BF16)
+    assert 0 < fscr < scr
+    assert _fwd(d, FAKE[:13], fscr - 1) == WS
     assert _bwd(d, FAKE[:22], scr - 256) == WS
 
 

@@ -3,16 +3,13 @@ fp64 oracle: single cosine, tanh, LeakyReLU and GELU, each as one application
 and (except cosine, whose two-application form is the CosNet covered by
 test_parity_gpu.py) as two applications with the mixing matrix M.
 
-Same metric and bounds as test_parity_gpu.py.  On the bf16 path the
-two-application forms compute A2 from bf16-rounded C1 (the mixing product's
-MFMA operand, as bf16 mixed precision rounds it), so the oracle is run with
-the same operand rounding (mix_round) there.  Two variants need it:
-LeakyReLU's slope is a sign decision on A2 (without the rounding the oracle
-moves by up to 0.2 in dx), and GELU's relative slope grows like |a| for
-negative a, which amplifies the rounding in rank columns whose C2 is near zero
-(0.0215 in dW_up at r = 128 between the oracle with and without it).  Every
-seeded LeakyReLU case also keeps its pre-activations clear of the band where
-float32 and float64 can disagree on the sign (kink_margin > 1).
+Same metric and bounds as test_parity_gpu.py, against the plain oracle.  On
+the bf16 path the kernels take the mixing operand (C1 in H2 = C1 M, dH2 in
+dC1 = dH2 M^T) and the operands of dM as high + low bf16 pairs, so A2 is
+float32-accurate: LeakyReLU's sign decision on A2 and GELU's slope, whose
+relative size grows like |a| for negative a, see the same values the oracle
+computes.  Every seeded LeakyReLU case keeps its pre-activations clear of the
+band where float32 and float64 can disagree on the sign (kink_margin > 1).
 """
 
 import numpy as np
@@ -21,7 +18,7 @@ import pytest
 from paper_2603_06492_amd import inputs as inp
 from paper_2603_06492_amd import noble
 
-from _parity import OUTPUTS, TOL, kink_margin, oracle_outputs, parity_report, round_bf16_f64
+from _parity import OUTPUTS, TOL, kink_margin, oracle_outputs, parity_report
 
 pytestmark = pytest.mark.gpu
 
@@ -49,23 +46,22 @@ def _run(p, act, **kw):
     return dp
 
 
-def _mix_round(act, dt):
-    return round_bf16_f64 if dt == "bf16" and noble.two_layers(act) else None
-
-
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 @pytest.mark.parametrize("act", VARIANTS)
 def test_activation_parity(act, case):
     name, T, di, do, r, dt, seed = case
-    _say(f"[activation] {act} {name}: T={T} d_in={di} d_out={do} r={r} {dt} seed={seed}")
-    p = inp.draw_projection(name, T, di, do, r, dt, seed=seed, bias_std=0.5)
-    mix = _mix_round(act, dt)
-    if act.startswith("leaky"):
-        m = kink_margin(p, act, mix)
-        assert m > 1.0, f"seeded case has a pre-activation inside the kink band (margin {m:.3f})"
+    # LeakyReLU: the seed is stepped (deterministically) until no
+    # pre-activation lies in the kink band, as in test_fuzz_gpu.py
+    for attempt in range(50 if act.startswith("leaky") else 1):
+        p = inp.draw_projection(name, T, di, do, r, dt, seed=seed + 1000 * attempt, bias_std=0.5)
+        if not act.startswith("leaky") or kink_margin(p, act) > 1.0:
+            break
+    else:
+        pytest.fail("no draw clears the LeakyReLU kink band")
+    _say(f"[activation] {act} {name}: T={T} d_in={di} d_out={do} r={r} {dt} seed={seed + 1000 * attempt}")
     dp = _run(p, act)
     got = dp.outputs()
-    ref = oracle_outputs(p, activation=act, mix_round=mix)
+    ref = oracle_outputs(p, activation=act)
     rep = parity_report(got, ref)
     _say(rep)
     want = set(OUTPUTS) - (set() if noble.two_layers(act) else set(SECOND))
@@ -105,12 +101,11 @@ def test_activation_full_size_block(act):
     rng = np.random.default_rng(3)
     rows = np.unique(np.concatenate([[0, 1, 255, 256, p.T - 1], rng.integers(0, p.T, 24)]))
     dw_rows = np.unique(np.concatenate([[0, p.d_in - 1], rng.integers(0, p.d_in, 8)]))
-    mix = _mix_round(act, "bf16")
     dp = _run(p, act)
     got = dp.outputs(rows=rows, dw_rows=dw_rows)
     ok = dp.guards_intact()
     del dp
-    ref = oracle_outputs(p, rows=rows, dw_rows=dw_rows, activation=act, mix_round=mix)
+    ref = oracle_outputs(p, rows=rows, dw_rows=dw_rows, activation=act)
     rep = parity_report(got, ref)
     _say(rep)
     for k, e in rep.items():
@@ -140,8 +135,7 @@ def test_saturated_units_keep_relative_gradient_accuracy(act, shift, dt):
     sat = np.arange(r) % 2 == 0
     sign = np.where(np.arange(r) % 4 == 0, 1.0, -1.0) if act.startswith("tanh") else 1.0
     p.arrays[k] = np.where(sat, sign * shift, p.arrays[k]).astype(np.float32)
-    mix = _mix_round(act, dt)
-    ref = oracle_outputs(p, activation=act, mix_round=mix)
+    ref = oracle_outputs(p, activation=act)
     got = _run(p, act).outputs()
     a = {n: np.asarray(v, dtype=np.float64) for n, v in p.arrays.items() if v is not None}
     terms = np.abs(a["dy"][0])[None, :] * np.abs(a["W_up"])

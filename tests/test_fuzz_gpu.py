@@ -2,12 +2,14 @@
 counts from 1 to 700, widths that are any multiple of 8, ranks up to 256
 (bf16) / 128 (f32), 1 to 4 groups, every activation, both storage types.
 
-The comparison follows the readings the targeted tests use: bf16
-two-application forms and single-token bf16 cases are compared with the
-oracle that rounds the mixing operand C1 to bf16 as the kernels do, and a
-LeakyReLU case is redrawn (deterministically) until no pre-activation lies
-in the band where float32 and float64 can take different sides of the
-kink."""
+Every case is compared with the plain oracle.  A LeakyReLU case is redrawn
+(deterministically) until no pre-activation lies in the band where float32
+and float64 can take different sides of the kink.
+
+FIXED holds cases of a wider one-off sweep that came nearest the bound
+before the mixing and gradient operands became high + low bf16 pairs (a
+4-group tanh_m layer over 256 tokens, whose dW_down rows cancel), and the
+single-token float32 case of test_f32_single_token_conditioning."""
 
 import numpy as np
 import pytest
@@ -15,7 +17,7 @@ import pytest
 from paper_2603_06492_amd import inputs as inp
 from paper_2603_06492_amd import noble
 
-from _parity import OUTPUTS, TOL, kink_margin, oracle_outputs, parity_report, round_bf16_f64
+from _parity import OUTPUTS, TOL, kink_margin, oracle_outputs, parity_report
 
 pytestmark = pytest.mark.gpu
 
@@ -36,19 +38,33 @@ def _cases(n=24, seed=2026):
     return out
 
 
-CASES = _cases()
+FIXED = [
+    ("fixed_bf16_T256_192x160_r8_g4_tanh_m", 256, 192, 160, 8, 4, "bf16", "tanh_m", 749),
+    ("fixed_bf16_T256_96x128_r16_g4_tanh_m", 256, 96, 128, 16, 4, "bf16", "tanh_m", 727),
+]
+CASES = _cases() + FIXED
+# A single float32 token whose dW_up row is the relative error of one tanh
+# value near zero: plain float32 evaluation misses the bound there
+# (tests/test_conditioning.py), so the row metric is expected to fail.
+COND = ("cond_f32_T1_40x352_r64_g4_tanh", 1, 40, 352, 64, 4, "f32", "tanh", 20166)
+CASES.append(pytest.param(COND, marks=pytest.mark.xfail(
+    reason="float32 conditioning: a float32 evaluation of the layer misses the 1e-4 row bound on this "
+           "single-token case (tests/test_conditioning.py)", strict=False)))
 
 
-@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def _case_id(c):
+    return (c.values[0] if hasattr(c, "values") else c)[0]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[_case_id(c) for c in CASES])
 def test_fuzz_parity(case):
     import torch
     from paper_2603_06492_amd.runner import DeviceProblem
     assert torch.cuda.is_available(), "GPU tests need an MI355X"
     name, T, d_in, d_out, r, G, dt, act, seed = case
-    mix = round_bf16_f64 if dt == "bf16" and (noble.two_layers(act) or T == 1) else None
     for attempt in range(50):
         p = inp.draw_projection(name, T, d_in, d_out, r, dt, seed=seed + 1000 * attempt, bias_std=0.5, groups=G)
-        if not act.startswith("leaky") or kink_margin(p, act, mix) > 1.0:
+        if not act.startswith("leaky") or kink_margin(p, act) > 1.0:
             break
     else:
         pytest.fail("no draw clears the LeakyReLU kink band")
@@ -57,7 +73,7 @@ def test_fuzz_parity(case):
     dp.fwd()
     dp.bwd()
     got = dp.outputs()
-    rep = parity_report(got, oracle_outputs(p, activation=act, mix_round=mix))
+    rep = parity_report(got, oracle_outputs(p, activation=act))
     print(rep, flush=True)
     second = {"dM", "domega2", "dphi2"}
     assert set(rep) == set(OUTPUTS) - (set() if noble.two_layers(act) else second)

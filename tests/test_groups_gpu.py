@@ -8,7 +8,7 @@ import pytest
 
 from paper_2603_06492_amd import inputs as inp
 
-from _parity import OUTPUTS, TOL, oracle_outputs, parity_report, round_bf16_f64
+from _parity import OUTPUTS, TOL, oracle_outputs, parity_report
 
 pytestmark = pytest.mark.gpu
 
@@ -50,11 +50,9 @@ def test_grouped_and_wide_rank_parity(case):
     got = dp.outputs()
     # A single token makes row q of dW_up one C2 value times dy (and row i of
     # dM one C1 value times dH2): the row metric is then the relative error
-    # of one cosine, unbounded near its zeros once C1 is rounded to bf16 for
-    # the mixing product.  Such cases compare with the oracle run with that
-    # rounding (the CPU oracle alone moves by 0.43 in dW_up without it).
-    mix = round_bf16_f64 if dt == "bf16" and T == 1 else None
-    rep = parity_report(got, oracle_outputs(p, mix_round=mix))
+    # of one cosine, which the float32-accurate mixing product keeps small
+    # near the cosine's zeros too.
+    rep = parity_report(got, oracle_outputs(p))
     _say(rep)
     assert set(rep) == set(OUTPUTS)
     for k, e in rep.items():
@@ -66,14 +64,12 @@ def test_grouped_and_wide_rank_parity(case):
 def test_grouped_activation_variants(act):
     """A 3-group layer with r = 256 tiles absent (r = 40) and a 1-group r = 256
     layer, with variant activations (two-application forms compared with the
-    bf16 mixing-operand rounding, as in test_activations_gpu.py)."""
-    from paper_2603_06492_amd import noble
-    mix = round_bf16_f64 if noble.two_layers(act) else None
+    plain oracle, as in test_activations_gpu.py)."""
     for (T, di, do, r, G) in ((300, 200, 264, 40, 3), (300, 264, 200, 256, 1)):
         _say(f"[groups] {act}: T={T} d_in={di} d_out={do} r={r} groups={G}")
         p = inp.draw_projection("grp_act", T, di, do, r, "bf16", seed=302, bias_std=0.5, groups=G)
         dp = _run(p, activation=act)
-        rep = parity_report(dp.outputs(), oracle_outputs(p, activation=act, mix_round=mix))
+        rep = parity_report(dp.outputs(), oracle_outputs(p, activation=act))
         _say(rep)
         for k, e in rep.items():
             assert e <= TOL["bf16"], (k, e)

@@ -482,77 +482,6 @@ def test_slopes_keep_relative_accuracy_in_the_tails():
     d = oracle.activation_slope("gelu", a)
     assert np.all(lo + a * dens < d) and np.all(d < hi + a * dens)
 
-# ------------------------------------------------- mixing-operand rounding --
-
-def _coarse(a):
-    """A deliberately coarse rounding (quarters), so that a misplaced rounding
-    is far outside the comparison tolerance."""
-    return np.round(np.asarray(a) * 4.0) / 4.0
-
-
-TWO_LAYER = sorted(a for a, (_, n) in oracle.ACTIVATIONS.items() if n == 2)
-
-
-@pytest.mark.parametrize("act", TWO_LAYER)
-def test_mix_round_matches_torch_straight_through(act):
-    """mix_round rounds C1 where it enters the mixing product and passes the
-    gradient straight through: torch's autograd of c1 + (R(c1) - c1).detach()
-    gives every gradient independently."""
-    torch = pytest.importorskip("torch")
-    F = torch.nn.functional
-    fn = {"cos": torch.cos, "tanh": torch.tanh, "leaky_relu": lambda a: F.leaky_relu(a, 0.01),
-          "gelu": lambda a: F.gelu(a)}[oracle.ACTIVATIONS[act][0]]
-    p = _tiny(seed=31, T=9, d_in=16, d_out=24, r=8)
-    t = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True) for k, v in p.items()}
-    h = t["x"] @ t["W_down"]
-    c1 = fn(t["omega1"] * h + t["phi1"])
-    c1r = c1 + (torch.round(c1 * 4.0) / 4.0 - c1).detach()
-    h2 = (c1r[:, :, None] * t["M"][None, :, :]).sum(dim=1)
-    y = t["x"] @ t["W"] + t["b"] + fn(t["omega2"] * h2 + t["phi2"]) @ t["W_up"]
-    (y * t["dy"]).sum().backward()
-    args = (p["x"], p["W"], p["b"], p["W_down"], p["omega1"], p["phi1"], p["M"], p["omega2"], p["phi2"],
-            p["W_up"])
-    Y, _ = oracle.forward(*args, activation=act, mix_round=_coarse)
-    np.testing.assert_allclose(Y, y.detach().numpy(), rtol=0, atol=1e-12)
-    g = oracle.backward(p["dy"], *(a for i, a in enumerate(args) if i != 2), activation=act, mix_round=_coarse)
-    names = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "M": "dM", "W_up": "dW_up",
-             "omega1": "domega1", "phi1": "dphi1", "omega2": "domega2", "phi2": "dphi2"}
-    for pname, gname in names.items():
-        np.testing.assert_allclose(g[gname], t[pname].grad.numpy(), rtol=1e-10, atol=1e-10,
-                                   err_msg=f"{act} {gname}")
-
-
-def test_mix_round_constant_map_closed_form():
-    """R(c) = 1/2 everywhere: H2 = (1/2) 1 M is the same for every token, so
-    C2 and y's branch are token-independent, and dM = (1/2) 1^T dH2."""
-    p = _tiny(seed=37, T=6)
-    half = lambda a: np.full_like(np.asarray(a, dtype=np.float64), 0.5)
-    args = (p["x"], p["W"], p["b"], p["W_down"], p["omega1"], p["phi1"], p["M"], p["omega2"], p["phi2"],
-            p["W_up"])
-    Y, _ = oracle.forward(*args, mix_round=half)
-    h2 = 0.5 * p["M"].sum(axis=0)
-    c2 = np.cos(p["omega2"] * h2 + p["phi2"])
-    np.testing.assert_allclose(Y, p["x"] @ p["W"] + p["b"] + c2 @ p["W_up"], rtol=0, atol=1e-12)
-    g = oracle.backward(p["dy"], *(a for i, a in enumerate(args) if i != 2), mix_round=half)
-    dA2 = -np.sin(p["omega2"] * h2 + p["phi2"]) * (p["dy"] @ p["W_up"].T)
-    np.testing.assert_allclose(g["dM"], 0.5 * np.outer(np.ones(p["M"].shape[0]), (dA2 * p["omega2"]).sum(axis=0)),
-                               rtol=0, atol=1e-12)
-    np.testing.assert_allclose(g["dphi2"], dA2.sum(axis=0), rtol=0, atol=1e-12)
-
-
-def test_mix_round_identity_is_exact():
-    p = _tiny(seed=41)
-    args = (p["x"], p["W"], p["b"], p["W_down"], p["omega1"], p["phi1"], p["M"], p["omega2"], p["phi2"],
-            p["W_up"])
-    Y0, _ = oracle.forward(*args)
-    Y1, _ = oracle.forward(*args, mix_round=lambda a: a)
-    np.testing.assert_array_equal(Y0, Y1)
-    g0 = oracle.backward(p["dy"], *(a for i, a in enumerate(args) if i != 2))
-    g1 = oracle.backward(p["dy"], *(a for i, a in enumerate(args) if i != 2), mix_round=lambda a: a)
-    for k in GRADS:
-        np.testing.assert_array_equal(g0[k], g1[k])
-
-
 # ------------------------------------------------------------ grouped layers --
 
 def _block_diagonal(p, G):

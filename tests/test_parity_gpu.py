@@ -163,15 +163,9 @@ def test_degenerate_chain(which):
     got, ref = dp.outputs(), oracle_outputs(p)
     rep = parity_report(got, ref)
     _say(rep)
-    if which == "omega1":
-        # Every token has the same C2 row, so row q of dW_up is C2[q] * sum(dy):
-        # its per-row error is the relative error of one cosine, which has no
-        # bound near a zero of cos once C1 is rounded to bf16 for the mixing
-        # product (a CPU simulation of that rounding gives the same 0.175).
-        # Normalise this one output by its largest entry instead.
-        e = float(np.max(np.abs(got["dW_up"] - ref["dW_up"])) / np.max(np.abs(ref["dW_up"])))
-        assert e <= TOL["bf16"], ("dW_up", e)
-        rep.pop("dW_up")
+    # With omega1 = 0 every token has the same C2 row, so row q of dW_up is
+    # C2[q] sum(dy): its row error is the relative error of one cosine value,
+    # which the float32-accurate mixing product keeps small near its zeros.
     for k, e in rep.items():
         assert e <= TOL["bf16"], (k, e)
 
@@ -313,13 +307,10 @@ WIDEST = [("bf16_max_d_in", 1 << 20, 16), ("bf16_max_d_out", 16, 1 << 20)]
 def test_maximum_widths(case):
     """The widest layers the ABI accepts (d = 2^20; T = 40, r = 8): K = 2^20
     in the forward GEMM or the backward's dx, 4096 tiles in the other
-    products.  Element by element against the oracle, every output by the
-    row metric except one: dW_down = x^T dH has 2^20 rows of 40-term sums,
-    and its worst row cancels to a seventh of the typical row size.  There
-    the bf16 MFMA operands of the chain (C1 in the mixing, dH2, dH) move the
-    result by 2-4% of that row (rounding only the oracle's final dH already
-    moves it by 0.024), so dW_down is normalised by its largest entry, as
-    for the degenerate chain."""
+    products.  Element by element against the oracle by the row metric.
+    dW_down = x^T dH has 2^20 rows of 40-term sums, and its worst row cancels
+    to a seventh of the typical row size: one bf16 dH operand would move it
+    by 2.4% of that row, the high + low pair keeps it at float32 accuracy."""
     name, di, do = case
     T, r = 40, 8
     _say(f"[parity] {name}: T={T} d_in={di} d_out={do} r={r}")
@@ -330,7 +321,6 @@ def test_maximum_widths(case):
     del dp
     ref = oracle_outputs(p)
     rep = parity_report(got, ref)
-    rep["dW_down"] = float(np.max(np.abs(got["dW_down"] - ref["dW_down"])) / np.max(np.abs(ref["dW_down"])))
     _say(rep)
     assert set(rep) == set(OUTPUTS)
     for k, e in rep.items():
