@@ -3,15 +3,17 @@
 
 A step is the forward of every projection of the workload in order, then the
 backward of each in reverse order, on one stream (inputs already resident in
-HBM).  The default workload is one block of the 1.5B-style LLM: T = 8 x 1024
-tokens, d = 2048, r = 128, projections QKV 2048->6144, O 2048->2048, FFN up
-2048->8192, FFN down 8192->2048.
+HBM).  The default workload is the largest one-GPU configuration: a slice of
+four 1.5B-style decoder blocks, T = 16 x 2048 tokens, d = 2048, r = 128,
+six projections per block (Q, K, V and O 2048->2048, FFN up 2048->8192, FFN
+down 8192->2048; Q, K and V read the same block input), 24 in all.
 
 Reported: algorithmic TFLOP/s, 6 T [d_in d_out + r (d_in + d_out) + r^2] per
 projection over the step time (no r^2 term for the one-application
 activations, which have no M); the same step with r = 0 (plain linear, same
-kernels) and the overhead over it; the roofline of the main MFMA GEMM; and the
-fp64 oracle's throughput on a bounded sample on the host cores.
+kernels) and the overhead over it; the roofline of the step's dominant launch
+(the weight-gradient product of an FFN projection); and the fp64 oracle's
+throughput on a bounded sample on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                       [--activation NAME]   (CosNet by default)
@@ -51,12 +53,14 @@ def branch_floor(d_in, d_out, r, mixing=True, groups=1):
     return (r * (G * d_in + d_out) + (G * r * r if mixing else 0)) / (d_in * d_out)
 
 
-TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "gemm_fwd_plain_ffn_up_T8192_traffic.md")
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "wgrad_ffn_up_T32768_traffic.md")
+WGRAD_KERNEL = "noble::gemm_bf16_kernel<false, false, true, 0>"
 
 
-# Sources of the roofline kernel (gemm_bf16_kernel): a traffic record stays
-# valid while these files and the compiler flags are unchanged.
-ROOFLINE_SOURCES = ("noble_tiles.hpp", "noble_gemm.hpp", "noble_gemm_dma.hpp")
+# Sources of the roofline kernel (gemm_bf16_kernel) and of the host code that
+# plans its launch (noble_api.hip): a traffic record stays valid while these
+# files and the compiler flags are unchanged.
+ROOFLINE_SOURCES = ("noble_tiles.hpp", "noble_gemm.hpp", "noble_gemm_dma.hpp", "noble_api.hip")
 
 
 def kernel_source_hash() -> str:
@@ -71,10 +75,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(kernel: str, workgroups: int):
+def recorded_traffic(kernel: str, workload: str):
     """HBM bytes per launch of the roofline kernel from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary, or None when that record was taken on
-    other kernel sources or another launch shape."""
+    other sources (kernel or launch planning) or another workload."""
     try:
         with open(TRAFFIC_RECORD) as fh:
             m = re.search(r"^traffic_record: (\{.*\})$", fh.read(), re.M)
@@ -83,9 +87,39 @@ def recorded_traffic(kernel: str, workgroups: int):
         return None
     if rec.get("source_sha256_16") != kernel_source_hash():
         return None
-    if rec.get("workgroups") != workgroups or not kernel.startswith(rec.get("kernel", "?")[5:45]):
+    if rec.get("workload") != workload or rec.get("kernel") != kernel:
         return None
     return rec.get("traffic_bytes")
+
+
+class HipEvents:
+    """hipEvent_t handles created and read through the HIP runtime (for the
+    launch that the library brackets itself, noble_profile_next_wgrad)."""
+
+    def __init__(self):
+        import ctypes
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self) -> int:
+        ev = self.ct.c_void_p()
+        if self.hip.hipEventCreate(self.ct.byref(ev)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return ev.value
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = self.ct.c_float()
+        if self.hip.hipEventSynchronize(self.ct.c_void_p(b)) != 0 or \
+                self.hip.hipEventElapsedTime(self.ct.byref(ms), self.ct.c_void_p(a), self.ct.c_void_p(b)) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def destroy(self, ev: int) -> None:
+        self.hip.hipEventDestroy(self.ct.c_void_p(ev))
 
 
 def _row_err(gpu, ref):
@@ -114,6 +148,7 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0, activ
         threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     except Exception:  # pragma: no cover
         threads = 1
+    cores = len(os.sched_getaffinity(0))
     shapes = inp.workload_shapes(workload)
     groups = inp.workload_groups(workload)
     T_full = shapes[0][1]
@@ -155,7 +190,8 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0, activ
         parity["y"] = max(parity["y"], round(_row_err(gy, Y), 6))
         parity["dx"] = max(parity["dx"], round(_row_err(gdx, dx), 6))
     flops = passes * sum(flop_alg(Ts, di, do, r, mixing, G) for (_, _, di, do, r), G in zip(shapes, groups))
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "blas_threads": int(threads),
+            "kind": "oracle",
             "sample": f"first {Ts} of {T_full} tokens of every projection (the bench's own arrays), "
                       f"numpy float64, {passes} fwd+bwd passes",
             "seconds": round(dt, 3), "parity_vs_gpu": parity}
@@ -166,7 +202,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llm1p5b_block_r128")
+    ap.add_argument("--workload", default="llm1p5b_stack4_r128")
     ap.add_argument("--activation", default="cosnet",
                     help="bottleneck activation: cosnet (default), cos, tanh, tanh_m, leaky_relu, "
                          "leaky_relu_m, gelu, gelu_m")
@@ -176,7 +212,7 @@ def main():
     ap.add_argument("--proj-reps", type=int, default=50,
                     help="calls per per-projection median (fwd, bwd, plain fwd, plain bwd)")
     ap.add_argument("--roofline-launches", type=int, default=20,
-                    help="timed launches of the plain main GEMM for the roofline entry")
+                    help="timed weight-gradient launches of the dominant projection for the roofline entry")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB (a kernel of known "
                          "traffic, for scaling FETCH_SIZE / WRITE_SIZE counters)")
@@ -204,9 +240,10 @@ def main():
           file=sys.stderr, flush=True)
     probs, plain, samples = [], [], []
     sample_rows = min(wl["T"], 8192)
+    xsrc = inp.workload_x_source(args.workload)
     for i in range(len(shapes)):
         p = inp.draw_workload_projection(args.workload, i)
-        dp = DeviceProblem(p, activation=args.activation)
+        dp = DeviceProblem(p, activation=args.activation, x_from=probs[xsrc[i]] if xsrc[i] != i else None)
         probs.append(dp)
         plain.append(DeviceProblem(p, branch=False, inputs_from=dp))
         if not args.no_cpu_baseline:
@@ -252,8 +289,13 @@ def main():
         d = sorted(evs[2 * i].elapsed_time(evs[2 * i + 1]) for i in range(reps))
         return d[reps // 2]
 
-    per = []
+    # one entry per distinct projection shape (the blocks of a stack repeat)
+    per, seen = [], {}
     for dp, d0 in zip(probs, plain):
+        key = (dp.p.d_in, dp.p.d_out, dp.G)
+        if key in seen:
+            seen[key]["also"].append(dp.p.name.split("/")[-1])
+            continue
         T, di, do, r, G = dp.p.T, dp.p.d_in, dp.p.d_out, dp.p.r, dp.G
         for _ in range(10):
             dp.fwd(); dp.bwd(); d0.fwd(); d0.bwd()
@@ -269,7 +311,8 @@ def main():
                  "pct_bf16_peak": round(100 * fl / ((tf + tb) * 1e-3) / PEAK_BF16, 2),
                  "main_gemm_pct_peak": round(100 * 6.0 * T * di * do / ((pf + pb) * 1e-3) / PEAK_BF16, 2),
                  "overhead": round((tf + tb) / (pf + pb) - 1, 4),
-                 "overhead_floor": round(branch_floor(di, do, r, mixing, G), 4)}
+                 "overhead_floor": round(branch_floor(di, do, r, mixing, G), 4), "also": []}
+        seen[key] = entry
         if not args.no_blas:
             # Context only: hipBLASLt (through torch.mm) on the same plain
             # products and operands, bf16 in and out: y = x W, dx = dy W^T,
@@ -287,29 +330,40 @@ def main():
                                                                   / PEAK_BF16, 2)}
         per.append(entry)
 
-    # Roofline entry: the main bf16 MFMA GEMM (x W, plain forward: exactly one
-    # kernel launch per call), timed over its own launches with HIP events on
-    # the stream it runs on.  Algorithmic FLOPs per launch = 2 T d_in d_out.
-    dom = max(plain, key=lambda d: d.p.d_in * d.p.d_out)
+    # Roofline entry: the step's dominant launch, the weight-gradient product
+    # of the projection with the most weight-gradient FLOPs (an FFN
+    # projection): one grouped bf16 MFMA launch computing dW = x^T dy,
+    # dW_down = x^T dH, dW_up = C2^T dy and dM = C1^T dH2 (and db's column
+    # sums).  The library records a pair of HIP events on its stream right
+    # before and after that launch (noble_profile_next_wgrad); `achieved` is
+    # the launch's algorithmic FLOPs, 2 T (d_in d_out + d_in R + r d_out +
+    # G r^2), over the mean of those launch durations.
+    def wgrad_flops(dp):
+        T, di, do, r, G = dp.p.T, dp.p.d_in, dp.p.d_out, dp.p.r, dp.G
+        return 2.0 * T * (di * do + G * r * di + r * do + (G * r * r if mixing else 0))
+    dom = max(probs, key=wgrad_flops)
+    hev = HipEvents()
+    evs = [(hev.create(), hev.create()) for _ in range(args.roofline_launches)]
     for _ in range(3):
-        dom.fwd()
+        dom.bwd()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.roofline_launches):
-        dom.fwd()
-    e1.record(stream)
+    for (a, b) in evs:
+        noble.noble_profile_next_wgrad(a, b)
+        dom.bwd()
     torch.cuda.synchronize()
-    t_launch = e0.elapsed_time(e1) / args.roofline_launches * 1e-3
-    gemm_flops = 2.0 * dom.p.T * dom.p.d_in * dom.p.d_out
-    ach = gemm_flops / t_launch / 1e12
-    wgs = -(-dom.p.T // 256) * -(-dom.p.d_out // 256)
-    kname = "noble::gemm_bf16_kernel<true, false, false, 1>"
+    t_launch = sum(hev.elapsed_ms(a, b) for (a, b) in evs) / len(evs) * 1e-3
+    for (a, b) in evs:
+        hev.destroy(a)
+        hev.destroy(b)
+    wg_flops = wgrad_flops(dom)
+    ach = wg_flops / t_launch / 1e12
+    pname = dom.p.name.split("/")[-1]
     roofline = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
-                "frac": round(ach / (PEAK_BF16 / 1e12), 4), "traffic": recorded_traffic(kname, wgs),
-                "kernel": f"{kname} (plain forward x W, "
-                          f"{dom.p.name.split('/')[-1]} T={dom.p.T} {dom.p.d_in}->{dom.p.d_out}, {wgs} workgroups)",
-                "avg_launch_us": round(t_launch * 1e6, 2), "flop_per_launch": gemm_flops}
+                "frac": round(ach / (PEAK_BF16 / 1e12), 4),
+                "traffic": recorded_traffic(WGRAD_KERNEL, f"{args.workload}/{pname}"),
+                "kernel": f"{WGRAD_KERNEL} (weight gradients dW, dW_down, dW_up, dM of "
+                          f"{pname} T={dom.p.T} {dom.p.d_in}->{dom.p.d_out} r={dom.r})",
+                "avg_launch_us": round(t_launch * 1e6, 2), "flop_per_launch": wg_flops}
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib * (1 << 20)

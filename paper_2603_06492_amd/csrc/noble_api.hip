@@ -158,9 +158,10 @@ noble_status optional(const void* p) { return (!p || aligned16(p)) ? NOBLE_OK : 
 // gfx950 check, cached per device ordinal (0 unknown, 1 ok, 2 unsupported).
 std::atomic<int> g_arch_ok[256];
 
-noble_status check_device() {
+noble_status check_device(int* dev_out = nullptr) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return NOBLE_ERR_HIP;
+    if (dev_out) *dev_out = dev;
     if (dev < 0 || dev >= 256) return NOBLE_ERR_UNSUPPORTED_DEVICE;
     int s = g_arch_ok[dev].load(std::memory_order_relaxed);
     if (s == 0) {
@@ -184,6 +185,10 @@ noble_status launch(void (*kernel)(Arg), dim3 grid, dim3 block, hipStream_t st, 
 }
 
 int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// Events of noble_profile_next_wgrad, one pair per host thread, consumed by
+// that thread's next backward with a weight-gradient launch.
+thread_local hipEvent_t t_wgrad_ev0 = nullptr, t_wgrad_ev1 = nullptr;
 
 // Grid of a launch of n workgroups on rows of kGridRow (see flat_block).
 dim3 flat_grid(int64_t n) {
@@ -818,7 +823,11 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
                 }
             }
         }
+        hipEvent_t ev0 = t_wgrad_ev0, ev1 = t_wgrad_ev1;
+        t_wgrad_ev0 = t_wgrad_ev1 = nullptr;
+        if (ev0 && hipEventRecord(ev0, st) != hipSuccess) return NOBLE_ERR_HIP;
         NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
+        if (ev1 && hipEventRecord(ev1, st) != hipSuccess) return NOBLE_ERR_HIP;
         if (copies) {
             const int64_t arr = (int64_t)kChainCopies * R;
             reduce(copies, dw1, R, kChainCopies);
@@ -876,10 +885,15 @@ noble_status noble_linear_fwd_scratch_size(const noble_linear_desc* desc, size_t
     return NOBLE_OK;
 }
 
-noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, const void* W, const float* b,
-                              const void* W_down, const float* omega1, const float* phi1, const void* M,
-                              const float* omega2, const float* phi2, const void* W_up, void* y, void* reserve,
-                              void* scratch, size_t scratch_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the forward.
+noble_status fwd_check(const noble_linear_desc* desc, const void* x, const void* W, const float* b,
+                       const void* W_down, const float* omega1, const float* phi1, const void* M,
+                       const float* omega2, const float* phi2, const void* W_up, const void* y,
+                       const void* reserve, const void* scratch, int64_t scratch_bytes) {
     NOBLE_TRY(check_desc(desc));
     NOBLE_TRY(check_grids(desc));
     const bool rows = desc->T > 0, br = desc->r > 0;
@@ -898,9 +912,22 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, cons
         NOBLE_TRY(need(W_up, true));
         NOBLE_TRY(optional(reserve));   // NULL: inference-only forward
         NOBLE_TRY(need(scratch, rows));
-        if (scratch_bytes < fwd_scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
+        if ((size_t)scratch_bytes < fwd_scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
     }
-    if (!rows) return NOBLE_OK;
+    return NOBLE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, const void* W, const float* b,
+                              const void* W_down, const float* omega1, const float* phi1, const void* M,
+                              const float* omega2, const float* phi2, const void* W_up, void* y, void* reserve,
+                              void* scratch, size_t scratch_bytes, void* stream) {
+    NOBLE_TRY(fwd_check(desc, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
+                        (int64_t)std::min<size_t>(scratch_bytes, (size_t)INT64_MAX)));
+    if (desc->T == 0) return NOBLE_OK;
     NOBLE_TRY(check_device());
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (desc->dtype == NOBLE_BF16)
@@ -952,6 +979,12 @@ noble_status noble_linear_bwd(const noble_linear_desc* desc, const void* dy, con
                                   dW_down, dM, dW_up, domega1, dphi1, domega2, dphi2, scratch, st);
     return bwd_impl<float>(desc, dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve, dx, dW, db, dW_down,
                            dM, dW_up, domega1, dphi1, domega2, dphi2, scratch, st);
+}
+
+noble_status noble_profile_next_wgrad(void* start_event, void* stop_event) {
+    t_wgrad_ev0 = static_cast<hipEvent_t>(start_event);
+    t_wgrad_ev1 = static_cast<hipEvent_t>(stop_event);
+    return NOBLE_OK;
 }
 
 void noble_recipe_defaults(noble_recipe* r) {

@@ -154,8 +154,10 @@ WORKLOADS: Dict[str, dict] = {
     # ViT-B-width layer: 128 images x 197 tokens, d = 768, r = 32
     "vitb_ffn_r32": dict(T=25216, r=32, dtype="bf16",
                          projections=[("ffn_up", 768, 3072), ("ffn_down", 3072, 768)]),
-    # four 1.5B-style blocks, six projections each, 16 x 2048 tokens
+    # four 1.5B-style blocks, six projections each, 16 x 2048 tokens; Q, K
+    # and V of a block read the same block input (K and V reuse Q's x)
     "llm1p5b_stack4_r128": dict(T=32768, r=128, dtype="bf16",
+                                share_x={6 * blk + j: 6 * blk for blk in range(4) for j in (1, 2)},
                                 projections=[(f"b{blk}_{p}", di, do)
                                              for blk in range(4)
                                              for (p, di, do) in (("q", 2048, 2048), ("k", 2048, 2048),
@@ -185,6 +187,21 @@ def workload_shapes(name: str) -> List[Tuple[str, int, int, int, int]]:
     return [(p, w["T"], di, do, w["r"]) for (p, di, do, _) in map(_proj, w["projections"])]
 
 
+def workload_x_source(name: str) -> List[int]:
+    """For each projection of a workload, the index of the projection whose x
+    it reads (itself, or the Q projection of its block for K and V)."""
+    w = WORKLOADS[name]
+    share = w.get("share_x", {})
+    return [share.get(i, i) for i in range(len(w["projections"]))]
+
+
+def draw_x(T: int, d_in: int, dtype: str, seed: int) -> np.ndarray:
+    """The x that draw_projection(..., seed) draws first, alone."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    x = rng.standard_normal((T, d_in), dtype=np.float32)
+    return round_bf16(x) if dtype == "bf16" else x
+
+
 def workload_groups(name: str) -> List[int]:
     """Branch groups of each projection of a workload."""
     return [_proj(e)[3] for e in WORKLOADS[name]["projections"]]
@@ -193,6 +210,8 @@ def workload_groups(name: str) -> List[int]:
 def draw_workload_projection(name: str, index: int, seed: int = 0, T: Optional[int] = None,
                              **overrides) -> Projection:
     """Projection ``index`` of workload ``name`` drawn with seed ``seed + index``.
+    A projection that shares its block's input (workload_x_source) has the
+    x of its source projection instead of its own first draw.
 
     ``T`` overrides the token count (a prefix sample of the workload's rows is
     not the same draw; use the full T for full-size checks)."""
@@ -201,5 +220,9 @@ def draw_workload_projection(name: str, index: int, seed: int = 0, T: Optional[i
     kw = dict(w.get("var", {}))
     kw.update(overrides)
     kw.setdefault("groups", G)
-    return draw_projection(f"{name}/{p}", w["T"] if T is None else T, di, do, w["r"],
-                           w["dtype"], seed + index, **kw)
+    TT = w["T"] if T is None else T
+    proj = draw_projection(f"{name}/{p}", TT, di, do, w["r"], w["dtype"], seed + index, **kw)
+    src = workload_x_source(name)[index]
+    if src != index:
+        proj.arrays["x"] = draw_x(TT, di, w["dtype"], seed + src)
+    return proj

@@ -123,6 +123,8 @@ def lib() -> ctypes.CDLL:
         L.noble_linear_workspace_size.argtypes = [ctypes.POINTER(noble_linear_desc),
                                                   ctypes.POINTER(ctypes.c_size_t),
                                                   ctypes.POINTER(ctypes.c_size_t)]
+        L.noble_profile_next_wgrad.restype = ctypes.c_int
+        L.noble_profile_next_wgrad.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         L.noble_linear_fwd_scratch_size.restype = ctypes.c_int
         L.noble_linear_fwd_scratch_size.argtypes = [ctypes.POINTER(noble_linear_desc),
                                                     ctypes.POINTER(ctypes.c_size_t)]
@@ -149,6 +151,12 @@ def noble_status_string(status: int) -> str:
 def make_desc(T: int, d_in: int, d_out: int, r: int, dtype: int, activation=0, groups: int = 1) -> noble_linear_desc:
     return noble_linear_desc(int(T), int(d_in), int(d_out), int(r), int(dtype), activation_code(activation),
                              int(groups), 0)
+
+
+def noble_profile_next_wgrad(start_event: int, stop_event: int) -> None:
+    """The calling thread's next backward records these hipEvent_t handles
+    around its weight-gradient launch (instrumentation)."""
+    lib().noble_profile_next_wgrad(ctypes.c_void_p(start_event), ctypes.c_void_p(stop_event))
 
 
 def noble_linear_fwd_scratch_size(T: int, d_in: int, d_out: int, r: int, dtype: int,

@@ -26,6 +26,8 @@ class DeviceProblem:
     ``canary=True`` surrounds every output with guard bands filled with a NaN
     pattern, so out-of-bounds writes can be detected with ``guards_intact``.
     ``branch=False`` runs the same shapes as a plain linear (r = 0).
+    ``x_from`` reads x from that problem's device tensor (the same values:
+    projections that share their block's input).
     ``activation`` names the bottleneck activation (noble.ACTIVATIONS).  For a
     one-application activation, M, omega2, phi2 and their gradients are passed
     as None unless ``pass_unused`` (then the gradients must come back zero).
@@ -34,7 +36,7 @@ class DeviceProblem:
     def __init__(self, p: Projection, device: str = "cuda", *, with_bias: bool = True,
                  with_db: bool = True, branch: bool = True, canary: bool = False,
                  inputs_from: Optional["DeviceProblem"] = None, activation: str = "cosnet",
-                 pass_unused: bool = False):
+                 pass_unused: bool = False, x_from: Optional["DeviceProblem"] = None):
         torch = _torch()
         if not torch.cuda.is_available():
             raise RuntimeError("DeviceProblem needs a GPU")
@@ -54,6 +56,11 @@ class DeviceProblem:
             self.t.update(inputs_from.t)
         else:
             for k, v in p.device_arrays().items():
+                if k == "x" and x_from is not None:
+                    # the same device tensor as x_from's (a shared block input)
+                    assert tuple(x_from.t["x"].shape) == v.shape
+                    self.t["x"] = x_from.t["x"]
+                    continue
                 if k in STORAGE and p.dtype == "bf16":
                     t = torch.from_numpy(v.view(np.int16)).to(device).view(torch.bfloat16)
                 else:

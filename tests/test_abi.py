@@ -31,7 +31,7 @@ def _declared_functions():
 def test_library_exports_every_declared_function():
     names = _declared_functions()
     assert set(names) == {"noble_linear_workspace_size", "noble_linear_fwd_scratch_size", "noble_linear_fwd",
-                          "noble_linear_bwd",
+                          "noble_linear_bwd", "noble_profile_next_wgrad",
                           "noble_status_string", "noble_abi_version", "noble_recipe_defaults",
                           "noble_lr_multipliers", "noble_init_params"}
     L = noble.lib()
