@@ -160,6 +160,31 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc,
                               void* scratch, size_t scratch_bytes,
                               void* stream);
 
+/* The forward above without a scratch argument, for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation).  It uses a scratch array that the library holds in
+ * device memory: NOBLE_STATIC_SCRATCH_BYTES on each GPU it runs on, from the
+ * first call on that GPU until the process ends.  It allocates nothing and
+ * makes no allocating call.  Arguments, outputs and status codes are those of
+ * noble_linear_fwd; a layer whose forward needs more scratch than the array
+ * holds (noble_linear_fwd_scratch_size above NOBLE_STATIC_SCRATCH_BYTES;
+ * at r = 128 that is beyond about 87000 tokens) returns
+ * NOBLE_ERR_WORKSPACE_TOO_SMALL before any HIP call.  Every call on one GPU
+ * shares that GPU's array: calls that overlap on one GPU (on different
+ * streams, or from different threads without ordering) race on it and must
+ * not be issued; calls ordered on one stream are safe.  The array's contents
+ * are never read before being written within a call. */
+#define NOBLE_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+noble_status noble_linear_fwd_static(const noble_linear_desc* desc,
+                                     const void* x, const void* W, const float* b,
+                                     const void* W_down,
+                                     const float* omega1, const float* phi1,
+                                     const void* M,
+                                     const float* omega2, const float* phi2,
+                                     const void* W_up,
+                                     void* y, void* reserve,
+                                     void* stream);
+
 /* Backward of the forward above for upstream gradient dy [T, d_out], using
  * the reserve written by the matching forward (same inputs, same desc).
  * Every gradient buffer is overwritten (not accumulated):

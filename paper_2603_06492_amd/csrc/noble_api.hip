@@ -186,6 +186,26 @@ noble_status launch(void (*kernel)(Arg), dim3 grid, dim3 block, hipStream_t st, 
 
 int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
+// Scratch of noble_linear_fwd_static: a file-scope device array, one copy per
+// GPU the library runs on, held until the process ends.  Host code never
+// passes this name to a kernel (in host code it is only a stand-in for the
+// device symbol): each device's address comes from hipGetSymbolAddress,
+// taken once per device with that device current, and cached here.
+constexpr size_t kStaticScratchBytes = NOBLE_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) char g_static_scratch[kStaticScratchBytes];
+std::atomic<void*> g_static_scratch_addr[256];
+
+// Device address of g_static_scratch on the current device `dev`.
+noble_status static_scratch(int dev, void** out) {
+    void* p = g_static_scratch_addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_static_scratch)) != hipSuccess || !p) return NOBLE_ERR_HIP;
+        g_static_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return NOBLE_OK;
+}
+
 // Events of noble_profile_next_wgrad, one pair per host thread, consumed by
 // that thread's next backward with a weight-gradient launch.
 thread_local hipEvent_t t_wgrad_ev0 = nullptr, t_wgrad_ev1 = nullptr;
@@ -889,7 +909,8 @@ noble_status noble_linear_fwd_scratch_size(const noble_linear_desc* desc, size_t
 
 namespace {
 
-// Argument checks of the forward.
+// Argument checks of the forward; `scratch_bytes` < 0: the scratch is the
+// static array (not checked here).
 noble_status fwd_check(const noble_linear_desc* desc, const void* x, const void* W, const float* b,
                        const void* W_down, const float* omega1, const float* phi1, const void* M,
                        const float* omega2, const float* phi2, const void* W_up, const void* y,
@@ -911,8 +932,12 @@ noble_status fwd_check(const noble_linear_desc* desc, const void* x, const void*
         NOBLE_TRY(l2 ? need(phi2, true) : optional(phi2));
         NOBLE_TRY(need(W_up, true));
         NOBLE_TRY(optional(reserve));   // NULL: inference-only forward
-        NOBLE_TRY(need(scratch, rows));
-        if ((size_t)scratch_bytes < fwd_scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
+        if (scratch_bytes >= 0) {
+            NOBLE_TRY(need(scratch, rows));
+            if ((size_t)scratch_bytes < fwd_scratch_need(desc)) return NOBLE_ERR_WORKSPACE_TOO_SMALL;
+        } else if (fwd_scratch_need(desc) > kStaticScratchBytes) {
+            return NOBLE_ERR_WORKSPACE_TOO_SMALL;
+        }
     }
     return NOBLE_OK;
 }
@@ -929,6 +954,22 @@ noble_status noble_linear_fwd(const noble_linear_desc* desc, const void* x, cons
                         (int64_t)std::min<size_t>(scratch_bytes, (size_t)INT64_MAX)));
     if (desc->T == 0) return NOBLE_OK;
     NOBLE_TRY(check_device());
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (desc->dtype == NOBLE_BF16)
+        return fwd_impl<uint16_t>(desc, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch, st);
+    return fwd_impl<float>(desc, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch, st);
+}
+
+noble_status noble_linear_fwd_static(const noble_linear_desc* desc, const void* x, const void* W, const float* b,
+                                     const void* W_down, const float* omega1, const float* phi1, const void* M,
+                                     const float* omega2, const float* phi2, const void* W_up, void* y,
+                                     void* reserve, void* stream) {
+    NOBLE_TRY(fwd_check(desc, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, nullptr, -1));
+    if (desc->T == 0) return NOBLE_OK;
+    int dev = 0;
+    NOBLE_TRY(check_device(&dev));
+    void* scratch = nullptr;
+    if (desc->r > 0) NOBLE_TRY(static_scratch(dev, &scratch));
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (desc->dtype == NOBLE_BF16)
         return fwd_impl<uint16_t>(desc, x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch, st);

@@ -123,6 +123,8 @@ def lib() -> ctypes.CDLL:
         L.noble_linear_workspace_size.argtypes = [ctypes.POINTER(noble_linear_desc),
                                                   ctypes.POINTER(ctypes.c_size_t),
                                                   ctypes.POINTER(ctypes.c_size_t)]
+        L.noble_linear_fwd_static.restype = ctypes.c_int
+        L.noble_linear_fwd_static.argtypes = [ctypes.POINTER(noble_linear_desc)] + [ctypes.c_void_p] * 13
         L.noble_profile_next_wgrad.restype = ctypes.c_int
         L.noble_profile_next_wgrad.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         L.noble_linear_fwd_scratch_size.restype = ctypes.c_int
@@ -277,6 +279,31 @@ def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, re
         st = lib().noble_linear_fwd(ctypes.byref(d), *args, nbytes, _stream(stream, dev))
     if st != 0:
         raise NobleError(st, "noble_linear_fwd")
+
+
+def noble_linear_fwd_static(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve,
+                            stream=None, activation=0, groups: int = 1) -> None:
+    """noble_linear_fwd without a scratch argument: the library's own static
+    device scratch (for callers that cannot allocate; see include/noble.h)."""
+    torch = _torch()
+    T, d_in = x.shape
+    d_out = W.shape[1]
+    R = 0 if W_down is None else W_down.shape[1]
+    sh, r = _branch_shapes(d_in, d_out, R, groups)
+    sd, f32, dev = x.dtype, torch.float32, x.device
+    d = make_desc(T, d_in, d_out, r, _dtype_code(x), activation, groups)
+    args = [
+        _ptr(x, "x", sd, (T, d_in), dev), _ptr(W, "W", sd, (d_in, d_out), dev), _ptr(b, "b", f32, (d_out,), dev),
+        _ptr(W_down, "W_down", sd, sh["W_down"], dev), _ptr(omega1, "omega1", f32, sh["vec"], dev),
+        _ptr(phi1, "phi1", f32, sh["vec"], dev), _ptr(M, "M", sd, sh["M"], dev),
+        _ptr(omega2, "omega2", f32, sh["vec"], dev), _ptr(phi2, "phi2", f32, sh["vec"], dev),
+        _ptr(W_up, "W_up", sd, sh["W_up"], dev), _ptr(y, "y", sd, (T, d_out), dev),
+        _ptr(reserve, "reserve", device=dev),
+    ]
+    with _on(dev):
+        st = lib().noble_linear_fwd_static(ctypes.byref(d), *args, _stream(stream, dev))
+    if st != 0:
+        raise NobleError(st, "noble_linear_fwd_static")
 
 
 def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve,

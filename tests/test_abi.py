@@ -31,7 +31,7 @@ def _declared_functions():
 def test_library_exports_every_declared_function():
     names = _declared_functions()
     assert set(names) == {"noble_linear_workspace_size", "noble_linear_fwd_scratch_size", "noble_linear_fwd",
-                          "noble_linear_bwd", "noble_profile_next_wgrad",
+                          "noble_linear_bwd", "noble_profile_next_wgrad", "noble_linear_fwd_static",
                           "noble_status_string", "noble_abi_version", "noble_recipe_defaults",
                           "noble_lr_multipliers", "noble_init_params"}
     L = noble.lib()
@@ -526,3 +526,26 @@ def test_workspace_queries_from_many_threads():
 
     with ThreadPoolExecutor(8) as ex:
         assert sum(ex.map(worker, range(16))) == 0
+
+
+def test_static_forward_rejects_before_any_hip_call():
+    """noble_linear_fwd_static checks like noble_linear_fwd and rejects a
+    layer whose forward scratch exceeds the static array
+    (NOBLE_STATIC_SCRATCH_BYTES, 64 MiB) with NOBLE_ERR_WORKSPACE_TOO_SMALL;
+    none of these calls reaches the device."""
+    L = noble.lib()
+    limit = 64 << 20
+    fits, big = 80000, 90000
+    assert _fws(fits, 2048, 2048, 128, noble.NOBLE_BF16)[1] <= limit < _fws(big, 2048, 2048, 128, noble.NOBLE_BF16)[1]
+    d = noble.make_desc(big, 2048, 2048, 128, noble.NOBLE_BF16)
+    assert L.noble_linear_fwd_static(ctypes.byref(d), *FAKE[:12], None) == WS
+    d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_BF16)
+    ptrs = list(FAKE[:12])
+    ptrs[0] = None
+    assert L.noble_linear_fwd_static(ctypes.byref(d), *ptrs, None) == NULL
+    ptrs = list(FAKE[:12])
+    ptrs[3] = FAKE[3] + 8
+    assert L.noble_linear_fwd_static(ctypes.byref(d), *ptrs, None) == MISAL
+    assert L.noble_linear_fwd_static(None, *FAKE[:12], None) == NULL
+    d = noble.make_desc(64, 64, 64, 20, noble.NOBLE_BF16)
+    assert L.noble_linear_fwd_static(ctypes.byref(d), *FAKE[:12], None) == SHAPE
