@@ -57,10 +57,10 @@ TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "wgrad_ffn_up_T32768_traffic.md"
 WGRAD_KERNEL = "noble::gemm_bf16_kernel<false, false, true, 0>"
 
 
-# Sources of the roofline kernel (gemm_bf16_kernel) and of the host code that
-# plans its launch (noble_api.hip): a traffic record stays valid while these
-# files and the compiler flags are unchanged.
-ROOFLINE_SOURCES = ("noble_tiles.hpp", "noble_gemm.hpp", "noble_gemm_dma.hpp", "noble_api.hip")
+# Sources of the roofline kernel (gemm_bf16_kernel): a traffic record stays
+# valid while these files and the compiler flags are unchanged and the launch
+# has the recorded workgroup count (which the host's plan sets).
+ROOFLINE_SOURCES = ("noble_tiles.hpp", "noble_gemm.hpp", "noble_gemm_dma.hpp")
 
 
 def kernel_source_hash() -> str:
@@ -75,10 +75,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(kernel: str, workload: str):
+def recorded_traffic(kernel: str, workload: str, workgroups: int):
     """HBM bytes per launch of the roofline kernel from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary, or None when that record was taken on
-    other sources (kernel or launch planning) or another workload."""
+    other kernel sources, another workload or another launch shape."""
     try:
         with open(TRAFFIC_RECORD) as fh:
             m = re.search(r"^traffic_record: (\{.*\})$", fh.read(), re.M)
@@ -87,7 +87,7 @@ def recorded_traffic(kernel: str, workload: str):
         return None
     if rec.get("source_sha256_16") != kernel_source_hash():
         return None
-    if rec.get("workload") != workload or rec.get("kernel") != kernel:
+    if rec.get("workload") != workload or rec.get("kernel") != kernel or rec.get("workgroups") != workgroups:
         return None
     return rec.get("traffic_bytes")
 
@@ -347,8 +347,10 @@ def main():
     for _ in range(3):
         dom.bwd()
     torch.cuda.synchronize()
+    import ctypes
+    wgs = ctypes.c_int64(0)
     for (a, b) in evs:
-        noble.noble_profile_next_wgrad(a, b)
+        noble.noble_profile_next_wgrad(a, b, wgs)
         dom.bwd()
     torch.cuda.synchronize()
     t_launch = sum(hev.elapsed_ms(a, b) for (a, b) in evs) / len(evs) * 1e-3
@@ -360,9 +362,9 @@ def main():
     pname = dom.p.name.split("/")[-1]
     roofline = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
                 "frac": round(ach / (PEAK_BF16 / 1e12), 4),
-                "traffic": recorded_traffic(WGRAD_KERNEL, f"{args.workload}/{pname}"),
+                "traffic": recorded_traffic(WGRAD_KERNEL, f"{args.workload}/{pname}", wgs.value),
                 "kernel": f"{WGRAD_KERNEL} (weight gradients dW, dW_down, dW_up, dM of "
-                          f"{pname} T={dom.p.T} {dom.p.d_in}->{dom.p.d_out} r={dom.r})",
+                          f"{pname} T={dom.p.T} {dom.p.d_in}->{dom.p.d_out} r={dom.r}, {wgs.value} workgroups)",
                 "avg_launch_us": round(t_launch * 1e6, 2), "flop_per_launch": wg_flops}
 
     if args.copy_calibration_mib > 0:

@@ -220,11 +220,12 @@ noble_status noble_linear_bwd(const noble_linear_desc* desc,
  * dW_up and dM, and db's column sums) records start_event and stop_event
  * (hipEvent_t values created by the caller, either may be NULL) on its
  * stream immediately before and after that launch, so that
- * hipEventElapsedTime gives the launch's duration; the hook then clears
- * itself.  Calling it again replaces the pending pair; NULL, NULL clears
- * it.  A backward that fails validation, or has T = 0, leaves it pending.
- * Returns NOBLE_OK; makes no HIP call. */
-noble_status noble_profile_next_wgrad(void* start_event, void* stop_event);
+ * hipEventElapsedTime gives the launch's duration, and stores the launch's
+ * workgroup count in *workgroups (host memory; may be NULL) when it enqueues
+ * it; the hook then clears itself.  Calling it again replaces the pending
+ * request; NULL, NULL, NULL clears it.  A backward that fails validation, or
+ * has T = 0, leaves it pending.  Returns NOBLE_OK; makes no HIP call. */
+noble_status noble_profile_next_wgrad(void* start_event, void* stop_event, int64_t* workgroups);
 
 /* ------------------------------------------------------------------------
  * Training recipe around the layer (Sec. 3.3 "Key Design Choices", App. A

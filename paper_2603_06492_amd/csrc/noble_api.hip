@@ -209,6 +209,7 @@ noble_status static_scratch(int dev, void** out) {
 // Events of noble_profile_next_wgrad, one pair per host thread, consumed by
 // that thread's next backward with a weight-gradient launch.
 thread_local hipEvent_t t_wgrad_ev0 = nullptr, t_wgrad_ev1 = nullptr;
+thread_local int64_t* t_wgrad_wgs = nullptr;
 
 // Grid of a launch of n workgroups on rows of kGridRow (see flat_block).
 dim3 flat_grid(int64_t n) {
@@ -844,7 +845,9 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             }
         }
         hipEvent_t ev0 = t_wgrad_ev0, ev1 = t_wgrad_ev1;
+        if (t_wgrad_wgs) *t_wgrad_wgs = bt.blocks;
         t_wgrad_ev0 = t_wgrad_ev1 = nullptr;
+        t_wgrad_wgs = nullptr;
         if (ev0 && hipEventRecord(ev0, st) != hipSuccess) return NOBLE_ERR_HIP;
         NOBLE_TRY((launch_gemm<E, false, false>(bt, st)));
         if (ev1 && hipEventRecord(ev1, st) != hipSuccess) return NOBLE_ERR_HIP;
@@ -1022,9 +1025,10 @@ noble_status noble_linear_bwd(const noble_linear_desc* desc, const void* dy, con
                            dM, dW_up, domega1, dphi1, domega2, dphi2, scratch, st);
 }
 
-noble_status noble_profile_next_wgrad(void* start_event, void* stop_event) {
+noble_status noble_profile_next_wgrad(void* start_event, void* stop_event, int64_t* workgroups) {
     t_wgrad_ev0 = static_cast<hipEvent_t>(start_event);
     t_wgrad_ev1 = static_cast<hipEvent_t>(stop_event);
+    t_wgrad_wgs = workgroups;
     return NOBLE_OK;
 }
 

@@ -126,7 +126,7 @@ def lib() -> ctypes.CDLL:
         L.noble_linear_fwd_static.restype = ctypes.c_int
         L.noble_linear_fwd_static.argtypes = [ctypes.POINTER(noble_linear_desc)] + [ctypes.c_void_p] * 13
         L.noble_profile_next_wgrad.restype = ctypes.c_int
-        L.noble_profile_next_wgrad.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        L.noble_profile_next_wgrad.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)]
         L.noble_linear_fwd_scratch_size.restype = ctypes.c_int
         L.noble_linear_fwd_scratch_size.argtypes = [ctypes.POINTER(noble_linear_desc),
                                                     ctypes.POINTER(ctypes.c_size_t)]
@@ -155,10 +155,12 @@ def make_desc(T: int, d_in: int, d_out: int, r: int, dtype: int, activation=0, g
                              int(groups), 0)
 
 
-def noble_profile_next_wgrad(start_event: int, stop_event: int) -> None:
+def noble_profile_next_wgrad(start_event: int, stop_event: int, workgroups=None) -> None:
     """The calling thread's next backward records these hipEvent_t handles
-    around its weight-gradient launch (instrumentation)."""
-    lib().noble_profile_next_wgrad(ctypes.c_void_p(start_event), ctypes.c_void_p(stop_event))
+    around its weight-gradient launch and, given a ctypes.c_int64,
+    stores that launch's workgroup count in it (instrumentation)."""
+    lib().noble_profile_next_wgrad(ctypes.c_void_p(start_event), ctypes.c_void_p(stop_event),
+                                   None if workgroups is None else ctypes.byref(workgroups))
 
 
 def noble_linear_fwd_scratch_size(T: int, d_in: int, d_out: int, r: int, dtype: int,
