@@ -71,8 +71,18 @@ ACTIVATIONS = {
     "leaky_relu_m": ("leaky_relu", 2),
     "gelu": ("gelu", 1),
     "gelu_m": ("gelu", 2),
+    "cosnet3": ("cos", 3),
 }
 LEAKY_SLOPE = 0.01
+# The 3-layer CosNet (last row of Table 5; §5 "CosNet Architecture
+# Evolution": three or more layers).  Reading: a third cosine application
+# after a second r x r mixing matrix, with its own per-dimension frequency
+# and phase, the same pattern that links the first two:
+#     A3 = w3 (.) (C2 M') + p3,  C3 = cos(A3),  sigma(h) = C3.
+# Its parameters travel stacked with the second layer's: M is [2, r, r]
+# (M[0] between layers 1 and 2, M[1] between 2 and 3; [2, G, r, r] for a
+# grouped layer), omega2 and phi2 are [2, r] (row 0 layer 2, row 1 layer 3),
+# and so are the gradients dM, domega2, dphi2.
 
 
 def _f64(a):
@@ -117,23 +127,41 @@ def activation_slope(f, a):
     raise ValueError(f"unknown activation {f!r}")
 
 
+def _third_layer(M, omega2, phi2):
+    """Split the stacked parameters of the 3-layer form: (M, w2, p2) of the
+    second layer and (M', w3, p3) of the third."""
+    M, omega2, phi2 = _f64(M), _f64(omega2), _f64(phi2)
+    return (M[0], omega2[0], phi2[0]), (M[1], omega2[1], phi2[1])
+
+
 def branch_forward(H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
     """The bottleneck nonlinearity sigma applied to every row of ``H: [T, r]``.
 
     2-layer forms (Eq. (2) for cosine):  A1 = w1 (.) H + p1, C1 = f(A1),
     H2 = C1 M, A2 = w2 (.) H2 + p2, C2 = f(A2).  1-layer forms stop at
-    C2 = C1 = f(A1) and ignore M, w2, p2.  Returns the intermediates by name.
+    C2 = C1 = f(A1) and ignore M, w2, p2.  The 3-layer form continues with
+    H3 = C2 M', A3 = w3 (.) H3 + p3, C3 = f(A3) (parameters stacked, see
+    ACTIVATIONS).  Returns the intermediates by name; "out" is sigma(H).
     """
     f, layers = ACTIVATIONS[activation]
     H = _f64(H)
+    if layers == 3:
+        (M, omega2, phi2), third = _third_layer(M, omega2, phi2)
     A1 = H * _f64(omega1) + _f64(phi1)          # w1 (.) h + p1
     C1 = activation_value(f, A1)                 # h1 = f(.)
     if layers == 1:
-        return {"A1": A1, "C1": C1, "C2": C1}
+        return {"A1": A1, "C1": C1, "C2": C1, "out": C1}
     H2 = C1 @ _f64(M)                            # h2 = h1 mixed by M (row form)
     A2 = H2 * _f64(omega2) + _f64(phi2)          # w2 (.) h2 + p2
     C2 = activation_value(f, A2)                 # sigma(h) = f(.)
-    return {"A1": A1, "C1": C1, "H2": H2, "A2": A2, "C2": C2}
+    fw = {"A1": A1, "C1": C1, "H2": H2, "A2": A2, "C2": C2, "out": C2}
+    if layers == 3:
+        M3, w3, p3 = third
+        H3 = C2 @ M3                             # the second layer's output mixed by M'
+        A3 = H3 * w3 + p3                        # w3 (.) h3 + p3
+        C3 = activation_value(f, A3)
+        fw.update(H3=H3, A3=A3, C3=C3, out=C3)
+    return fw
 
 
 def cosnet_forward(H, omega1, phi1, M, omega2, phi2):
@@ -153,7 +181,7 @@ def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="co
     """
     x = _f64(x)
     H = x @ _f64(W_down)
-    C2 = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)["C2"]
+    C2 = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)["out"]
     Y = x @ _f64(W) + C2 @ _f64(W_up)
     if b is not None:
         Y = Y + _f64(b)
@@ -161,18 +189,29 @@ def forward(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, activation="co
 
 
 def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=None):
-    """Chain rule through sigma for ``L`` with ``dL/dC2 = dC2`` (rows = tokens).
+    """Chain rule through sigma for ``L`` with ``dL/d sigma = dC2`` (rows =
+    tokens).
 
     Recomputes the forward chain from ``H``.  Returns dH, domega1, dphi1, the
-    recomputed C2 and, for 2-layer forms, dM, domega2, dphi2 (None otherwise).
+    recomputed sigma(H) ("out") and, for 2-layer forms, dM, domega2, dphi2
+    (None otherwise; stacked [2, ...] for the 3-layer form).
     """
     f, layers = ACTIVATIONS[activation]
     dC2 = _f64(dC2)
     H = _f64(H)
     w1 = _f64(omega1)
     fw = branch_forward(H, activation, omega1, phi1, M, omega2, phi2)
-    out = {"dM": None, "domega2": None, "dphi2": None, "C2": fw["C2"]}
-    if layers == 2:
+    out = {"dM": None, "domega2": None, "dphi2": None, "out": fw["out"]}
+    if layers == 3:
+        # the third layer first; dC2 becomes the gradient of the middle C2
+        (M, omega2, phi2), (M3, w3, p3) = _third_layer(M, omega2, phi2)
+        dA3 = activation_slope(f, fw["A3"]) * dC2    # C3 = f(A3)
+        domega3 = np.sum(dA3 * fw["H3"], axis=0)     # A3 = w3 (.) H3 + p3
+        dphi3 = np.sum(dA3, axis=0)
+        dH3 = dA3 * w3
+        dM3 = fw["C2"].T @ dH3                       # H3 = C2 @ M'
+        dC2 = dH3 @ M3.T
+    if layers >= 2:
         dA2 = activation_slope(f, fw["A2"]) * dC2    # C2 = f(A2)
         out["domega2"] = np.sum(dA2 * fw["H2"], axis=0)   # A2 = w2 (.) H2 + p2
         out["dphi2"] = np.sum(dA2, axis=0)
@@ -185,6 +224,10 @@ def branch_backward(dC2, H, activation, omega1, phi1, M=None, omega2=None, phi2=
     out["domega1"] = np.sum(dA1 * H, axis=0)         # A1 = w1 (.) H + p1
     out["dphi1"] = np.sum(dA1, axis=0)
     out["dH"] = dA1 * w1
+    if layers == 3:
+        out["dM"] = np.stack([out["dM"], dM3])
+        out["domega2"] = np.stack([out["domega2"], domega3])
+        out["dphi2"] = np.stack([out["dphi2"], dphi3])
     return out
 
 
@@ -217,7 +260,7 @@ def backward(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up,
     cb = branch_backward(dC2, H, activation, omega1, phi1, M, omega2, phi2)
     dH = cb["dH"]
     out = {
-        "dW_up": cb["C2"].T @ dy,
+        "dW_up": cb["out"].T @ dy,
         "dW_down": x.T @ dH,                     # H = x @ W_down
         "db": np.sum(dy, axis=0),
         "dM": cb["dM"],
@@ -261,11 +304,14 @@ def branch_param_shapes(d_in, d_out, r):
 # g r .. g r + r - 1 and W_up's row block g ([G r, d_out / G]).
 
 
-def _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g):
+def _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g, layers=2):
     r, dg = R // G, d_out // G
     rs = slice(g * r, (g + 1) * r)
-    pick = lambda v: None if v is None else _f64(v)[rs]
-    Mg = None if M is None else (_f64(M) if G == 1 else _f64(M)[g])
+    pick = lambda v: None if v is None else _f64(v)[..., rs]     # stacked [2, R] vectors too
+    if M is None or G == 1:
+        Mg = _f64(M)
+    else:
+        Mg = _f64(M)[:, g] if layers == 3 else _f64(M)[g]       # [2, G, r, r] or [G, r, r]
     return (slice(g * dg, (g + 1) * dg), _f64(W_down)[:, rs], pick(omega1), pick(phi1), Mg, pick(omega2),
             pick(phi2), _f64(W_up)[rs])
 
@@ -278,7 +324,8 @@ def forward_grouped(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, groups
     G, d_out, R = int(groups), W.shape[1], _f64(W_down).shape[1]
     Ys = []
     for g in range(G):
-        cs, Dg, w1, p1, Mg, w2, p2, Ug = _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g)
+        cs, Dg, w1, p1, Mg, w2, p2, Ug = _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g,
+                                                      ACTIVATIONS[activation][1])
         Y, _ = forward(x, W[:, cs], None if b is None else _f64(b)[cs], Dg, w1, p1, Mg, w2, p2, Ug,
                        activation=activation)
         Ys.append(Y)
@@ -290,21 +337,24 @@ def backward_grouped(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, grou
     """Gradients of L = sum(dy * Y) for the grouped layer: each block's
     backward on its columns of dy; dx, which every block reaches through x,
     is the sum of the blocks' dx, every other gradient is the blocks'
-    gradients side by side (dM stacked [G, r, r], or [r, r] for G = 1)."""
+    gradients side by side (dM stacked [G, r, r], or [r, r] for G = 1; for
+    the 3-layer form [2, G, r, r] and domega2, dphi2 [2, G r])."""
     W, dy = _f64(W), _f64(dy)
     G, d_out, R = int(groups), W.shape[1], _f64(W_down).shape[1]
+    layers = ACTIVATIONS[activation][1]
     parts = []
     for g in range(G):
-        cs, Dg, w1, p1, Mg, w2, p2, Ug = _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g)
+        cs, Dg, w1, p1, Mg, w2, p2, Ug = _group_views(G, d_out, R, W_down, omega1, phi1, M, omega2, phi2, W_up, g,
+                                                      layers)
         parts.append(backward(dy[:, cs], x, W[:, cs], Dg, w1, p1, Mg, w2, p2, Ug, dx_rows=dx_rows,
                               dW_rows=dW_rows, activation=activation))
     cat = lambda k, ax: None if parts[0][k] is None else np.concatenate([q[k] for q in parts], axis=ax)
     out = {"dx": sum(q["dx"] for q in parts), "dW": cat("dW", 1), "db": cat("db", 0),
            "dW_down": cat("dW_down", 1), "dW_up": cat("dW_up", 0)}
     for k in ("domega1", "dphi1", "domega2", "dphi2"):
-        out[k] = cat(k, 0)
+        out[k] = cat(k, -1)
     if parts[0]["dM"] is None:
         out["dM"] = None
     else:
-        out["dM"] = parts[0]["dM"] if G == 1 else np.stack([q["dM"] for q in parts])
+        out["dM"] = parts[0]["dM"] if G == 1 else np.stack([q["dM"] for q in parts], axis=1 if layers == 3 else 0)
     return out

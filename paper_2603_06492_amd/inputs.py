@@ -85,10 +85,13 @@ def draw_projection(name: str, T: int, d_in: int, d_out: int, r: int,
                     dtype: str = "bf16", seed: int = 0, *,
                     w_var: Optional[float] = None, d_var: Optional[float] = None,
                     m_var: Optional[float] = None, u_var: Optional[float] = None,
-                    bias_std: float = 0.0, groups: int = 1) -> Projection:
+                    bias_std: float = 0.0, groups: int = 1, layers: int = 2) -> Projection:
     """Seeded inputs of one layer.  ``groups`` G > 1 gives the grouped layout:
     W_down [d_in, G r], M [G, r, r], frequency / phase vectors [G r] and
-    W_up [G r, d_out / G]; G = 1 draws exactly the single-layer arrays."""
+    W_up [G r, d_out / G]; G = 1 draws exactly the single-layer arrays.
+    ``layers`` = 3 (the 3-layer CosNet) draws the mixing matrices and the
+    second frequency / phase pair stacked: M [2, r, r] ([2, G, r, r]),
+    omega2 and phi2 [2, G r], in the same draw order."""
     if dtype not in ("bf16", "f32"):
         raise ValueError(f"dtype must be 'bf16' or 'f32', got {dtype!r}")
     w_var = 1.0 / d_in if w_var is None else w_var
@@ -110,11 +113,15 @@ def draw_projection(name: str, T: int, d_in: int, d_out: int, r: int,
         raise ValueError(f"d_out ({d_out}) must split into {G} groups")
     R = G * r
 
-    def freq():
-        return (f32(1.0) + f32(0.1) * rng.standard_normal(R, dtype=f32)).astype(f32)
+    def freq(n=None):
+        shape = R if n is None else (n, R)
+        return (f32(1.0) + f32(0.1) * rng.standard_normal(shape, dtype=f32)).astype(f32)
 
-    def phase():
-        return (rng.random(R, dtype=f32) * f32(2.0 * math.pi)).astype(f32)
+    def phase(n=None):
+        shape = R if n is None else (n, R)
+        return (rng.random(shape, dtype=f32) * f32(2.0 * math.pi)).astype(f32)
+
+    stack = (2,) if layers == 3 else ()
 
     a = {}
     a["x"] = normal((T, d_in), 1.0)
@@ -123,9 +130,9 @@ def draw_projection(name: str, T: int, d_in: int, d_out: int, r: int,
     a["W_down"] = normal((d_in, R), d_var)
     a["omega1"] = freq()
     a["phi1"] = phase()
-    a["M"] = normal((r, r) if G == 1 else (G, r, r), m_var)
-    a["omega2"] = freq()
-    a["phi2"] = phase()
+    a["M"] = normal(stack + ((r, r) if G == 1 else (G, r, r)), m_var)
+    a["omega2"] = freq(2 if layers == 3 else None)
+    a["phi2"] = phase(2 if layers == 3 else None)
     a["W_up"] = normal((R, d_out // G), u_var)
     a["dy"] = normal((T, d_out), 1.0)
     if dtype == "bf16":

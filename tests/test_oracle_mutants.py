@@ -32,7 +32,7 @@ MUTATIONS = {
     "dH_missing_omega1": ("out[\"dH\"] = dA1 * w1", "out[\"dH\"] = dA1"),
     "dH2_missing_omega2": ("dH2 = dA2 * _f64(omega2)", "dH2 = dA2"),
     "dx_missing_branch": ("out[\"dx\"] = dy @ W.T + dH @ D.T", "out[\"dx\"] = dy @ W.T"),
-    "dW_up_uses_cos_argument": ("\"dW_up\": cb[\"C2\"].T @ dy", "\"dW_up\": np.cos(cb[\"C2\"]).T @ dy"),
+    "dW_up_uses_cos_argument": ("\"dW_up\": cb[\"out\"].T @ dy", "\"dW_up\": np.cos(cb[\"out\"]).T @ dy"),
     # activation variants
     "tanh_slope_not_squared": ("return 1.0 - np.tanh(a) ** 2", "return 1.0 - np.tanh(a)"),
     "tanh_value_is_sin": ("return np.tanh(a)\n", "return np.sin(a)\n"),
@@ -47,10 +47,19 @@ MUTATIONS = {
                              "from scipy.special import erf\n    return 0.5 * (1.0 + erf(a / np.sqrt(2.0)))"),
     "one_layer_chain_mixes": ("        dC1 = dC2                                    # C2 = C1",
                               "        dC1 = 2.0 * dC2"),
+    # the 3-layer CosNet
+    "third_layer_phase_dropped": ("A3 = H3 * w3 + p3", "A3 = H3 * w3"),
+    "third_layer_reuses_first_matrix": ("H3 = C2 @ M3", "H3 = C2 @ _f64(M)"),
+    "third_layer_output_ignored": ("fw.update(H3=H3, A3=A3, C3=C3, out=C3)", "fw.update(H3=H3, A3=A3, C3=C3)"),
+    "third_layer_gradient_skips_mixing": ("dC2 = dH3 @ M3.T", "dC2 = dH3"),
+    "third_layer_dM_from_C1": ("dM3 = fw[\"C2\"].T @ dH3", "dM3 = fw[\"C1\"].T @ dH3"),
+    "third_layer_frequency_gradient_without_H3": ("domega3 = np.sum(dA3 * fw[\"H3\"], axis=0)",
+                                                  "domega3 = np.sum(dA3, axis=0)"),
     # grouped layers
     "grouped_dx_last_block_only": ('out = {"dx": sum(q["dx"] for q in parts),', 'out = {"dx": parts[-1]["dx"],'),
     "grouped_rank_slice_fixed": ("rs = slice(g * r, (g + 1) * r)", "rs = slice(0, r)"),
-    "grouped_first_M_only": ("(_f64(M) if G == 1 else _f64(M)[g])", "(_f64(M) if G == 1 else _f64(M)[0])"),
+    "grouped_first_M_only": ("Mg = _f64(M)[:, g] if layers == 3 else _f64(M)[g]",
+                             "Mg = _f64(M)[:, 0] if layers == 3 else _f64(M)[0]"),
     "grouped_column_block_shifted": ("return (slice(g * dg, (g + 1) * dg),", "return (slice((G - 1 - g) * dg, (G - g) * dg),"),
 }
 
@@ -105,9 +114,9 @@ def _battery_passes(mod):
                 got = Y if k == "y" else g[k]
                 if not np.allclose(got, _eval(v), rtol=0, atol=1e-12):
                     return False
-    p = {k: v.astype(np.float64) for k, v in
-         inp.draw_projection("t", 4, 5, 6, 3, "f32", 21, bias_std=0.5).arrays.items()}
     for act, (_, layers) in sorted(good.ACTIVATIONS.items()):
+        p = {k: v.astype(np.float64) for k, v in
+             inp.draw_projection("t", 4, 5, 6, 3, "f32", 21, bias_std=0.5, layers=layers).arrays.items()}
         g = mod.backward(p["dy"], p["x"], p["W"], p["W_down"], p["omega1"], p["phi1"], p["M"],
                          p["omega2"], p["phi2"], p["W_up"], activation=act)
 
@@ -118,7 +127,7 @@ def _battery_passes(mod):
 
         pairs = {"x": "dx", "W": "dW", "b": "db", "W_down": "dW_down", "W_up": "dW_up",
                  "omega1": "domega1", "phi1": "dphi1"}
-        if layers == 2:
+        if layers >= 2:
             pairs.update({"M": "dM", "omega2": "domega2", "phi2": "dphi2"})
         for pn, gn in pairs.items():
             for idx in np.ndindex(p[pn].shape):

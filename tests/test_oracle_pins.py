@@ -45,8 +45,8 @@ def _bwd(p, **kw):
                            p["M"], p["omega2"], p["phi2"], p["W_up"], **kw)
 
 
-def _tiny(seed=3, T=5, d_in=7, d_out=6, r=3):
-    p = inp.draw_projection("tiny", T, d_in, d_out, r, "f32", seed, bias_std=0.5)
+def _tiny(seed=3, T=5, d_in=7, d_out=6, r=3, layers=2):
+    p = inp.draw_projection("tiny", T, d_in, d_out, r, "f32", seed, bias_std=0.5, layers=layers)
     return {k: v.astype(np.float64) for k, v in p.arrays.items()}
 
 
@@ -349,9 +349,10 @@ def test_activation_hand_examples(ex):
 
 @pytest.mark.parametrize("act", ACTS)
 def test_activation_gradients_match_central_differences(act):
-    p = _tiny(seed=17)
+    layers = oracle.ACTIVATIONS[act][1]
+    p = _tiny(seed=17, layers=layers)
     g = _bwd_a(p, act)
-    two = oracle.ACTIVATIONS[act][1] == 2
+    two = layers >= 2
 
     def loss(q):
         return float(np.sum(q["dy"] * _fwd_a(q, act)[0]))
@@ -380,19 +381,25 @@ def test_activation_gradients_match_central_differences(act):
 @pytest.mark.parametrize("act", ACTS)
 def test_activation_gradients_match_torch_autograd(act):
     """An independent torch formulation (torch's own tanh, leaky_relu with
-    slope 0.01, exact gelu, cos), differentiated by autograd in float64."""
+    slope 0.01, exact gelu, cos), differentiated by autograd in float64.  The
+    3-layer form applies the stacked second matrix and vectors once more."""
     torch = pytest.importorskip("torch")
     F = torch.nn.functional
     fn = {"cos": torch.cos, "tanh": torch.tanh, "leaky_relu": lambda a: F.leaky_relu(a, 0.01),
           "gelu": lambda a: F.gelu(a)}[oracle.ACTIVATIONS[act][0]]
-    two = oracle.ACTIVATIONS[act][1] == 2
-    p = _tiny(seed=23, T=9, d_in=16, d_out=24, r=8)
+    layers = oracle.ACTIVATIONS[act][1]
+    two = layers >= 2
+    p = _tiny(seed=23, T=9, d_in=16, d_out=24, r=8, layers=layers)
     t = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True) for k, v in p.items()}
     h = t["x"] @ t["W_down"]
     c = fn(t["omega1"] * h + t["phi1"])
-    if two:
+    if layers == 2:
         h2 = (c[:, :, None] * t["M"][None, :, :]).sum(dim=1)
         c = fn(t["omega2"] * h2 + t["phi2"])
+    elif layers == 3:
+        for l in range(2):
+            h2 = (c[:, :, None] * t["M"][l][None, :, :]).sum(dim=1)
+            c = fn(t["omega2"][l] * h2 + t["phi2"][l])
     y = t["x"] @ t["W"] + t["b"] + c @ t["W_up"]
     (y * t["dy"]).sum().backward()
     Y, _ = _fwd_a(p, act)
@@ -484,28 +491,32 @@ def test_slopes_keep_relative_accuracy_in_the_tails():
 
 # ------------------------------------------------------------ grouped layers --
 
-def _block_diagonal(p, G):
+def _block_diagonal(p, G, layers=2):
     """The grouped layer's parameters as one rank-G r layer: M and W_up block
-    diagonal (zeros off the blocks), everything else as is."""
+    diagonal (zeros off the blocks), everything else as is.  For the 3-layer
+    form each of the two stacked mixing matrices is made block diagonal."""
     R = p["W_down"].shape[1]
     r, dg = R // G, p["W"].shape[1] // G
-    Mb = np.zeros((R, R))
+    L = 2 if layers == 3 else 1
+    Mb = np.zeros((L, R, R))
     Ub = np.zeros((R, G * dg))
     for g in range(G):
-        Mb[g * r:(g + 1) * r, g * r:(g + 1) * r] = p["M"][g]
+        for l in range(L):
+            Mb[l, g * r:(g + 1) * r, g * r:(g + 1) * r] = p["M"][l, g] if layers == 3 else p["M"][g]
         Ub[g * r:(g + 1) * r, g * dg:(g + 1) * dg] = p["W_up"][g * r:(g + 1) * r]
-    return Mb, Ub
+    return (Mb if layers == 3 else Mb[0]), Ub
 
 
-@pytest.mark.parametrize("act", ["cosnet", "gelu_m", "tanh"])
+@pytest.mark.parametrize("act", ["cosnet", "gelu_m", "tanh", "cosnet3"])
 def test_grouped_layer_is_block_diagonal_single_layer(act):
     """G branches on G column blocks of one x equal one rank-G r branch whose
     M and W_up are block diagonal: same y, dx, dW, db, dW_down and vector
     gradients; dM and dW_up are the diagonal blocks of the single layer's."""
     G = 3
-    q = inp.draw_projection("grp", 7, 10, 3 * 6, 4, "f32", 43, bias_std=0.5, groups=G)
+    layers = oracle.ACTIVATIONS[act][1]
+    q = inp.draw_projection("grp", 7, 10, 3 * 6, 4, "f32", 43, bias_std=0.5, groups=G, layers=layers)
     p = {k: v.astype(np.float64) for k, v in q.arrays.items()}
-    Mb, Ub = _block_diagonal(p, G)
+    Mb, Ub = _block_diagonal(p, G, layers)
     args = (p["W_down"], p["omega1"], p["phi1"])
     Yg, Hg = oracle.forward_grouped(p["x"], p["W"], p["b"], *args, p["M"], p["omega2"], p["phi2"], p["W_up"], G,
                                     activation=act)
@@ -524,7 +535,11 @@ def test_grouped_layer_is_block_diagonal_single_layer(act):
     for g in range(G):
         np.testing.assert_allclose(gg["dW_up"][g * r:(g + 1) * r], gs["dW_up"][g * r:(g + 1) * r, g * dg:(g + 1) * dg],
                                    rtol=0, atol=1e-12)
-        if gs["dM"] is not None:
+        if gs["dM"] is not None and layers == 3:
+            for l in range(2):
+                np.testing.assert_allclose(gg["dM"][l, g], gs["dM"][l, g * r:(g + 1) * r, g * r:(g + 1) * r],
+                                           rtol=0, atol=1e-12)
+        elif gs["dM"] is not None:
             np.testing.assert_allclose(gg["dM"][g], gs["dM"][g * r:(g + 1) * r, g * r:(g + 1) * r], rtol=0, atol=1e-12)
 
 
@@ -564,3 +579,71 @@ def test_grouped_gradients_match_central_differences():
             qm[pn][idx] -= 1e-6
             fd[idx] = (loss(qp) - loss(qm)) / 2e-6
         assert np.max(np.abs(fd - g[gn])) <= 1e-6 * max(1.0, float(np.max(np.abs(g[gn])))), gn
+
+
+# ---------------------------------------------------- 3-layer CosNet -------
+# (Table 5, last row.)  Closed forms where the third layer degenerates.
+
+def _fwd3(p):
+    return _fwd_a(p, "cosnet3")
+
+
+def _bwd3(p):
+    return _bwd_a(p, "cosnet3")
+
+
+@pytest.mark.parametrize("which", ["M2", "omega3"])
+def test_three_layer_constant_third_input(which):
+    """The second mixing matrix, or the third frequency, at zero makes the
+    third layer's input constant: sigma = cos(p3) in every row, so y = x W +
+    b + cos(p3) W_up and every gradient below the third layer is exactly 0
+    (dM[0], dW_down, the first two frequency / phase pairs); with M' = 0 the
+    third frequency gets no gradient either (H3 = 0)."""
+    p = _tiny(seed=61, layers=3)
+    if which == "M2":
+        p["M"][1] = 0.0
+    else:
+        p["omega2"][1] = 0.0
+    Y, _ = _fwd3(p)
+    np.testing.assert_allclose(Y, p["x"] @ p["W"] + p["b"] + np.cos(p["phi2"][1]) @ p["W_up"], rtol=0, atol=1e-12)
+    g = _bwd3(p)
+    for k in ("dW_down", "domega1", "dphi1"):
+        assert np.all(g[k] == 0), k
+    assert np.all(g["dM"][0] == 0) and np.all(g["domega2"][0] == 0) and np.all(g["dphi2"][0] == 0)
+    dC3 = p["dy"] @ p["W_up"].T
+    np.testing.assert_allclose(g["dphi2"][1], np.sum(-np.sin(p["phi2"][1]) * dC3, axis=0), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(g["dx"], p["dy"] @ p["W"].T, rtol=0, atol=1e-12)
+    if which == "M2":
+        assert np.all(g["domega2"][1] == 0)
+
+
+def test_three_layer_evenness_of_the_last_cosine():
+    """(w3, p3) -> (-w3, -p3) leaves y and every gradient outside the third
+    pair unchanged and flips the sign of dw3 and dp3."""
+    p = _tiny(seed=67, layers=3)
+    q = {k: v.copy() for k, v in p.items()}
+    q["omega2"][1] *= -1.0
+    q["phi2"][1] *= -1.0
+    np.testing.assert_allclose(_fwd3(p)[0], _fwd3(q)[0], rtol=0, atol=1e-12)
+    a, b = _bwd3(p), _bwd3(q)
+    for k in ("dx", "dW", "dW_down", "dW_up", "domega1", "dphi1"):
+        np.testing.assert_allclose(a[k], b[k], rtol=0, atol=1e-12, err_msg=k)
+    np.testing.assert_allclose(a["dM"], b["dM"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(a["domega2"][0], b["domega2"][0], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(a["domega2"][1], -b["domega2"][1], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(a["dphi2"][1], -b["dphi2"][1], rtol=0, atol=1e-12)
+
+
+def test_three_layer_with_identity_tail_is_not_the_two_layer_form():
+    """The third layer is a real extra cosine: with M' = I, w3 = 1, p3 = 0
+    the 3-layer output is cos(C2), the cosine of the 2-layer output."""
+    p = _tiny(seed=71, layers=3)
+    r = p["M"].shape[-1]
+    p["M"][1] = np.eye(r)
+    p["omega2"][1] = 1.0
+    p["phi2"][1] = 0.0
+    q = dict(p, M=p["M"][0], omega2=p["omega2"][0], phi2=p["phi2"][0])
+    H = p["x"] @ p["W_down"]
+    c2 = oracle.branch_forward(H, "cosnet", q["omega1"], q["phi1"], q["M"], q["omega2"], q["phi2"])["out"]
+    c3 = oracle.branch_forward(H, "cosnet3", p["omega1"], p["phi1"], p["M"], p["omega2"], p["phi2"])["out"]
+    np.testing.assert_allclose(c3, np.cos(c2), rtol=0, atol=1e-12)
