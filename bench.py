@@ -40,17 +40,18 @@ PEAK_F32 = 157.3e12  # dense fp32 MFMA, MI355X
 METRIC = "NOBLE linear fwd+bwd TFLOP/s, % bf16 MFMA peak, overhead vs plain GEMM"
 
 
-def flop_alg(T, d_in, d_out, r, mixing=True, groups=1):
-    """Forward + backward FLOPs: 6 T [d_in d_out + r (G d_in + d_out) + G r^2]
-    for G groups of rank r (each group maps d_in to d_out / G)."""
+def flop_alg(T, d_in, d_out, r, mixing=1, groups=1):
+    """Forward + backward FLOPs: 6 T [d_in d_out + r (G d_in + d_out) + m G r^2]
+    for G groups of rank r (each group maps d_in to d_out / G) with m = mixing
+    r x r matrices per group (0, 1, or 2 for the 3-layer CosNet)."""
     G = groups
-    return 6.0 * T * (d_in * d_out + r * (G * d_in + d_out) + (G * r * r if mixing else 0))
+    return 6.0 * T * (d_in * d_out + r * (G * d_in + d_out) + int(mixing) * G * r * r)
 
 
-def branch_floor(d_in, d_out, r, mixing=True, groups=1):
+def branch_floor(d_in, d_out, r, mixing=1, groups=1):
     """Branch FLOPs over the main product's."""
     G = groups
-    return (r * (G * d_in + d_out) + (G * r * r if mixing else 0)) / (d_in * d_out)
+    return (r * (G * d_in + d_out) + int(mixing) * G * r * r) / (d_in * d_out)
 
 
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "wgrad_ffn_up_T32768_traffic.md")
@@ -141,7 +142,7 @@ def cpu_baseline(workload: str, samples, gpu_rows, budget_s: float = 12.0, activ
     import oracle  # test infrastructure: only this leg of the bench uses it
     from paper_2603_06492_amd import inputs as inp
     from paper_2603_06492_amd import noble
-    mixing = noble.two_layers(activation)
+    mixing = noble.layers(activation) - 1   # mixing matrices per group
     kw = dict(activation=activation)
     try:
         from threadpoolctl import threadpool_info
@@ -205,7 +206,7 @@ def main():
     ap.add_argument("--workload", default="llm1p5b_stack4_r128")
     ap.add_argument("--activation", default="cosnet",
                     help="bottleneck activation: cosnet (default), cos, tanh, tanh_m, leaky_relu, "
-                         "leaky_relu_m, gelu, gelu_m")
+                         "leaky_relu_m, gelu, gelu_m, cosnet3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-blas", action="store_true",
                     help="skip the hipBLASLt (torch.mm) context timings of the plain products")
@@ -228,7 +229,7 @@ def main():
     from paper_2603_06492_amd import noble
     from paper_2603_06492_amd.runner import DeviceProblem
 
-    mixing = noble.two_layers(args.activation)
+    mixing = noble.layers(args.activation) - 1   # mixing matrices per group
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
@@ -242,7 +243,7 @@ def main():
     sample_rows = min(wl["T"], 8192)
     xsrc = inp.workload_x_source(args.workload)
     for i in range(len(shapes)):
-        p = inp.draw_workload_projection(args.workload, i)
+        p = inp.draw_workload_projection(args.workload, i, layers=max(2, mixing + 1))
         dp = DeviceProblem(p, activation=args.activation, x_from=probs[xsrc[i]] if xsrc[i] != i else None)
         probs.append(dp)
         plain.append(DeviceProblem(p, branch=False, inputs_from=dp))
@@ -337,10 +338,10 @@ def main():
     # sums).  The library records a pair of HIP events on its stream right
     # before and after that launch (noble_profile_next_wgrad); `achieved` is
     # the launch's algorithmic FLOPs, 2 T (d_in d_out + d_in R + r d_out +
-    # G r^2), over the mean of those launch durations.
+    # m G r^2), over the mean of those launch durations.
     def wgrad_flops(dp):
         T, di, do, r, G = dp.p.T, dp.p.d_in, dp.p.d_out, dp.p.r, dp.G
-        return 2.0 * T * (di * do + G * r * di + r * do + (G * r * r if mixing else 0))
+        return 2.0 * T * (di * do + G * r * di + r * do + mixing * G * r * r)
     dom = max(probs, key=wgrad_flops)
     hev = HipEvents()
     evs = [(hev.create(), hev.create()) for _ in range(args.roofline_launches)]

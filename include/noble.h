@@ -20,6 +20,12 @@
  * LeakyReLU (negative slope 0.01) or GELU (exact, a Phi(a)), each either in
  * the two-application form above (f in place of cos, with M between) or as
  * one application C2 = f(H (.) omega1 + phi1), which has no M, omega2, phi2.
+ * A third form, the 3-layer CosNet (last row of Table 5; Sec. 5), applies a
+ * third cosine after a second mixing matrix M':
+ *   C3 = cos((C2 M') (.) omega3 + phi3),   y = x W + b + C3 W_up
+ * and stores its parameters stacked with the second layer's: M holds
+ * [M ; M'] as [2, r, r], omega2 holds [omega2 ; omega3] and phi2
+ * [phi2 ; phi3] as [2, r], and so do dM, domega2 and dphi2.
  *
  * Conventions shared by every call
  * --------------------------------
@@ -38,7 +44,8 @@
  *    throughout on the f32 path.
  *  - Shapes: 0 <= T <= 2^31 - 4096; 8 <= d_in, d_out <= 2^20, multiples of
  *    8; r = 0 (plain linear: every branch pointer is ignored and may be NULL)
- *    or 8 <= r <= 256 (bf16) / 128 (f32) with r a multiple of 8.  Each
+ *    or 8 <= r <= 256 (bf16) / 128 (f32, and the 3-layer form) with r a
+ *    multiple of 8.  Each
  *    matrix product of a call must also fit one dispatch (2^32 - 1
  *    work-items): at most 8388607 output tiles of 256 x 256 (bf16) or
  *    16777215 of 128 x 128 (f32) in y = x W, dx and dW (plus, for dW, the
@@ -51,6 +58,7 @@
  *    Sec. 4.1.1).  With d_g = d_out / G (a multiple of 8) and R = G r:
  *      W_down [d_in, R]   (group g: columns g r .. g r + r - 1)
  *      M [G, r, r], omega1/phi1/omega2/phi2 [R]   (group g: entries g r ..)
+ *      (3-layer form: M [2, G, r, r], omega2/phi2 [2, R])
  *      W_up [R, d_g]      (group g: rows g r .., mapping onto y[:, g d_g ..])
  *    and the gradients have the same shapes.  G = 1 is the single layer.
  *  - Argument checking is complete before any HIP call: on any error the call
@@ -99,7 +107,8 @@ typedef enum noble_activation {
     NOBLE_ACT_LEAKY_RELU = 4,
     NOBLE_ACT_LEAKY_RELU_M = 5,
     NOBLE_ACT_GELU = 6,
-    NOBLE_ACT_GELU_M = 7
+    NOBLE_ACT_GELU_M = 7,
+    NOBLE_ACT_COSNET3 = 8       /* cos(w3 (.) (C2 M') + p3), C2 of COSNET; r <= 128 */
 } noble_activation;
 
 /* Problem description.  `dtype` holds a noble_dtype value and `activation`
@@ -125,7 +134,8 @@ typedef struct noble_linear_desc {
  *                  (split-K partial sums of dW), whenever scratch_bytes > 0.
  * Either output pointer may be NULL.  Returns NOBLE_ERR_NULL_ARG (desc NULL),
  * NOBLE_ERR_BAD_SHAPE, NOBLE_ERR_BAD_DTYPE or NOBLE_ERR_BAD_ACTIVATION;
- * makes no HIP call.  The sizes do not depend on the activation. */
+ * makes no HIP call.  The 3-layer form's scratch is larger; the other
+ * activations share one size. */
 noble_status noble_linear_workspace_size(const noble_linear_desc* desc,
                                          size_t* reserve_bytes,
                                          size_t* scratch_bytes);
@@ -148,7 +158,7 @@ noble_status noble_linear_fwd_scratch_size(const noble_linear_desc* desc,
  * reserve may be NULL: an inference-only forward that keeps no H (the
  * branch's permanent inference cost, Sec. 6); no backward can follow it.
  * With a one-application activation, M, omega2 and phi2 are not read and
- * may be NULL. */
+ * may be NULL; the 3-layer form reads them in their stacked shapes. */
 noble_status noble_linear_fwd(const noble_linear_desc* desc,
                               const void* x, const void* W, const float* b,
                               const void* W_down,
@@ -190,7 +200,8 @@ noble_status noble_linear_fwd_static(const noble_linear_desc* desc,
  * Every gradient buffer is overwritten (not accumulated):
  *   dx [T, d_in] (storage dtype), dW [d_in, d_out], db [d_out] (nullable =
  *   not computed), dW_down [d_in, r], dM [r, r], dW_up [r, d_out],
- *   domega1, dphi1, domega2, dphi2 [r]  (all float32).
+ *   domega1, dphi1, domega2, dphi2 [r]  (all float32; the 3-layer form's
+ *   dM [2, r, r] and domega2, dphi2 [2, r]).
  * With T = 0 the parameter gradients are set to zero.  db and the four
  * omega / phi gradients are summed over tokens with float atomics, so they
  * may differ in the last bits between runs; dx, dW, dW_down, dM and dW_up
@@ -270,7 +281,8 @@ noble_status noble_lr_multipliers(const noble_linear_desc* desc,
  *   M ~ U(-sqrt(3 / r), sqrt(3 / r))  (Xavier uniform, fan_in = fan_out = r),
  *   W_up ~ N(0, (alpha / sqrt(r))^2).
  * Storage tensors (W, W_down, M, W_up) in desc->dtype, the rest float32;
- * shapes as in noble_linear_fwd.  A NULL pointer skips that tensor.
+ * shapes as in noble_linear_fwd (the 3-layer form's M' and omega3, phi3 are
+ * drawn like M, omega2, phi2, as the second halves of those tensors).  A NULL pointer skips that tensor.
  * Random numbers: Philox4x32-10 (Salmon et al., SC 2011) keyed by `seed`
  * (key = low, high 32 bits); element e (row-major) of tensor t takes the
  * block at counter (e mod 2^32, e / 2^32, t, 0), t = 0 W, 1 W_down,
@@ -295,7 +307,7 @@ const char* noble_status_string(int status);
 /* ABI version of this header (bumped on incompatible changes). */
 int noble_abi_version(void);
 
-#define NOBLE_ABI_VERSION 4
+#define NOBLE_ABI_VERSION 5
 
 #ifdef __cplusplus
 }

@@ -83,12 +83,17 @@ def to_bf16(a):
     return u.astype(np.uint32).view(np.float32)
 
 
-def init_values(d_in, d_out, r, seed, dtype="bf16", recipe=None, groups=1):
+def init_values(d_in, d_out, r, seed, dtype="bf16", recipe=None, groups=1, layers=2):
     """Initial values of every parameter, as float32 arrays (storage tensors
     rounded to bf16 when ``dtype`` is "bf16").  ``groups`` G > 1: W_down
     [d_in, G r], M [G, r, r], the vectors [G r], W_up [G r, d_out / G], each
-    tensor drawn as one row-major stream."""
+    tensor drawn as one row-major stream.  ``layers`` = 3 (the 3-layer CosNet
+    of Table 5): M is [2, (G,) r, r] and omega2, phi2 are [2, G r], the second
+    mixing matrix and the third frequency / phase drawn as the continuation
+    of the same streams (the paper gives no initialisation for them; this
+    reading takes the second layer's)."""
     G = groups
+    n = 2 if layers == 3 else 1
     R, dog = G * r, d_out // G
     rc = dict(DEFAULTS, **(recipe or {}))
     store = (lambda a: to_bf16(a.astype(np.float32))) if dtype == "bf16" else (lambda a: a.astype(np.float32))
@@ -101,14 +106,18 @@ def init_values(d_in, d_out, r, seed, dtype="bf16", recipe=None, groups=1):
         db = 1.0 / np.sqrt(d_in)
         mb = np.sqrt(6.0 / (r + r))
         out["W_down"] = store(draw_uniform(seed, TENSOR_IDS["W_down"], d_in * R, -db, db)).reshape(d_in, R)
-        M = store(draw_uniform(seed, TENSOR_IDS["M"], G * r * r, -mb, mb))
-        out["M"] = M.reshape(r, r) if G == 1 else M.reshape(G, r, r)
+        M = store(draw_uniform(seed, TENSOR_IDS["M"], n * G * r * r, -mb, mb))
+        mshape = (r, r) if G == 1 else (G, r, r)
+        out["M"] = M.reshape(((n,) if n > 1 else ()) + mshape)
         out["W_up"] = store(draw_normal(seed, TENSOR_IDS["W_up"], R * dog, rc["alpha"] / np.sqrt(r))
                             ).reshape(R, dog)
         for i in (1, 2):
-            out[f"omega{i}"] = draw_uniform(seed, TENSOR_IDS[f"omega{i}"], R, rc["omega_min"],
-                                            rc["omega_max"]).astype(np.float32)
-            out[f"phi{i}"] = draw_normal(seed, TENSOR_IDS[f"phi{i}"], R, rc["phi_std"]).astype(np.float32)
+            k = n if i == 2 else 1
+            vshape = (k, R) if k > 1 else (R,)
+            out[f"omega{i}"] = draw_uniform(seed, TENSOR_IDS[f"omega{i}"], k * R, rc["omega_min"],
+                                            rc["omega_max"]).astype(np.float32).reshape(vshape)
+            out[f"phi{i}"] = draw_normal(seed, TENSOR_IDS[f"phi{i}"], k * R,
+                                         rc["phi_std"]).astype(np.float32).reshape(vshape)
     return out
 
 

@@ -35,13 +35,15 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 noble_status check_desc(const noble_linear_desc* d) {
     if (!d) return NOBLE_ERR_NULL_ARG;
     if (d->dtype != NOBLE_BF16 && d->dtype != NOBLE_F32) return NOBLE_ERR_BAD_DTYPE;
-    if (d->activation < NOBLE_ACT_COSNET || d->activation > NOBLE_ACT_GELU_M) return NOBLE_ERR_BAD_ACTIVATION;
+    if (d->activation < NOBLE_ACT_COSNET || d->activation > NOBLE_ACT_COSNET3) return NOBLE_ERR_BAD_ACTIVATION;
     if (d->reserved != 0) return NOBLE_ERR_BAD_SHAPE;
     if (d->T < 0 || d->T > kMaxTokens) return NOBLE_ERR_BAD_SHAPE;
     if (d->d_in < 8 || d->d_in % 8 || d->d_in > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
     if (d->d_out < 8 || d->d_out % 8 || d->d_out > kMaxDim) return NOBLE_ERR_BAD_SHAPE;
     const int64_t rmax = d->dtype == NOBLE_BF16 ? 256 : 128;
     if (d->r < 0 || (d->r > 0 && (d->r < 8 || d->r % 8 || d->r > rmax))) return NOBLE_ERR_BAD_SHAPE;
+    // the 3-layer form keeps both mixing matrices in LDS: r <= 128
+    if (d->activation == NOBLE_ACT_COSNET3 && d->r > 128) return NOBLE_ERR_BAD_SHAPE;
     if (d->groups < 0 || d->groups > kMaxGroups) return NOBLE_ERR_BAD_SHAPE;
     const int64_t G = d->groups > 0 ? d->groups : 1;
     if (d->d_out % (8 * G)) return NOBLE_ERR_BAD_SHAPE;
@@ -71,22 +73,31 @@ Act act_fn(int a) {
         default: return Act::Cos;
     }
 }
-bool act_two_layers(int a) {
-    return a == NOBLE_ACT_COSNET || a == NOBLE_ACT_TANH_M || a == NOBLE_ACT_LEAKY_RELU_M || a == NOBLE_ACT_GELU_M;
+// Applications of the activation: 1 (single), 2 (with M between, the
+// CosNet), 3 (the 3-layer CosNet, M and M').
+int act_layers(int a) {
+    if (a == NOBLE_ACT_COSNET3) return 3;
+    return a == NOBLE_ACT_COSNET || a == NOBLE_ACT_TANH_M || a == NOBLE_ACT_LEAKY_RELU_M || a == NOBLE_ACT_GELU_M
+               ? 2
+               : 1;
 }
+bool act_two_layers(int a) { return act_layers(a) >= 2; }
 
-// Calls fn.template operator()<F, L2>() for the activation `a`.
+// Calls fn.template operator()<F, L>() for the activation `a` (L its
+// applications).
 template <typename Fn>
 noble_status with_act(int a, Fn&& fn) {
-    const bool l2 = act_two_layers(a);
+    const int L = act_layers(a);
     switch (act_fn(a)) {
-        case Act::Cos: return l2 ? fn.template operator()<Act::Cos, true>() : fn.template operator()<Act::Cos, false>();
+        case Act::Cos:
+            return L == 3 ? fn.template operator()<Act::Cos, 3>()
+                          : (L == 2 ? fn.template operator()<Act::Cos, 2>() : fn.template operator()<Act::Cos, 1>());
         case Act::Tanh:
-            return l2 ? fn.template operator()<Act::Tanh, true>() : fn.template operator()<Act::Tanh, false>();
+            return L == 2 ? fn.template operator()<Act::Tanh, 2>() : fn.template operator()<Act::Tanh, 1>();
         case Act::Leaky:
-            return l2 ? fn.template operator()<Act::Leaky, true>() : fn.template operator()<Act::Leaky, false>();
+            return L == 2 ? fn.template operator()<Act::Leaky, 2>() : fn.template operator()<Act::Leaky, 1>();
         case Act::Gelu:
-            return l2 ? fn.template operator()<Act::Gelu, true>() : fn.template operator()<Act::Gelu, false>();
+            return L == 2 ? fn.template operator()<Act::Gelu, 2>() : fn.template operator()<Act::Gelu, 1>();
     }
     return NOBLE_ERR_BAD_ACTIVATION;
 }
@@ -111,9 +122,11 @@ int proj_jobs(const noble_linear_desc* d) { return ngroups(d) * rank_blocks(d); 
 // then the backward's:
 //  - C1, dH2, dH [T, hl R] storage type, hl = 2 on the bf16 path (each value
 //    as a high + low bf16 pair, see branch_bwd_kernel), 1 on the float32
-//    path;
+//    path; the 3-layer form adds the middle C2 and dH3 alike;
 //  - bf16: the copies of the frequency / phase gradients;
 //  - the float32 split-K partials of the weight-gradient products.
+// The 3-layer form's extra regions and products make its sizes larger than
+// the other activations' (which share one size).
 int hilo(const noble_linear_desc* d) { return d->dtype == NOBLE_BF16 ? 2 : 1; }
 size_t scratch_region(const noble_linear_desc* d) {
     return align_up((size_t)d->T * rank_total(d) * elt_size(d));
@@ -127,18 +140,23 @@ size_t partial_need(const noble_linear_desc* d) {
     const int s = std::max(proj_split(d->T, d->d_in, J), proj_split(d->T, group_dout(d), J));
     return align_up((size_t)s * d->T * rank_total(d) * 4);
 }
-// bf16 backward: kChainCopies copies of the four frequency / phase gradient
-// vectors, [4][kChainCopies][R] float32.
+bool three_layers(const noble_linear_desc* d) { return d->activation == NOBLE_ACT_COSNET3; }
+// [T, hl R] regions of the backward: C1, dH2, dH (and C2, dH3).
+int bwd_regions(const noble_linear_desc* d) { return three_layers(d) ? 5 : 3; }
+// bf16 backward: kChainCopies copies of the frequency / phase gradient
+// vectors, [2 L][kChainCopies][R] float32 (four vectors, six for three layers).
+int nvec(const noble_linear_desc* d) { return three_layers(d) ? 6 : 4; }
 size_t copies_need(const noble_linear_desc* d) {
     if (d->r == 0 || d->dtype != NOBLE_BF16) return 0;
-    return align_up((size_t)4 * kChainCopies * rank_total(d) * 4);
+    return align_up((size_t)nvec(d) * kChainCopies * rank_total(d) * 4);
 }
 size_t wgrad_need(const noble_linear_desc* d);
 size_t fwd_scratch_need(const noble_linear_desc* d) {
     return d->r > 0 ? scratch_region(d) + partial_need(d) : 0;
 }
 size_t scratch_need(const noble_linear_desc* d) {
-    return (d->r > 0 ? fwd_scratch_need(d) + 3 * scratch_region_w(d) + copies_need(d) : 0) + wgrad_need(d);
+    return (d->r > 0 ? fwd_scratch_need(d) + bwd_regions(d) * scratch_region_w(d) + copies_need(d) : 0) +
+           wgrad_need(d);
 }
 size_t reserve_need(const noble_linear_desc* d) { return (size_t)d->T * rank_total(d) * 4; }
 
@@ -373,9 +391,12 @@ struct RankParts {
     int64_t folded;     // dW_down and dM, per piece
     int64_t unfolded;   // dW_up, per piece
 };
+// dM products per group: 1, or 2 for the 3-layer form (counted for every
+// other activation too, so that their sizes agree).
+int64_t n_mix(const noble_linear_desc* d) { return three_layers(d) ? 2 : 1; }
 RankParts rank_parts(const noble_linear_desc* d) {
     const int64_t hl = hilo(d), G = ngroups(d), r = d->r, R = rank_total(d), dog = group_dout(d);
-    return RankParts{d->d_in * hl * R + G * hl * r * hl * r, G * r * dog};
+    return RankParts{d->d_in * hl * R + n_mix(d) * G * hl * r * hl * r, G * r * dog};
 }
 // Pieces of partials stored for the folded and the unfolded rank products.
 int64_t rank_folded_pieces(const noble_linear_desc* d, int rank) {
@@ -398,7 +419,8 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
         const int64_t R = rank_total(d), dog = group_dout(d), hl = hilo(d);
         const int G = ngroups(d);
         const int rank_tiles = cdiv(din, tile) * cdiv(hl * R, tile) +
-                               G * (cdiv(r, tile) * cdiv(dog, tile) + cdiv(hl * r, tile) * cdiv(hl * r, tile));
+                               G * (cdiv(r, tile) * cdiv(dog, tile) +
+                                    (int)n_mix(d) * cdiv(hl * r, tile) * cdiv(hl * r, tile));
         const RankParts rp = rank_parts(d);
         double best = -1.0;
         for (int sw : {1, 2, 3, 4, 6, 8, 12, 16}) {
@@ -436,20 +458,20 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
 WgradPlan plan_wgrad(const noble_linear_desc* d) {
     struct Entry {
         int64_t T, d_in, d_out, r;
-        int32_t dtype, groups;
+        int32_t dtype, groups, mix;
         WgradPlan w;
     };
     thread_local Entry cache[8];
     thread_local int used = 0, next = 0;
-    const int32_t G = ngroups(d);
+    const int32_t G = ngroups(d), mix = (int32_t)n_mix(d);
     for (int i = 0; i < used; ++i) {
         const Entry& e = cache[i];
         if (e.T == d->T && e.d_in == d->d_in && e.d_out == d->d_out && e.r == d->r && e.dtype == d->dtype &&
-            e.groups == G)
+            e.groups == G && e.mix == mix)
             return e.w;
     }
     const WgradPlan w = plan_wgrad_uncached(d);
-    cache[next] = Entry{d->T, d->d_in, d->d_out, d->r, d->dtype, G, w};
+    cache[next] = Entry{d->T, d->d_in, d->d_out, d->r, d->dtype, G, mix, w};
     next = (next + 1) % 8;
     used = std::min(used + 1, 8);
     return w;
@@ -469,7 +491,8 @@ noble_status check_grids(const noble_linear_desc* d) {
     auto tiles = [tile](int64_t m, int64_t n) { return ((m + tile - 1) / tile) * ((n + tile - 1) / tile); };
     const int64_t fwd = G * tiles(T, dog), dx = tiles(T, din);
     const int64_t hl = hilo(d);
-    const int64_t wgrad = tiles(din, dout) + (r > 0 ? tiles(din, hl * R) + G * (tiles(r, dog) + tiles(hl * r, hl * r)) : 0);
+    const int64_t wgrad =
+        tiles(din, dout) + (r > 0 ? tiles(din, hl * R) + G * (tiles(r, dog) + n_mix(d) * tiles(hl * r, hl * r)) : 0);
     return std::max({fwd, dx, wgrad}) <= max_gemm_blocks(d) ? NOBLE_OK : NOBLE_ERR_BAD_SHAPE;
 }
 
@@ -492,11 +515,11 @@ noble_status launch_gemm(const Batch& bt, hipStream_t st, bool plain = false) {
 // group (the arguments already point at the group's operands and columns).
 noble_status launch_chain(bool fwd, int RP, int act, const ChainArgs& a, int T, hipStream_t st) {
     const dim3 grid = flat_grid(cdiv(T, kChainRows)), block(kThreads);
-    return with_act(act, [&]<Act F, bool L2>() -> noble_status {
+    return with_act(act, [&]<Act F, int L>() -> noble_status {
 #define NOBLE_CHAIN(RPV)                                                                       \
     if (RP == RPV)                                                                             \
-        return fwd ? launch(fwd_chain_kernel<float, RPV, F, L2>, grid, block, st, a)           \
-                   : launch(bwd_chain_kernel<float, RPV, F, L2>, grid, block, st, a);
+        return fwd ? launch(fwd_chain_kernel<float, RPV, F, L>, grid, block, st, a)            \
+                   : launch(bwd_chain_kernel<float, RPV, F, L>, grid, block, st, a);
         NOBLE_CHAIN(32)
         NOBLE_CHAIN(64)
         NOBLE_CHAIN(128)
@@ -549,31 +572,40 @@ noble_status launch_branch(bool fwd, const noble_linear_desc* d, const ChainArgs
     a.pstride = d->T * rank_total(d);
     a.S = S;
     a.M = reinterpret_cast<const uint16_t*>(c.M);
+    a.M2 = reinterpret_cast<const uint16_t*>(c.M2);
     a.w1 = c.w1;
     a.p1 = c.p1;
     a.w2 = c.w2;
     a.p2 = c.p2;
+    a.w3 = c.w3;
+    a.p3 = c.p3;
     a.H = c.H;
     a.C1s = reinterpret_cast<uint16_t*>(c.C1s);
     a.C2s = reinterpret_cast<uint16_t*>(c.C2s);
     a.dH2s = reinterpret_cast<uint16_t*>(c.dH2s);
     a.dHs = reinterpret_cast<uint16_t*>(c.dHs);
+    a.C2ms = reinterpret_cast<uint16_t*>(c.C2ms);
+    a.dH3s = reinterpret_cast<uint16_t*>(c.dH3s);
     a.dw1 = c.dw1;
     a.dp1 = c.dp1;
     a.dw2 = c.dw2;
     a.dp2 = c.dp2;
+    a.dw3 = c.dw3;
+    a.dp3 = c.dp3;
     a.T = (int)d->T;
     a.r = (int)d->r;
     a.G = ngroups(d);
     a.R = (int)rank_total(d);
     const int NT = rank_blocks(d);
     const dim3 grid = flat_grid((int64_t)cdiv(d->T, kSkRows) * a.G), block(kThreads * NT);
-    return with_act(d->activation, [&]<Act F, bool L2>() -> noble_status {
+    return with_act(d->activation, [&]<Act F, int L>() -> noble_status {
         if (NT == 1)
-            return fwd ? launch(branch_fwd_kernel<F, L2, 1>, grid, block, st, a)
-                       : launch(branch_bwd_kernel<F, L2, 1>, grid, block, st, a);
-        return fwd ? launch(branch_fwd_kernel<F, L2, 2>, grid, block, st, a)
-                   : launch(branch_bwd_kernel<F, L2, 2>, grid, block, st, a);
+            return fwd ? launch(branch_fwd_kernel<F, L, 1>, grid, block, st, a)
+                       : launch(branch_bwd_kernel<F, L, 1>, grid, block, st, a);
+        if constexpr (L != 3)   // the 3-layer form is validated to r <= 128 (NT = 1)
+            return fwd ? launch(branch_fwd_kernel<F, L, 2>, grid, block, st, a)
+                       : launch(branch_bwd_kernel<F, L, 2>, grid, block, st, a);
+        return NOBLE_ERR_BAD_SHAPE;
     });
 }
 
@@ -599,20 +631,42 @@ ChainArgs group_chain(const ChainArgs& a, const noble_linear_desc* d, int g, siz
     auto off = [&](char* p, int64_t elems, size_t e) { return p ? p + elems * (int64_t)e : p; };
     auto offf = [&](auto* p, int64_t elems) { return p ? p + elems : p; };
     c.M = a.M ? a.M + g * r * r * (int64_t)es : a.M;
+    c.M2 = a.M2 ? a.M2 + g * r * r * (int64_t)es : a.M2;
     c.w1 = offf(a.w1, c0);
     c.p1 = offf(a.p1, c0);
     c.w2 = offf(a.w2, c0);
     c.p2 = offf(a.p2, c0);
+    c.w3 = offf(a.w3, c0);
+    c.p3 = offf(a.p3, c0);
     c.H = offf(a.H, c0);
     c.C1s = off(a.C1s, c0, es);
     c.C2s = off(a.C2s, c0, es);
     c.dH2s = off(a.dH2s, c0, es);
     c.dHs = off(a.dHs, c0, es);
+    c.C2ms = off(a.C2ms, c0, es);
+    c.dH3s = off(a.dH3s, c0, es);
     c.dw1 = offf(a.dw1, c0);
     c.dp1 = offf(a.dp1, c0);
     c.dw2 = offf(a.dw2, c0);
     c.dp2 = offf(a.dp2, c0);
+    c.dw3 = offf(a.dw3, c0);
+    c.dp3 = offf(a.dp3, c0);
     return c;
+}
+
+// The mixing parameters: M [G][r][r] with omega2, phi2 [R]; the 3-layer form
+// stores both mixing matrices as M [2][G][r][r] and the second and third
+// frequency / phase vectors as omega2, phi2 [2][R].
+void set_mixing(ChainArgs& a, const noble_linear_desc* d, const void* M, const float* w2, const float* p2) {
+    a.M = static_cast<const char*>(M);
+    a.w2 = w2;
+    a.p2 = p2;
+    if (three_layers(d)) {
+        const int64_t R = rank_total(d);
+        a.M2 = a.M + (int64_t)ngroups(d) * d->r * d->r * elt_size(d);
+        a.w3 = w2 + R;
+        a.p3 = p2 + R;
+    }
 }
 
 template <typename E>
@@ -627,11 +681,9 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
     char* C2s = static_cast<char*>(scratch);
     if (r > 0) {
         ChainArgs a{};
-        a.M = static_cast<const char*>(M);
+        set_mixing(a, d, M, w2, p2);
         a.w1 = w1;
         a.p1 = p1;
-        a.w2 = w2;
-        a.p2 = p2;
         a.H = static_cast<float*>(reserve);
         a.C2s = C2s;
         a.T = (int)T;
@@ -680,24 +732,28 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     const int64_t T = d->T, din = d->d_in, dout = d->d_out, r = d->r;
     const int64_t R = rank_total(d), dog = group_dout(d);
     const int G = ngroups(d);
-    const bool two = act_two_layers(d->activation);
-    const int64_t hl = hilo(d);   // C1, dH2, dH as high + low bf16 pairs on the bf16 path
+    const bool two = act_two_layers(d->activation), three = three_layers(d);
+    const int64_t nm = n_mix(d);   // mixing matrices per group
+    const int64_t hl = hilo(d);    // C1, dH2, dH as high + low bf16 pairs on the bf16 path
     const size_t regw = scratch_region_w(d);
     char* base = static_cast<char*>(scratch);
     char* C2s = base;
     char* C1s = base + fwd_scratch_need(d);
     char* dH2s = C1s + regw;
     char* dHs = dH2s + regw;
+    char* C2ms = three ? dHs + regw : nullptr;   // 3-layer form: the middle C2 and dH3
+    char* dH3s = three ? C2ms + regw : nullptr;
 
     // dW, dW_down, dW_up and dM are overwritten by their products (or by
     // the sums of their split-K partials); db and the dw / dp vectors are
     // accumulated atomically and start from zero.  T = 0 zeroes every
     // gradient; so does a one-application activation for the unused dM, dw2
-    // and dp2 (when given).
+    // and dp2 (when given).  The 3-layer form's dM is [2][G][r][r] and its
+    // dw2, dp2 are [2][R].
     constexpr int GBK = gemm_bk<E>();
     const int nkT = cdiv(T, GBK);
     const WgradPlan wp = plan_wgrad(d);
-    char* after_rank = r > 0 ? dHs + regw : base;
+    char* after_rank = r > 0 ? C1s + bwd_regions(d) * regw : base;
     float* copies = copies_need(d) ? reinterpret_cast<float*>(after_rank) : nullptr;
     float* wpart = reinterpret_cast<float*>(after_rank + copies_need(d));
     float* rpart = reinterpret_cast<float*>(reinterpret_cast<char*>(wpart) + wp.bytes);
@@ -717,10 +773,10 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             zero(dWd, din * R);
             zero(dWu, R * dog);
         }
-        if (T == 0 || !two) zero(dM, G * r * r);
+        if (T == 0 || !two) zero(dM, nm * G * r * r);
         if (copies && T > 0) {
             // the reduction of the copies overwrites dw1, dp1 (and dw2, dp2)
-            zero(copies, (int64_t)4 * kChainCopies * R);
+            zero(copies, (int64_t)nvec(d) * kChainCopies * R);
             if (!two) {
                 zero(dw2, R);
                 zero(dp2, R);
@@ -728,8 +784,8 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         } else {
             zero(dw1, R);
             zero(dp1, R);
-            zero(dw2, R);
-            zero(dp2, R);
+            zero(dw2, nm * R);
+            zero(dp2, nm * R);
         }
     }
     // On the bf16 path with a branch, the projection kernel does the zeroing.
@@ -741,20 +797,24 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
 
     if (r > 0) {
         ChainArgs a{};
-        a.M = static_cast<const char*>(M);
+        set_mixing(a, d, M, w2, p2);
         a.w1 = w1;
         a.p1 = p1;
-        a.w2 = w2;
-        a.p2 = p2;
         a.H = static_cast<float*>(const_cast<void*>(reserve));
         a.C1s = C1s;
         a.C2s = C2s;
         a.dH2s = dH2s;
         a.dHs = dHs;
+        a.C2ms = C2ms;
+        a.dH3s = dH3s;
         a.dw1 = dw1;
         a.dp1 = dp1;
         a.dw2 = dw2;
         a.dp2 = dp2;
+        if (three) {
+            a.dw3 = dw2 + R;
+            a.dp3 = dp2 + R;
+        }
         a.T = (int)T;
         a.r = (int)r;
         a.ldr = (int)R;
@@ -795,7 +855,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
     {
         ReduceList red{};
         static_assert(kChainCopies <= kMaxReduceSlices, "copies exceed the reduction's slices");
-        static_assert(kMaxZero >= kMaxProblems + 4, "the reduction list holds every product and four copies");
+        static_assert(kMaxZero >= kMaxProblems + 6, "the reduction list holds every product and six copies");
         auto reduce = [&](const float* part, float* out, int64_t n, int S, int fw = 0, int fold = 0) {
             red.part[red.count] = part;
             red.out[red.count] = out;
@@ -842,6 +902,13 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
                     const Operand dH2N = operand1(seg(dH2s + hl * c0 * (int64_t)ES, hl * R, T), hl * r);
                     rank(C1T, dH2N, hl * r, hl * r, dM + g * r * r, hl == 2 ? 3 : 0, r);
                 }
+                if (three) {
+                    // dM'_g = C2_g^T dH3_g (the middle layer's output and the
+                    // third layer's pre-mixing gradient), stored after dM
+                    const Operand C2mT = operand1(seg(C2ms + hl * c0 * (int64_t)ES, hl * R, T), hl * r);
+                    const Operand dH3N = operand1(seg(dH3s + hl * c0 * (int64_t)ES, hl * R, T), hl * r);
+                    rank(C2mT, dH3N, hl * r, hl * r, dM + (G + g) * r * r, hl == 2 ? 3 : 0, r);
+                }
             }
         }
         hipEvent_t ev0 = t_wgrad_ev0, ev1 = t_wgrad_ev1;
@@ -858,6 +925,10 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
             if (two) {
                 reduce(copies + 2 * arr, dw2, R, kChainCopies);
                 reduce(copies + 3 * arr, dp2, R, kChainCopies);
+            }
+            if (three) {
+                reduce(copies + 4 * arr, dw2 + R, R, kChainCopies);
+                reduce(copies + 5 * arr, dp2 + R, R, kChainCopies);
             }
         }
         if (red.count > 0) {
@@ -1095,9 +1166,11 @@ noble_status noble_init_params(const noble_linear_desc* desc, const noble_recipe
         NOBLE_TRY(add(W_down, din * R, 1, -dbound, dbound, true, 1));
         NOBLE_TRY(add(omega1, R, 1, recipe->omega_min, recipe->omega_max, false, 2));
         NOBLE_TRY(add(phi1, R, 0, recipe->phi_std, 0.0, false, 3));
-        NOBLE_TRY(add(M, G * r * r, 1, -mbound, mbound, true, 4));
-        NOBLE_TRY(add(omega2, R, 1, recipe->omega_min, recipe->omega_max, false, 5));
-        NOBLE_TRY(add(phi2, R, 0, recipe->phi_std, 0.0, false, 6));
+        // the 3-layer form: M [2][G][r][r], omega2 and phi2 [2][R]
+        const int64_t nm = n_mix(desc);
+        NOBLE_TRY(add(M, nm * G * r * r, 1, -mbound, mbound, true, 4));
+        NOBLE_TRY(add(omega2, nm * R, 1, recipe->omega_min, recipe->omega_max, false, 5));
+        NOBLE_TRY(add(phi2, nm * R, 0, recipe->phi_std, 0.0, false, 6));
         NOBLE_TRY(add(W_up, R * dog, 0, recipe->alpha / std::sqrt((double)r), 0.0, true, 7));
     }
     if (L.count == 0) return NOBLE_OK;

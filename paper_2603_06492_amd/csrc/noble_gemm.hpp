@@ -49,7 +49,7 @@ struct GemmProblem {
     int64_t pstride;    // elements between the partials of consecutive pieces
 };
 
-constexpr int kMaxProblems = 10;   // weight gradients of a 4-group layer: dW, dW_down, 4 x (dW_up, dM)
+constexpr int kMaxProblems = 14;   // weight gradients of a 4-group 3-layer CosNet: dW, dW_down, 4 x (dW_up, dM, dM')
 struct GemmBatch {
     GemmProblem p[kMaxProblems];
     int count;

@@ -41,7 +41,7 @@ __device__ __forceinline__ int64_t flat_block() { return (int64_t)blockIdx.y * g
 
 // ---------------------------------------------------------------- zero fill --
 
-constexpr int kMaxZero = 16;
+constexpr int kMaxZero = 24;
 struct ZeroList {
     float* ptr[kMaxZero];
     int64_t n[kMaxZero];
@@ -156,19 +156,26 @@ struct ChainArgs {
     Operand A;          // fwd: x [T, d_in];  bwd: dy [T, d_out]   (K-major)
     Operand B;          // fwd: W_down [d_in, r] (MN-major);  bwd: W_up as W_up^T (K-major)
     const char* M;      // [r, r] storage type
+    const char* M2;     // 3-layer form: the second mixing matrix [r, r]
     const float* w1;
     const float* p1;
     const float* w2;
     const float* p2;
+    const float* w3;    // 3-layer form
+    const float* p3;
     float* H;           // reserve [T, r]: written by fwd, read by bwd
     char* C1s;          // scratch [T, r] storage type (bwd)
-    char* C2s;          // scratch [T, r] storage type
+    char* C2s;          // scratch [T, r] storage type: the branch output (C2, or C3)
     char* dH2s;         // scratch [T, r] storage type (bwd)
     char* dHs;          // scratch [T, r] storage type (bwd)
+    char* C2ms;         // scratch [T, r] storage type (bwd, 3-layer form): the middle C2
+    char* dH3s;         // scratch [T, r] storage type (bwd, 3-layer form)
     float* dw1;
     float* dp1;
     float* dw2;
     float* dp2;
+    float* dw3;         // 3-layer form
+    float* dp3;
     int T, r, nk;
     int ldr;            // row stride of H and of the scratch arrays (G r for grouped layers)
 };
@@ -220,9 +227,45 @@ __device__ __forceinline__ float wave_colsum(float x) {
     return x;
 }
 
-// Forward chain for activation F; L2 = two applications with M between them
-// (CosNet for F = Cos), otherwise C2 = f(H w1 + p1) and M, w2, p2 are unused.
-template <typename E, int RP, Act F, bool L2>
+// f(acc w + p) of the wave's tile as the A operand of the next mixing
+// product (element type E in LDS), or, with `out`, stored to the [T, ldr]
+// array out.
+template <typename E, int TN, Act F>
+__device__ __forceinline__ void chain_apply(const f32x4 (&acc)[1][TN], const float* w, const float* p, int r, int wm0,
+                                            int wn0, int r16, int g, int m0, int T, int ldr, char* tile, char* out) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = wn0 + 16 * j + r16;
+        const bool cv = col < r;
+        const float ww = cv ? w[col] : 0.f, pp = cv ? p[col] : 0.f;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = wm0 + 4 * g + v, grow = m0 + row;
+            const float c = cv ? act_value<F, false>(acc[0][j][v] * ww + pp) : 0.f;
+            if (tile)
+                *reinterpret_cast<E*>(tile + tile_elem_off<E>(row, col, kChainRows)) = to_elt<E>(c);
+            else if (cv && grow < T)
+                reinterpret_cast<E*>(out)[(int64_t)grow * ldr + col] = to_elt<E>(c);
+        }
+    }
+}
+
+// acc = the tile in LDS (A operand, all NKB K chunks) times the staged M.
+template <typename E, int RP>
+__device__ __forceinline__ void chain_mix(const char* Cb, const char* Mb, int wm0, int wn0, int lane,
+                                          f32x4 (&acc)[1][ChainShape<E, RP>::TN]) {
+    using S = ChainShape<E, RP>;
+#pragma unroll
+    for (int j = 0; j < S::TN; ++j) acc[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < S::NKB; ++kb)
+        mma_chunk<E, 1, S::TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, acc);
+}
+
+// Forward chain for activation F with L applications: L = 2 with M between
+// them (CosNet for F = Cos), L = 1 (C2 = f(H w1 + p1); M, w2, p2 unused),
+// L = 3 with M2 between the second and third (the 3-layer CosNet).
+template <typename E, int RP, Act F, int L>
 __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
     using S = ChainShape<E, RP>;
     constexpr int TN = S::TN;
@@ -242,56 +285,84 @@ __global__ __launch_bounds__(kThreads) void fwd_chain_kernel(ChainArgs a) {
 
     char* Cb = lds;
     char* Mb = lds + S::NKB * kChainRows * kRowBytes;
-    if constexpr (L2) stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
+    if constexpr (L >= 2) stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
 
-    // H -> reserve; C1 = f(H w1 + p1) -> LDS (A operand of the mixing), or
-    // straight to C2 for one application
+    // H -> reserve
+    if (a.H) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = wn0 + 16 * j + r16;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int grow = m0 + wm0 + 4 * g + v;
+                if (col < r && grow < a.T) a.H[(int64_t)grow * a.ldr + col] = acc[0][j][v];
+            }
+        }
+    }
+    // C1 = f(H w1 + p1) -> LDS (A operand of the mixing), or straight to the
+    // output for one application
+    chain_apply<E, TN, F>(acc, a.w1, a.p1, r, wm0, wn0, r16, g, m0, a.T, a.ldr, L >= 2 ? Cb : nullptr, a.C2s);
+    if constexpr (L == 1) return;
+    __syncthreads();
+    f32x4 mix[1][TN];
+    chain_mix<E, RP>(Cb, Mb, wm0, wn0, lane, mix);   // H2 = C1 M
+    if constexpr (L == 3) {
+        __syncthreads();   // every wave is done with C1 and M in LDS
+        stage_mix_matrix<E, RP, false>(a.M2, r, Mb, tid);
+        chain_apply<E, TN, F>(mix, a.w2, a.p2, r, wm0, wn0, r16, g, m0, a.T, a.ldr, Cb, nullptr);   // C2 -> LDS
+        __syncthreads();
+        chain_mix<E, RP>(Cb, Mb, wm0, wn0, lane, mix);   // H3 = C2 M2
+        // C3 = f(H3 w3 + p3) -> scratch
+        chain_apply<E, TN, F>(mix, a.w3, a.p3, r, wm0, wn0, r16, g, m0, a.T, a.ldr, nullptr, a.C2s);
+    } else {
+        // C2 = f(H2 w2 + p2) -> scratch
+        chain_apply<E, TN, F>(mix, a.w2, a.p2, r, wm0, wn0, r16, g, m0, a.T, a.ldr, nullptr, a.C2s);
+    }
+}
+
+// One layer of the backward through A = acc w + p, C = f(A), for the wave's
+// tile: with the output gradient dC (registers), dA = f'(A) dC, the column
+// sums of dA acc and dA are added to dw and dp, dA w goes to LDS (the A
+// operand of the next gradient mixing product) and to dst; C = f(A) goes to
+// cdst (when given).
+template <typename E, int TN, Act F>
+__device__ __forceinline__ void chain_back_layer(const f32x4 (&acc)[1][TN], const f32x4 (&dC)[1][TN], const float* w,
+                                                 const float* p, float* dw, float* dp, int r, int wm0, int wn0, int r16,
+                                                 int g, int m0, int T, int ldr, char* tile, char* dst, char* cdst) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int col = wn0 + 16 * j + r16;
         const bool cv = col < r;
-        const float w = cv ? a.w1[col] : 0.f, p = cv ? a.p1[col] : 0.f;
+        const float ww = cv ? w[col] : 0.f, pp = cv ? p[col] : 0.f;
+        float sw = 0.f, sp = 0.f;
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int row = wm0 + 4 * g + v, grow = m0 + row;
-            const float h = acc[0][j][v];
-            if (a.H && cv && grow < a.T) a.H[(int64_t)grow * a.ldr + col] = h;
-            const float c1 = cv ? act_value<F, false>(h * w + p) : 0.f;
-            if constexpr (L2)
-                *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = to_elt<E>(c1);
-            else if (cv && grow < a.T)
-                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * a.ldr + col] = to_elt<E>(c1);
+            const bool ok = cv && grow < T;
+            float f = 0.f, d = 0.f;
+            if (cv) act_value_slope<F, false>(acc[0][j][v] * ww + pp, f, d);
+            const float da = ok ? d * dC[0][j][v] : 0.f;
+            sw += da * acc[0][j][v];
+            sp += da;
+            const E dh = to_elt<E>(da * ww);
+            *reinterpret_cast<E*>(tile + tile_elem_off<E>(row, col, kChainRows)) = dh;
+            if (ok) {
+                if (cdst) reinterpret_cast<E*>(cdst)[(int64_t)grow * ldr + col] = to_elt<E>(f);
+                reinterpret_cast<E*>(dst)[(int64_t)grow * ldr + col] = dh;
+            }
         }
-    }
-    if constexpr (!L2) return;
-    __syncthreads();
-
-    f32x4 mix[1][TN];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) mix[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < S::NKB; ++kb)
-        mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, mix);
-
-    // C2 = f(H2 w2 + p2) -> scratch
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int col = wn0 + 16 * j + r16;
-        if (col >= r) continue;
-        const float w = a.w2[col], p = a.p2[col];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int grow = m0 + wm0 + 4 * g + v;
-            if (grow < a.T)
-                reinterpret_cast<E*>(a.C2s)[(int64_t)grow * a.ldr + col] =
-                    to_elt<E>(act_value<F, false>(mix[0][j][v] * w + p));
+        sw = wave_colsum(sw);
+        sp = wave_colsum(sp);
+        if (g == 0 && cv) {
+            unsafeAtomicAdd(dw + col, sw);
+            unsafeAtomicAdd(dp + col, sp);
         }
     }
 }
 
 // Backward chain, same forms as fwd_chain_kernel.  The one-application form
 // writes C2 and dH only.
-template <typename E, int RP, Act F, bool L2>
+template <typename E, int RP, Act F, int L>
 __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
     using S = ChainShape<E, RP>;
     constexpr int TN = S::TN;
@@ -304,7 +375,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
     const int m0 = (int)wg * kChainRows;
     const int r = a.r;
 
-    // dC2 = dy W_up^T
+    // the output's gradient dy W_up^T
     f32x4 dc2[1][TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) dc2[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -312,10 +383,10 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
 
     char* Cb = lds;
     char* Mb = lds + S::NKB * kChainRows * kRowBytes;
-    if constexpr (L2) stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
+    if constexpr (L >= 2) stage_mix_matrix<E, RP, false>(a.M, r, Mb, tid);
 
-    // Recompute A1 = H w1 + p1 and C1 = f(A1) (-> LDS and scratch, or to C2
-    // for one application); keep H and f'(A1).
+    // Recompute A1 = H w1 + p1 and C1 = f(A1) (-> LDS and scratch, or to the
+    // output for one application); keep H and f'(A1).
     float hr[TN][4], d1[TN][4];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -332,7 +403,7 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
             hr[j][v] = h;
             d1[j][v] = d;
             const E c1 = to_elt<E>(f);
-            if constexpr (L2) {
+            if constexpr (L >= 2) {
                 *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = c1;
                 if (ok) reinterpret_cast<E*>(a.C1s)[(int64_t)grow * a.ldr + col] = c1;
             } else if (ok) {
@@ -341,63 +412,47 @@ __global__ __launch_bounds__(kThreads) void bwd_chain_kernel(ChainArgs a) {
         }
     }
 
-    // dC1: dC2 itself (one application) or dH2 M^T (two)
+    // dC1: the output's gradient itself (one application), or back through
+    // the mixing layers
     f32x4 dc1[1][TN];
-    if constexpr (!L2) {
+    if constexpr (L == 1) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) dc1[0][j] = dc2[0][j];
     } else {
         __syncthreads();
-
-        // H2 = C1 M
         f32x4 h2[1][TN];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) h2[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kb = 0; kb < S::NKB; ++kb)
-            mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, h2);
+        chain_mix<E, RP>(Cb, Mb, wm0, wn0, lane, h2);   // H2 = C1 M
         __syncthreads();  // every wave is done with C1 and M in LDS
 
-        stage_mix_matrix<E, RP, true>(a.M, r, Mb, tid);
-
-        // A2 = H2 w2 + p2; C2 = f(A2) -> scratch; dA2 = f'(A2) dC2;
-        // dw2 += dA2 H2, dp2 += dA2; dH2 = dA2 w2 -> LDS and scratch.
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int col = wn0 + 16 * j + r16;
-            const bool cv = col < r;
-            const float w = cv ? a.w2[col] : 0.f, p = cv ? a.p2[col] : 0.f;
-            float sw = 0.f, sp = 0.f;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int row = wm0 + 4 * g + v, grow = m0 + row;
-                const bool ok = cv && grow < a.T;
-                float f = 0.f, d = 0.f;
-                if (cv) act_value_slope<F, false>(h2[0][j][v] * w + p, f, d);
-                const float da2 = ok ? d * dc2[0][j][v] : 0.f;
-                sw += da2 * h2[0][j][v];
-                sp += da2;
-                const E dh2 = to_elt<E>(da2 * w);
-                *reinterpret_cast<E*>(Cb + tile_elem_off<E>(row, col, kChainRows)) = dh2;
-                if (ok) {
-                    reinterpret_cast<E*>(a.C2s)[(int64_t)grow * a.ldr + col] = to_elt<E>(f);
-                    reinterpret_cast<E*>(a.dH2s)[(int64_t)grow * a.ldr + col] = dh2;
-                }
-            }
-            sw = wave_colsum(sw);
-            sp = wave_colsum(sp);
-            if (g == 0 && cv) {
-                unsafeAtomicAdd(a.dw2 + col, sw);
-                unsafeAtomicAdd(a.dp2 + col, sp);
-            }
+        f32x4 dcm[1][TN];   // gradient of C2
+        if constexpr (L == 3) {
+            // C2 = f(H2 w2 + p2) -> LDS and scratch (the middle layer's C2)
+            stage_mix_matrix<E, RP, false>(a.M2, r, Mb, tid);
+            chain_apply<E, TN, F>(h2, a.w2, a.p2, r, wm0, wn0, r16, g, m0, a.T, a.ldr, Cb, nullptr);
+            chain_apply<E, TN, F>(h2, a.w2, a.p2, r, wm0, wn0, r16, g, m0, a.T, a.ldr, nullptr, a.C2ms);
+            __syncthreads();
+            f32x4 h3[1][TN];
+            chain_mix<E, RP>(Cb, Mb, wm0, wn0, lane, h3);   // H3 = C2 M2
+            __syncthreads();
+            stage_mix_matrix<E, RP, true>(a.M2, r, Mb, tid);
+            // C3 -> output; dA3 = f'(A3) dC3; dw3, dp3; dH3 -> LDS and scratch
+            chain_back_layer<E, TN, F>(h3, dc2, a.w3, a.p3, a.dw3, a.dp3, r, wm0, wn0, r16, g, m0, a.T, a.ldr, Cb,
+                                       a.dH3s, a.C2s);
+            __syncthreads();
+            chain_mix<E, RP>(Cb, Mb, wm0, wn0, lane, dcm);   // dC2 = dH3 M2^T
+            __syncthreads();
+            stage_mix_matrix<E, RP, true>(a.M, r, Mb, tid);
+            // C2 was stored above; dA2, dH2
+            chain_back_layer<E, TN, F>(h2, dcm, a.w2, a.p2, a.dw2, a.dp2, r, wm0, wn0, r16, g, m0, a.T, a.ldr, Cb,
+                                       a.dH2s, nullptr);
+        } else {
+            stage_mix_matrix<E, RP, true>(a.M, r, Mb, tid);
+            // C2 -> output; dA2 = f'(A2) dC2; dw2, dp2; dH2 -> LDS and scratch
+            chain_back_layer<E, TN, F>(h2, dc2, a.w2, a.p2, a.dw2, a.dp2, r, wm0, wn0, r16, g, m0, a.T, a.ldr, Cb,
+                                       a.dH2s, a.C2s);
         }
         __syncthreads();
-
-#pragma unroll
-        for (int j = 0; j < TN; ++j) dc1[0][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kb = 0; kb < S::NKB; ++kb)
-            mma_chunk<E, 1, TN>(Cb + kb * kChainRows * kRowBytes, Mb + kb * RP * kRowBytes, wm0, wn0, lane, dc1);
+        chain_mix<E, RP>(Cb, Mb, wm0, wn0, lane, dc1);   // dC1 = dH2 M^T
     }
 
     // dA1 = f'(A1) dC1; dw1 += dA1 H, dp1 += dA1; dH = dA1 w1 -> scratch

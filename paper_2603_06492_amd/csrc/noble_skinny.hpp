@@ -45,13 +45,15 @@ constexpr int kSkN = 128;       // rank columns of one M tile
 constexpr int kSkM = kSkN * kSkN * 2;     // one M tile, 128 x 128 bf16
 constexpr int kSkC = kSkRows * kSkN * 2;  // 32 x 128 bf16 of the C1 / dH2 operand tile
 constexpr int kSkMaxNT = 2;               // ranks up to 2 x 128 per group
-// LDS of a chain workgroup with NT x NT M tiles and two 32 x 128 NT operand
-// tiles: the high and low bf16 parts of the mixing operand (C1 or dH2).
-template <int NT>
+// LDS of a chain workgroup with L - 1 mixing matrices of NT x NT M tiles
+// and two 32 x 128 NT operand tiles: the high and low bf16 parts of the
+// mixing operand (C1, C2, dH2 or dH3).  The 3-layer form runs at NT = 1.
+template <int NT, int L = 2>
 constexpr int sk_lds() {
-    return NT * NT * kSkM + 2 * NT * kSkC;
+    return (L == 3 ? 2 : 1) * NT * NT * kSkM + 2 * NT * kSkC;
 }
 static_assert(sk_lds<kSkMaxNT>() <= 160 * 1024, "chain LDS exceeds a CU's 160 KB");
+static_assert(sk_lds<1, 3>() <= 160 * 1024, "chain LDS exceeds a CU's 160 KB");
 
 // A float32 value as the sum of two bf16 values (round to nearest even
 // twice): hi carries the leading 8 significant bits, lo the next 8.  hi + lo
@@ -117,22 +119,29 @@ struct BranchArgs {
     const float* P;       // projection partials [S][T][R]
     int64_t pstride;
     const uint16_t* M;    // [G][r][r]
+    const uint16_t* M2;   // 3-layer form: the second mixing matrices [G][r][r]
     const float* w1;      // [R]
     const float* p1;
     const float* w2;
     const float* p2;
+    const float* w3;      // 3-layer form: the third frequency / phase [R]
+    const float* p3;
     float* H;             // reserve [T, R] float32 (NULL in an inference forward)
-    uint16_t* C1s;        // scratch [T, R] bf16 (backward)
-    uint16_t* C2s;        // scratch [T, R] bf16
-    uint16_t* dH2s;       // scratch [T, R] bf16 (backward)
-    uint16_t* dHs;        // scratch [T, R] bf16 (backward)
+    uint16_t* C1s;        // scratch (backward), see branch_bwd_kernel
+    uint16_t* C2s;        // scratch [T, R] bf16: the branch output (C2, or C3 in the 3-layer form)
+    uint16_t* dH2s;       // scratch (backward)
+    uint16_t* dHs;        // scratch (backward)
+    uint16_t* C2ms;       // scratch (backward, 3-layer form): the middle layer's C2 pairs
+    uint16_t* dH3s;       // scratch (backward, 3-layer form): dH3 pairs
     float* dw1;           // [R]
     float* dp1;
     float* dw2;
     float* dp2;
-    // Backward: when set, the four frequency / phase gradients are added into
-    // kChainCopies zeroed copies [4][kChainCopies][R] (dw1, dp1, dw2, dp2),
-    // copy = workgroup % kChainCopies, instead of into dw1 .. dp2; a
+    float* dw3;           // 3-layer form
+    float* dp3;
+    // Backward: when set, the frequency / phase gradients are added into
+    // kChainCopies zeroed copies [2 L][kChainCopies][R] (dw1, dp1, dw2, dp2,
+    // dw3, dp3), copy = workgroup % kChainCopies, instead of into dw1 ..; a
     // reduction sums the copies afterwards.  Fewer workgroups then add into
     // one address, which float atomics serialise on.
     float* copies;
@@ -475,17 +484,51 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t group_rsrc(const void* base, c
     return rows_rsrc(base, a.T, q.row0, a.R, q.c0, es);
 }
 
-// Forward chain.  L2: the two-application form with M (CosNet for F = Cos);
-// otherwise C2 = f(H w1 + p1) and M, w2, p2 are not read.  The mixing
-// operand C1 enters the MFMAs as three bf16 parts (bf_split3): the high and
-// middle parts from the two operand tiles, then the low part from the first
-// tile again, so H2 = C1 M is as accurate as a float32 product and A2 carries
-// float32 rounding only.
-template <Act F, bool L2, int NT>
+// The wave's 32 x 32 block of P M (TRANS = false) or P M^T (TRANS = true)
+// for a float32 operand P held in registers (the lane's 16 values at rows
+// 8(v/4) + 4h + v%4, column col): P goes to the operand tiles in three bf16
+// parts (two passes), so the product is as accurate as a float32 one.
+// Leaves the tiles free (a barrier after the last read).
+template <bool TRANS, int NT>
+__device__ __forceinline__ void mix3(const float (&pv)[16], char* chi, char* clo, const char* mt, int wave, int lane,
+                                     int col, f32x16& acc) {
+    const int h = lane >> 5;
+    uint16_t lo[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
+        const BfTriple t = bf_split3(pv[v]);
+        *reinterpret_cast<uint16_t*>(chi + ctile_off(row, col)) = t.hi;
+        *reinterpret_cast<uint16_t*>(clo + ctile_off(row, col)) = t.mid;
+        lo[v] = t.lo;
+        acc[v] = 0.f;
+    }
+    __syncthreads();
+    mix_mma<TRANS, NT>(chi, clo, mt, wave, lane, acc);
+    __syncthreads();   // every wave is done with the high part
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+        *reinterpret_cast<uint16_t*>(chi + ctile_off(8 * (v >> 2) + 4 * h + (v & 3), col)) = lo[v];
+    __syncthreads();
+    mix_mma1<TRANS, NT>(chi, mt, wave, lane, acc);
+    __syncthreads();   // done reading the tiles
+}
+
+// Forward chain.  L = 2: the two-application form with M (CosNet for F =
+// Cos); L = 1: C2 = f(H w1 + p1), M, w2, p2 not read; L = 3 (the 3-layer
+// CosNet): C3 = f((C2 M') w3 + p3) after the second layer, M' = a.M2.  Each
+// mixing operand (C1, and C2 in the 3-layer form) enters the MFMAs as three
+// bf16 parts (bf_split3: high and middle parts from the two operand tiles,
+// then the low part from the first tile again), so every mixing product is
+// as accurate as a float32 one and the cosine arguments carry float32
+// rounding only.
+template <Act F, int L, int NT>
 __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs a) {
-    __shared__ __attribute__((aligned(1024))) char lds[sk_lds<NT>()];
+    static_assert(L != 3 || NT == 1, "the 3-layer form holds both mixing matrices in LDS at r <= 128");
+    __shared__ __attribute__((aligned(1024))) char lds[sk_lds<NT, L>()];
     char* mt = lds;
-    char* chi = mt + NT * NT * kSkM;
+    char* mt2 = mt + NT * NT * kSkM;   // 3-layer form
+    char* chi = mt + (L == 3 ? 2 : 1) * NT * NT * kSkM;
     char* clo = chi + NT * kSkC;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
@@ -493,7 +536,9 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
     const ChainPos q = chain_pos(a);
     const int r = a.r, R = a.R;
 
-    if constexpr (L2) m_dma<NT>(a.M + (int64_t)q.g * r * r, r, mt, wave, lane);   // lands while the partials are summed
+    // M (and M') land while the partials are summed
+    if constexpr (L >= 2) m_dma<NT>(a.M + (int64_t)q.g * r * r, r, mt, wave, lane);
+    if constexpr (L == 3) m_dma<NT>(a.M2 + (int64_t)q.g * r * r, r, mt2, wave, lane);
     // acc[v]: token row0 + 8(v/4) + 4h + v%4, rank column 32 wave + r32 of the group
     const int col = 32 * wave + r32;
     f32x16 acc;
@@ -510,50 +555,41 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
     // H is read again only by the backward, after every other projection's
     // forward: it is stored non-temporal, so that it does not linger dirty in
     // the memory-side cache.
-    // Stores count in vmcnt: in the two-application form H is stored after
-    // the barrier, whose wait for M would otherwise also wait for them.
+    // Stores count in vmcnt: in the mixing forms H is stored after the
+    // barrier, whose wait for M would otherwise also wait for them.
     auto store_h = [&]() {
         if (keep_h)
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), rh, vo4, soff(v, 4), kStoreNT);
     };
-    if constexpr (!L2) store_h();
-    uint16_t c1lo[16];
+    float c1[16];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-        const float c1 = cv ? act_value<F, true>(acc[v] * w1 + p1) : 0.f;
-        if constexpr (L2) {
-            const int row = 8 * (v >> 2) + 4 * h + (v & 3);
-            const BfTriple c = bf_split3(c1);
-            *reinterpret_cast<uint16_t*>(chi + ctile_off(row, col)) = c.hi;
-            *reinterpret_cast<uint16_t*>(clo + ctile_off(row, col)) = c.mid;
-            c1lo[v] = c.lo;
-        } else {
-            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(c1), rc, vo2, soff(v, 2), 0);
-        }
-    }
-    if constexpr (L2) {
-        const float w2 = cv ? a.w2[q.c0 + col] : 0.f, p2 = cv ? a.p2[q.c0 + col] : 0.f;
-        wait_vmcnt<0>();   // this wave's part of M has landed
-        __syncthreads();   // C1 tiles and M complete
+    for (int v = 0; v < 16; ++v) c1[v] = cv ? act_value<F, true>(acc[v] * w1 + p1) : 0.f;
+    if constexpr (L == 1) {
         store_h();
-
-        f32x16 h2;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) h2[v] = 0.f;
-        mix_mma<false, NT>(chi, clo, mt, wave, lane, h2);
-        __syncthreads();   // every wave is done with the high part
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-            *reinterpret_cast<uint16_t*>(chi + ctile_off(8 * (v >> 2) + 4 * h + (v & 3), col)) = c1lo[v];
-        __syncthreads();
-        mix_mma1<false, NT>(chi, mt, wave, lane, h2);
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(act_value<F, true>(h2[v] * w2 + p2)), rc, vo2,
-                                                  soff(v, 2), 0);
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(c1[v]), rc, vo2, soff(v, 2), 0);
+        return;
     }
+    const float w2 = cv ? a.w2[q.c0 + col] : 0.f, p2 = cv ? a.p2[q.c0 + col] : 0.f;
+    wait_vmcnt<0>();   // this wave's part of M (and M') has landed
+    store_h();
+    f32x16 h2;
+    mix3<false, NT>(c1, chi, clo, mt, wave, lane, col, h2);   // H2 = C1 M (its first barrier publishes M)
+    float c2[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) c2[v] = cv ? act_value<F, true>(h2[v] * w2 + p2) : 0.f;
+    if constexpr (L == 3) {
+        const float w3 = cv ? a.w3[q.c0 + col] : 0.f, p3 = cv ? a.p3[q.c0 + col] : 0.f;
+        f32x16 h3;
+        mix3<false, NT>(c2, chi, clo, mt2, wave, lane, col, h3);   // H3 = C2 M'
+#pragma unroll
+        for (int v = 0; v < 16; ++v) c2[v] = cv ? act_value<F, true>(h3[v] * w3 + p3) : 0.f;
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(c2[v]), rc, vo2, soff(v, 2), 0);
 }
 
 // Backward chain, same forms as branch_fwd_kernel.  The one-application form
@@ -561,18 +597,24 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_fwd_kernel(BranchArgs
 //
 // Scratch layouts (operands of the weight-gradient products, each a high +
 // low bf16 pair so that those products are float32-accurate):
-//  - C1 and dH2: [T][G][2 r], group g's high part in columns 2 g r .. 2 g r
-//    + r - 1 and its low part in the next r (row stride 2 R);
+//  - C1 and dH2 (and in the 3-layer form the middle C2 and dH3): [T][G][2 r],
+//    group g's high part in columns 2 g r .. 2 g r + r - 1 and its low part
+//    in the next r (row stride 2 R);
 //  - dH: [T][2 R], the high part of all groups in columns 0 .. R - 1, the
 //    low part in R .. 2 R - 1 (the dx product reads only the high part);
-//  - C2: [T][R], one bf16 value (the operand of y and dW_up).
-// Both mixing products (H2 = C1 M recomputed, dC1 = dH2 M^T) take their
-// operand as the same pair.
-template <Act F, bool L2, int NT>
+//  - the branch output (C2, or C3): [T][R], one bf16 value (the operand of
+//    dW_up).
+// The recomputed mixing products take their float32 operand in three
+// parts, as the forward does (so the cosine arguments are the forward's);
+// the gradient mixing products (dC1 = dH2 M^T, dC2 = dH3 M'^T) take theirs as
+// a high + low pair.
+template <Act F, int L, int NT>
 __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs a) {
-    __shared__ __attribute__((aligned(1024))) char lds[sk_lds<NT>()];
+    static_assert(L != 3 || NT == 1, "the 3-layer form holds both mixing matrices in LDS at r <= 128");
+    __shared__ __attribute__((aligned(1024))) char lds[sk_lds<NT, L>()];
     char* mt = lds;
-    char* chi = mt + NT * NT * kSkM;
+    char* mt2 = mt + NT * NT * kSkM;   // 3-layer form
+    char* chi = mt + (L == 3 ? 2 : 1) * NT * NT * kSkM;
     char* clo = chi + NT * kSkC;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r32 = lane & 31, h = lane >> 5;
@@ -584,6 +626,8 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     float* gp1 = a.dp1;
     float* gw2 = a.dw2;
     float* gp2 = a.dp2;
+    float* gw3 = a.dw3;
+    float* gp3 = a.dp3;
     if (a.copies) {
         float* c = a.copies + (flat_block() % kChainCopies) * R;
         const int64_t arr = (int64_t)kChainCopies * R;
@@ -591,9 +635,12 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
         gp1 = c + arr;
         gw2 = c + 2 * arr;
         gp2 = c + 3 * arr;
+        gw3 = c + 4 * arr;
+        gp3 = c + 5 * arr;
     }
 
-    if constexpr (L2) m_dma<NT>(a.M + (int64_t)q.g * r * r, r, mt, wave, lane);
+    if constexpr (L >= 2) m_dma<NT>(a.M + (int64_t)q.g * r * r, r, mt, wave, lane);
+    if constexpr (L == 3) m_dma<NT>(a.M2 + (int64_t)q.g * r * r, r, mt2, wave, lane);
     const int col = 32 * wave + r32;
     const bool cv = col < r;
     const int gc = q.c0 + col;   // column of the [R] vectors
@@ -607,6 +654,16 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     const uint32_t vw2 = cv ? (uint32_t)(((4 * h) * 2 * R + col) * 2) : kOOB;   // row stride 2R
     auto soff = [&](int v, int es) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * R * es); };
     auto soffw = [&](int v) { return (uint32_t)((8 * (v >> 2) + (v & 3)) * 2 * R * 2); };
+    const uint32_t lo_off = (uint32_t)r * 2;   // [T][G][2r] pairs: bytes from the high part to the low part
+    // the group's pair columns of a [T][G][2r] array start at 2 c0
+    auto pair_rsrc = [&](const uint16_t* base) {
+        return rows_rsrc(base, a.T, q.row0, 2 * (int64_t)R, 2 * (int64_t)q.c0, 2);
+    };
+    auto store_pair = [&](__amdgpu_buffer_rsrc_t rs, int v, uint16_t hi, uint16_t lo) {
+        __builtin_amdgcn_raw_buffer_store_b16(hi, rs, vw2, soffw(v), 0);
+        __builtin_amdgcn_raw_buffer_store_b16(lo, rs, vw2 + lo_off, soffw(v), 0);
+    };
+    auto row_of = [&](int v) { return 8 * (v >> 2) + 4 * h + (v & 3); };
 
     // H from the reserve (rows past T and columns past r read as zero),
     // issued before the partial sums so that both arrive in one round trip
@@ -615,80 +672,108 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     for (int v = 0; v < 16; ++v)
         hr[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rh, vo4, soff(v, 4), 0));
     f32x16 dc2;
-    sum_partials(a, q.row0, q.c0, col, h, dc2);   // dC2 = dy W_up^T
+    sum_partials(a, q.row0, q.c0, col, h, dc2);   // the output's gradient dy W_up^T
     // A1 = H w1 + p1, keep f'(A1)
     const float w1 = cv ? a.w1[gc] : 0.f, p1 = cv ? a.p1[gc] : 0.f;
+    float c1[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        float f = 0.f, d = 0.f;
+        if (cv) act_value_slope<F, true>(hr[v] * w1 + p1, f, d);
+        d1[v] = d;
+        c1[v] = f;
+    }
 
-    // dC1: dC2 itself (one application) or dH2 M^T (two)
+    // dC1: the output's gradient itself (one application), or back through
+    // the mixing layers
     f32x16 dc1;
-    if constexpr (!L2) {
+    if constexpr (L == 1) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-            float f = 0.f, d = 0.f;
-            if (cv) act_value_slope<F, true>(hr[v] * w1 + p1, f, d);
-            d1[v] = d;
-            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(f), rc2, vo2, soff(v, 2), 0);   // C2 = C1
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(c1[v]), rc2, vo2, soff(v, 2), 0);   // C2 = C1
             dc1[v] = dc2[v];
         }
     } else {
         const float w2 = cv ? a.w2[gc] : 0.f, p2 = cv ? a.p2[gc] : 0.f;
-        // C1 and dH2 [T][G][2r]: the group's pair starts at column 2 c0
-        const __amdgpu_buffer_rsrc_t rc1 = rows_rsrc(a.C1s, a.T, q.row0, 2 * (int64_t)R, 2 * (int64_t)q.c0, 2);
-        const __amdgpu_buffer_rsrc_t rdh2 = rows_rsrc(a.dH2s, a.T, q.row0, 2 * (int64_t)R, 2 * (int64_t)q.c0, 2);
-        const uint32_t lo_off = (uint32_t)r * 2;   // bytes from the high part to the low part
-        // C1 in three parts for the recomputed H2 (as in the forward, so that
-        // A2 is the forward's); its high and middle parts are the pair
-        // stored for dM
-        BfTriple c1[16];
+        const __amdgpu_buffer_rsrc_t rc1 = pair_rsrc(a.C1s), rdh2 = pair_rsrc(a.dH2s);
+        wait_vmcnt<0>();   // this wave's part of M (and M') has landed
+        // C1's pair (for dM) to scratch; the barrier in mix3 publishes M
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-            const int row = 8 * (v >> 2) + 4 * h + (v & 3);
-            float f = 0.f, d = 0.f;
-            if (cv) act_value_slope<F, true>(hr[v] * w1 + p1, f, d);
-            d1[v] = d;
-            c1[v] = bf_split3(f);
-            *reinterpret_cast<uint16_t*>(chi + ctile_off(row, col)) = c1[v].hi;
-            *reinterpret_cast<uint16_t*>(clo + ctile_off(row, col)) = c1[v].mid;
+            const BfPair c = bf_split(c1[v]);
+            store_pair(rc1, v, c.hi, c.lo);
         }
-        wait_vmcnt<0>();   // this wave's part of M has landed
-        __syncthreads();   // C1 tiles and M complete
-        // C1 to scratch after the barrier: stores count in vmcnt, and the
-        // wait above is for M only
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            __builtin_amdgcn_raw_buffer_store_b16(c1[v].hi, rc1, vw2, soffw(v), 0);
-            __builtin_amdgcn_raw_buffer_store_b16(c1[v].mid, rc1, vw2 + lo_off, soffw(v), 0);
-        }
-
         f32x16 h2;
+        mix3<false, NT>(c1, chi, clo, mt, wave, lane, col, h2);   // H2 = C1 M
+        // A2 = H2 w2 + p2: C2 = f(A2), keep f'(A2)
+        float c2[16], d2[16];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) h2[v] = 0.f;
-        mix_mma<false, NT>(chi, clo, mt, wave, lane, h2);   // H2 = C1 M: high and middle parts
-        __syncthreads();                                     // every wave is done with the high part
+        for (int v = 0; v < 16; ++v) {
+            float f = 0.f, d = 0.f;
+            if (cv) act_value_slope<F, true>(h2[v] * w2 + p2, f, d);
+            c2[v] = f;
+            d2[v] = d;
+        }
+        f32x16 dcm;   // gradient of C2
+        if constexpr (L == 2) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-            *reinterpret_cast<uint16_t*>(chi + ctile_off(8 * (v >> 2) + 4 * h + (v & 3), col)) = c1[v].lo;
-        __syncthreads();
-        mix_mma1<false, NT>(chi, mt, wave, lane, h2);       // ... and the low part
-        __syncthreads();                                     // done reading C1 from LDS
+            for (int v = 0; v < 16; ++v) {
+                __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(c2[v]), rc2, vo2, soff(v, 2), 0);
+                dcm[v] = dc2[v];
+            }
+        } else {
+            // the third layer: H3 = C2 M', A3 = H3 w3 + p3, C3 = f(A3);
+            // dA3 = f'(A3) dC3, dH3 = dA3 w3, dC2 = dH3 M'^T
+            const float w3 = cv ? a.w3[gc] : 0.f, p3 = cv ? a.p3[gc] : 0.f;
+            const __amdgpu_buffer_rsrc_t rc2m = pair_rsrc(a.C2ms), rdh3 = pair_rsrc(a.dH3s);
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const BfPair c = bf_split(c2[v]);
+                store_pair(rc2m, v, c.hi, c.lo);
+            }
+            f32x16 h3;
+            mix3<false, NT>(c2, chi, clo, mt2, wave, lane, col, h3);
+            float da3h3[16], da3[16];
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const bool ok = cv && row_of(v) < rows_left;
+                float f = 0.f, d = 0.f;
+                if (cv) act_value_slope<F, true>(h3[v] * w3 + p3, f, d);
+                __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(f), rc2, vo2, soff(v, 2), 0);
+                const float g = ok ? d * dc2[v] : 0.f;
+                da3[v] = g;
+                da3h3[v] = g * h3[v];
+                const BfPair dh3 = bf_split(g * w3);
+                *reinterpret_cast<uint16_t*>(chi + ctile_off(row_of(v), col)) = dh3.hi;
+                *reinterpret_cast<uint16_t*>(clo + ctile_off(row_of(v), col)) = dh3.lo;
+                store_pair(rdh3, v, dh3.hi, dh3.lo);
+            }
+            {
+                const float sw = block_colsum(da3h3), sp = block_colsum(da3);
+                if (h == 0 && cv) {
+                    unsafeAtomicAdd(gw3 + gc, sw);
+                    unsafeAtomicAdd(gp3 + gc, sp);
+                }
+            }
+            __syncthreads();   // dH3 tiles complete
+#pragma unroll
+            for (int v = 0; v < 16; ++v) dcm[v] = 0.f;
+            mix_mma<true, NT>(chi, clo, mt2, wave, lane, dcm);   // dC2 = dH3 M'^T
+            __syncthreads();                                      // done reading the dH3 tiles
+        }
 
-        // A2 = H2 w2 + p2, C2 = f(A2), dA2 = f'(A2) dC2, dH2 = dA2 w2
+        // dA2 = f'(A2) dC2, dH2 = dA2 w2
         float da2h2[16], da2[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-            const int row = 8 * (v >> 2) + 4 * h + (v & 3);
-            const bool ok = cv && row < rows_left;
-            float f = 0.f, d = 0.f;
-            if (cv) act_value_slope<F, true>(h2[v] * w2 + p2, f, d);
-            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)f2bf(f), rc2, vo2, soff(v, 2), 0);
-            const float g = ok ? d * dc2[v] : 0.f;
+            const bool ok = cv && row_of(v) < rows_left;
+            const float g = ok ? d2[v] * dcm[v] : 0.f;
             da2[v] = g;
             da2h2[v] = g * h2[v];
             const BfPair dh2 = bf_split(g * w2);
-            *reinterpret_cast<uint16_t*>(chi + ctile_off(row, col)) = dh2.hi;
-            *reinterpret_cast<uint16_t*>(clo + ctile_off(row, col)) = dh2.lo;
-            __builtin_amdgcn_raw_buffer_store_b16(dh2.hi, rdh2, vw2, soffw(v), 0);
-            __builtin_amdgcn_raw_buffer_store_b16(dh2.lo, rdh2, vw2 + lo_off, soffw(v), 0);
+            *reinterpret_cast<uint16_t*>(chi + ctile_off(row_of(v), col)) = dh2.hi;
+            *reinterpret_cast<uint16_t*>(clo + ctile_off(row_of(v), col)) = dh2.lo;
+            store_pair(rdh2, v, dh2.hi, dh2.lo);
         }
         {
             const float sw = block_colsum(da2h2), sp = block_colsum(da2);
@@ -709,8 +794,7 @@ __global__ __launch_bounds__(kThreads * NT, 1) void branch_bwd_kernel(BranchArgs
     const uint32_t dh_lo = (uint32_t)R * 2;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-        const int row = 8 * (v >> 2) + 4 * h + (v & 3);
-        const bool ok = cv && row < rows_left;
+        const bool ok = cv && row_of(v) < rows_left;
         const float g = ok ? d1[v] * dc1[v] : 0.f;
         da1[v] = g;
         da1h[v] = g * hr[v];

@@ -29,7 +29,7 @@ LIB_PATH = os.path.join(PKG_DIR, "libnoble.so")
 NOBLE_BF16 = 0
 NOBLE_F32 = 1
 # NOBLE_ABI_VERSION of include/noble.h that the structures below mirror
-ABI_VERSION = 4
+ABI_VERSION = 5
 
 STATUS = {
     0: "NOBLE_OK",
@@ -53,8 +53,12 @@ ACTIVATIONS = {
     "leaky_relu_m": 5,
     "gelu": 6,
     "gelu_m": 7,
+    "cosnet3": 8,
 }
-TWO_LAYER = {"cosnet", "tanh_m", "leaky_relu_m", "gelu_m"}
+# applications of the nonlinearity per activation (mixing matrices: one fewer)
+LAYERS = {"cosnet": 2, "cos": 1, "tanh": 1, "tanh_m": 2, "leaky_relu": 1, "leaky_relu_m": 2, "gelu": 1,
+          "gelu_m": 2, "cosnet3": 3}
+TWO_LAYER = {n for n, k in LAYERS.items() if k >= 2}
 
 
 def activation_code(activation) -> int:
@@ -66,10 +70,19 @@ def activation_code(activation) -> int:
     return int(activation)
 
 
-def two_layers(activation) -> bool:
-    """True for the forms with the mixing matrix M (CosNet and the _m names)."""
+def layers(activation) -> int:
+    """Applications of the nonlinearity: 1, 2 (CosNet and the _m names) or 3
+    (the 3-layer CosNet)."""
     code = activation_code(activation)
-    return code in {ACTIVATIONS[n] for n in TWO_LAYER}
+    for n, c in ACTIVATIONS.items():
+        if c == code:
+            return LAYERS[n]
+    raise ValueError(f"unknown activation code {code}")
+
+
+def two_layers(activation) -> bool:
+    """True for the forms with a mixing matrix M (two or three layers)."""
+    return layers(activation) >= 2
 
 
 class NobleError(RuntimeError):
@@ -236,14 +249,19 @@ def _on(device):
     return _torch().cuda.device(device)
 
 
-def _branch_shapes(d_in, d_out, R, groups):
-    """Shapes of W_down, the [R] vectors, M and W_up for ``groups`` groups of
-    total rank R (M is [r, r] for one group, [G, r, r] otherwise)."""
+def _branch_shapes(d_in, d_out, R, groups, activation=0):
+    """Shapes of W_down, the [R] vectors, M, the second-layer vectors (vec2)
+    and W_up for ``groups`` groups of total rank R (M is [r, r] for one group,
+    [G, r, r] otherwise; the 3-layer form stacks two of each: M [2, ...],
+    omega2 / phi2 [2, R])."""
     G = int(groups)
     if R % G or d_out % G:
         raise ValueError(f"d_out ({d_out}) and the total rank ({R}) must divide into {G} groups")
     r = R // G
-    return dict(W_down=(d_in, R), vec=(R,), M=(r, r) if G == 1 else (G, r, r), W_up=(R, d_out // G)), r
+    M = (r, r) if G == 1 else (G, r, r)
+    three = layers(activation) == 3
+    return dict(W_down=(d_in, R), vec=(R,), M=(2,) + M if three else M, vec2=(2, R) if three else (R,),
+                W_up=(R, d_out // G)), r
 
 
 def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
@@ -262,7 +280,7 @@ def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, re
     T, d_in = x.shape
     d_out = W.shape[1]
     R = 0 if W_down is None else W_down.shape[1]
-    sh, r = _branch_shapes(d_in, d_out, R, groups)
+    sh, r = _branch_shapes(d_in, d_out, R, groups, activation)
     dt = _dtype_code(x)
     sd = x.dtype
     f32 = torch.float32
@@ -272,7 +290,7 @@ def noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, re
         _ptr(x, "x", sd, (T, d_in), dev), _ptr(W, "W", sd, (d_in, d_out), dev), _ptr(b, "b", f32, (d_out,), dev),
         _ptr(W_down, "W_down", sd, sh["W_down"], dev), _ptr(omega1, "omega1", f32, sh["vec"], dev),
         _ptr(phi1, "phi1", f32, sh["vec"], dev), _ptr(M, "M", sd, sh["M"], dev),
-        _ptr(omega2, "omega2", f32, sh["vec"], dev), _ptr(phi2, "phi2", f32, sh["vec"], dev),
+        _ptr(omega2, "omega2", f32, sh["vec2"], dev), _ptr(phi2, "phi2", f32, sh["vec2"], dev),
         _ptr(W_up, "W_up", sd, sh["W_up"], dev), _ptr(y, "y", sd, (T, d_out), dev),
         _ptr(reserve, "reserve", device=dev), _ptr(scratch, "scratch", device=dev),
     ]
@@ -291,14 +309,14 @@ def noble_linear_fwd_static(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up
     T, d_in = x.shape
     d_out = W.shape[1]
     R = 0 if W_down is None else W_down.shape[1]
-    sh, r = _branch_shapes(d_in, d_out, R, groups)
+    sh, r = _branch_shapes(d_in, d_out, R, groups, activation)
     sd, f32, dev = x.dtype, torch.float32, x.device
     d = make_desc(T, d_in, d_out, r, _dtype_code(x), activation, groups)
     args = [
         _ptr(x, "x", sd, (T, d_in), dev), _ptr(W, "W", sd, (d_in, d_out), dev), _ptr(b, "b", f32, (d_out,), dev),
         _ptr(W_down, "W_down", sd, sh["W_down"], dev), _ptr(omega1, "omega1", f32, sh["vec"], dev),
         _ptr(phi1, "phi1", f32, sh["vec"], dev), _ptr(M, "M", sd, sh["M"], dev),
-        _ptr(omega2, "omega2", f32, sh["vec"], dev), _ptr(phi2, "phi2", f32, sh["vec"], dev),
+        _ptr(omega2, "omega2", f32, sh["vec2"], dev), _ptr(phi2, "phi2", f32, sh["vec2"], dev),
         _ptr(W_up, "W_up", sd, sh["W_up"], dev), _ptr(y, "y", sd, (T, d_out), dev),
         _ptr(reserve, "reserve", device=dev),
     ]
@@ -322,25 +340,25 @@ def noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, rese
     T, d_in = x.shape
     d_out = W.shape[1]
     R = 0 if W_down is None else W_down.shape[1]
-    sh, r = _branch_shapes(d_in, d_out, R, groups)
+    sh, r = _branch_shapes(d_in, d_out, R, groups, activation)
     dt = _dtype_code(x)
     sd = x.dtype
     f32 = torch.float32
     d = make_desc(T, d_in, d_out, r, dt, activation, groups)
-    v = sh["vec"]
+    v, v2 = sh["vec"], sh["vec2"]
     dev = x.device
     args = [
         _ptr(dy, "dy", sd, (T, d_out), dev), _ptr(x, "x", sd, (T, d_in), dev), _ptr(W, "W", sd, (d_in, d_out), dev),
         _ptr(W_down, "W_down", sd, sh["W_down"], dev), _ptr(omega1, "omega1", f32, v, dev),
-        _ptr(phi1, "phi1", f32, v, dev), _ptr(M, "M", sd, sh["M"], dev), _ptr(omega2, "omega2", f32, v, dev),
-        _ptr(phi2, "phi2", f32, v, dev), _ptr(W_up, "W_up", sd, sh["W_up"], dev),
+        _ptr(phi1, "phi1", f32, v, dev), _ptr(M, "M", sd, sh["M"], dev), _ptr(omega2, "omega2", f32, v2, dev),
+        _ptr(phi2, "phi2", f32, v2, dev), _ptr(W_up, "W_up", sd, sh["W_up"], dev),
         _ptr(reserve, "reserve", device=dev),
         _ptr(dx, "dx", sd, (T, d_in), dev), _ptr(dW, "dW", f32, (d_in, d_out), dev),
         _ptr(db, "db", f32, (d_out,), dev),
         _ptr(dW_down, "dW_down", f32, sh["W_down"], dev), _ptr(dM, "dM", f32, sh["M"], dev),
         _ptr(dW_up, "dW_up", f32, sh["W_up"], dev),
         _ptr(domega1, "domega1", f32, v, dev), _ptr(dphi1, "dphi1", f32, v, dev),
-        _ptr(domega2, "domega2", f32, v, dev), _ptr(dphi2, "dphi2", f32, v, dev),
+        _ptr(domega2, "domega2", f32, v2, dev), _ptr(dphi2, "dphi2", f32, v2, dev),
         _ptr(scratch, "scratch", device=dev),
     ]
     nbytes = 0 if scratch is None else scratch.numel() * scratch.element_size()
@@ -376,29 +394,31 @@ def noble_lr_multipliers(d_in: int, d_out: int, r: int, recipe: Optional[noble_r
 
 
 def noble_init_params(W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, seed: int,
-                      recipe: Optional[noble_recipe] = None, stream=None, groups: int = 1) -> None:
+                      recipe: Optional[noble_recipe] = None, stream=None, groups: int = 1,
+                      activation=0) -> None:
     """Fill the layer's parameter tensors on the device from ``seed``
-    (None skips a tensor).  Storage tensors share one dtype (bf16 or f32)."""
+    (None skips a tensor).  Storage tensors share one dtype (bf16 or f32);
+    the 3-layer form's M, omega2, phi2 are its stacked [2, ...] tensors."""
     torch = _torch()
     rc = noble_recipe_defaults() if recipe is None else recipe
     d_in, d_out = W.shape
     R = 0
-    for t, dim in ((W_down, 1), (W_up, 0), (omega1, 0), (phi1, 0), (omega2, 0), (phi2, 0)):
+    for t, dim in ((W_down, 1), (W_up, 0), (omega1, 0), (phi1, 0), (omega2, -1), (phi2, -1)):
         if t is not None:
             R = t.shape[dim]
             break
     if R == 0 and M is not None:
         R = M.shape[-1] * groups
-    sh, r = _branch_shapes(d_in, d_out, R, groups)
+    sh, r = _branch_shapes(d_in, d_out, R, groups, activation)
     dt = _dtype_code(W)
     sd, f32 = W.dtype, torch.float32
-    d = make_desc(0, d_in, d_out, r, dt, 0, groups)
-    v = sh["vec"]
+    d = make_desc(0, d_in, d_out, r, dt, activation, groups)
+    v, v2 = sh["vec"], sh["vec2"]
     dev = W.device
     args = [_ptr(W, "W", sd, (d_in, d_out), dev), _ptr(b, "b", f32, (d_out,), dev),
             _ptr(W_down, "W_down", sd, sh["W_down"], dev), _ptr(omega1, "omega1", f32, v, dev),
-            _ptr(phi1, "phi1", f32, v, dev), _ptr(M, "M", sd, sh["M"], dev), _ptr(omega2, "omega2", f32, v, dev),
-            _ptr(phi2, "phi2", f32, v, dev), _ptr(W_up, "W_up", sd, sh["W_up"], dev)]
+            _ptr(phi1, "phi1", f32, v, dev), _ptr(M, "M", sd, sh["M"], dev), _ptr(omega2, "omega2", f32, v2, dev),
+            _ptr(phi2, "phi2", f32, v2, dev), _ptr(W_up, "W_up", sd, sh["W_up"], dev)]
     with _on(dev):
         st = lib().noble_init_params(ctypes.byref(d), ctypes.byref(rc), int(seed) & (2 ** 64 - 1), *args,
                                      _stream(stream, dev))
@@ -428,13 +448,14 @@ def param_groups(params: dict, lr: float, d_in: int, d_out: int, r: int,
 
 # ------------------------------------------------------------ conveniences --
 
-def alloc_workspace(T, d_in, d_out, r, dtype_code, device="cuda", groups: int = 1, forward_only=False):
+def alloc_workspace(T, d_in, d_out, r, dtype_code, device="cuda", groups: int = 1, forward_only=False,
+                    activation=0):
     """(reserve, scratch) uint8 tensors of the required sizes; with
     ``forward_only`` the scratch covers the forward alone."""
     torch = _torch()
-    res, scr = noble_linear_workspace_size(T, d_in, d_out, r, dtype_code, groups=groups)
+    res, scr = noble_linear_workspace_size(T, d_in, d_out, r, dtype_code, activation, groups=groups)
     if forward_only:
-        scr = noble_linear_fwd_scratch_size(T, d_in, d_out, r, dtype_code, groups=groups)
+        scr = noble_linear_fwd_scratch_size(T, d_in, d_out, r, dtype_code, activation, groups=groups)
     return (torch.empty(max(res, 16), dtype=torch.uint8, device=device),
             torch.empty(max(scr, 16), dtype=torch.uint8, device=device))
 
@@ -456,7 +477,8 @@ def _make_function():
             r = R // groups
             dt = _dtype_code(x)
             act = activation_code(activation)
-            reserve, scratch = alloc_workspace(T, d_in, d_out, r, dt, x.device, groups=groups, forward_only=True)
+            reserve, scratch = alloc_workspace(T, d_in, d_out, r, dt, x.device, groups=groups, forward_only=True,
+                                               activation=act)
             y = torch.empty((T, d_out), dtype=x.dtype, device=x.device)
             noble_linear_fwd(x, W, b, W_down, omega1, phi1, M, omega2, phi2, W_up, y, reserve, scratch,
                              activation=act, groups=groups)
@@ -472,16 +494,16 @@ def _make_function():
             T, d_in = x.shape
             d_out, R = W.shape[1], W_down.shape[1]
             G = ctx.groups
-            sh, r = _branch_shapes(d_in, d_out, R, G)
+            sh, r = _branch_shapes(d_in, d_out, R, G, ctx.act)
             dev, f32 = x.device, torch.float32
             two = two_layers(ctx.act)
             dy = dy.contiguous().to(x.dtype)
-            _, scratch = alloc_workspace(T, d_in, d_out, r, _dtype_code(x), dev, groups=G)
+            _, scratch = alloc_workspace(T, d_in, d_out, r, _dtype_code(x), dev, groups=G, activation=ctx.act)
             dx = torch.empty_like(x)
             g = {n: torch.empty(s, dtype=f32, device=dev) for n, s in (
                 ("dW", (d_in, d_out)), ("db", (d_out,)), ("dW_down", sh["W_down"]), ("dM", sh["M"]),
-                ("dW_up", sh["W_up"]), ("domega1", sh["vec"]), ("dphi1", sh["vec"]), ("domega2", sh["vec"]),
-                ("dphi2", sh["vec"]))}
+                ("dW_up", sh["W_up"]), ("domega1", sh["vec"]), ("dphi1", sh["vec"]), ("domega2", sh["vec2"]),
+                ("dphi2", sh["vec2"]))}
             if not two:
                 g["dM"] = g["domega2"] = g["dphi2"] = None
             noble_linear_bwd(dy, x, W, W_down, omega1, phi1, M, omega2, phi2, W_up, reserve,
@@ -519,7 +541,7 @@ def _make_module():
             self.activation = activation
             self.recipe = recipe
             R = self.groups * self.r
-            sh, _ = _branch_shapes(self.d_in, self.d_out, R, self.groups)
+            sh, _ = _branch_shapes(self.d_in, self.d_out, R, self.groups, activation)
             f32 = torch.float32
             P = lambda shape, dt: torch.nn.Parameter(torch.empty(shape, dtype=dt, device=device))
             self.W = P((self.d_in, self.d_out), dtype)
@@ -530,8 +552,8 @@ def _make_module():
                 self.omega1 = P(sh["vec"], f32)
                 self.phi1 = P(sh["vec"], f32)
                 self.M = P(sh["M"], dtype) if two else None
-                self.omega2 = P(sh["vec"], f32) if two else None
-                self.phi2 = P(sh["vec"], f32) if two else None
+                self.omega2 = P(sh["vec2"], f32) if two else None
+                self.phi2 = P(sh["vec2"], f32) if two else None
                 self.W_up = P(sh["W_up"], dtype)
             self.reset_parameters(seed)
 
@@ -542,14 +564,16 @@ def _make_module():
 
         @torch.no_grad()
         def reset_parameters(self, seed=0):
-            noble_init_params(self.W, self.b, *self._branch(), seed=seed, recipe=self.recipe, groups=self.groups)
+            noble_init_params(self.W, self.b, *self._branch(), seed=seed, recipe=self.recipe, groups=self.groups,
+                              activation=self.activation)
 
         def _infer(self, x2):
             # Nothing to differentiate: the forward without the reserve, so H
             # is neither written nor kept.
             T = x2.shape[0]
             _, scratch = alloc_workspace(T, self.d_in, self.d_out, self.r, _dtype_code(x2), x2.device,
-                                         groups=self.groups, forward_only=True)
+                                         groups=self.groups, forward_only=True,
+                                         activation=activation_code(self.activation))
             y = torch.empty((T, self.d_out), dtype=x2.dtype, device=x2.device)
             noble_linear_fwd(x2, self.W, self.b, *self._branch(), y, None, scratch,
                              activation=activation_code(self.activation), groups=self.groups)

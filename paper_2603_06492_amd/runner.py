@@ -85,8 +85,11 @@ class DeviceProblem:
         }
         if r > 0:
             mshape = (r, r) if G == 1 else (G, r, r)
+            v2 = (R,)
+            if noble.layers(activation) == 3:   # stacked second and third layers
+                mshape, v2 = (2,) + mshape, (2, R)
             for n, s in (("dW_down", (di, R)), ("dM", mshape), ("dW_up", (R, dog)), ("domega1", (R,)),
-                         ("dphi1", (R,)), ("domega2", (R,)), ("dphi2", (R,))):
+                         ("dphi1", (R,)), ("domega2", v2), ("dphi2", v2)):
                 self.g[n] = self._out(s, f32)
             for n in unused:
                 self.g["d" + n] = None

@@ -72,7 +72,7 @@ int main(void) {
     bad.groups = 2;   /* 72 / 2 = 36 is not a multiple of 8 */
     CHECK(noble_linear_workspace_size(&bad, &reserve, &scratch) == NOBLE_ERR_BAD_SHAPE);
     bad = desc(64, 64, 64, 8, NOBLE_BF16);
-    bad.activation = 8;
+    bad.activation = NOBLE_ACT_COSNET3 + 1;
     CHECK(noble_linear_workspace_size(&bad, &reserve, &scratch) == NOBLE_ERR_BAD_ACTIVATION);
     /* a forward product past one dispatch: 8388592 token tiles x 2 column tiles */
     bad = desc(2147483648LL - 4096, 8, 264, 8, NOBLE_BF16);

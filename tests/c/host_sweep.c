@@ -49,7 +49,7 @@ int main(void) {
                             d.r = rs[e];
                             d.dtype = (int32_t)g;
                             d.groups = gs[f];
-                            d.activation = (int32_t)((a + b + c + e) % 9);
+                            d.activation = (int32_t)((a + b + c + e) % (NOBLE_ACT_COSNET3 + 2));   /* and one past */
                             check_status(noble_linear_workspace_size(&d, &res, &scr));
                             check_status(noble_linear_fwd_scratch_size(&d, &fs));
                             check_status(noble_lr_multipliers(&d, &rc, &lr));

@@ -37,7 +37,7 @@ def test_library_exports_every_declared_function():
     L = noble.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.noble_abi_version() == 4 == noble.ABI_VERSION
+    assert L.noble_abi_version() == 5 == noble.ABI_VERSION
 
 
 def test_status_strings():
@@ -46,8 +46,8 @@ def test_status_strings():
     assert "UNKNOWN" in noble.noble_status_string(99)
 
 
-def _ws(T, di, do, r, dt, groups=1):
-    d = noble.make_desc(T, di, do, r, dt, 0, groups)
+def _ws(T, di, do, r, dt, groups=1, act=0):
+    d = noble.make_desc(T, di, do, r, dt, act, groups)
     a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
     st = noble.lib().noble_linear_workspace_size(ctypes.byref(d), ctypes.byref(a), ctypes.byref(b))
     return st, a.value, b.value
@@ -83,9 +83,10 @@ def _split_partials(tiles, nk, mn):
     return bs
 
 
-def _copies(R):
-    """bf16 backward: 8 copies of the four frequency / phase gradient vectors."""
-    return _align(4 * 8 * R * 4)
+def _copies(R, nvec=4):
+    """bf16 backward: 8 copies of the four frequency / phase gradient vectors
+    (six for the 3-layer form)."""
+    return _align(nvec * 8 * R * 4)
 
 
 def _makespan(groups):
@@ -102,17 +103,18 @@ def _makespan(groups):
     return end
 
 
-def _rank_parts(di, do, r, groups, hl):
+def _rank_parts(di, do, r, groups, hl, nm=1):
     """Float32 elements of one K piece of the rank products' partials:
     (folded, unfolded).  On the bf16 path (hl = 2) dW_down = x^T [dH_hi |
     dH_lo] ([d_in, 2 R]) and dM_g = [C1_hi | C1_lo]_g^T [dH2_hi | dH2_lo]_g
-    ([2 r, 2 r]) are stored for any split and folded by the reduction; dW_up
-    [r, d_out / G] per group is stored only when split."""
+    ([2 r, 2 r]; nm = 2 such products per group for the 3-layer form) are
+    stored for any split and folded by the reduction; dW_up [r, d_out / G]
+    per group is stored only when split."""
     R, dog = groups * r, do // groups
-    return di * hl * R + groups * (hl * r) ** 2, groups * r * dog
+    return di * hl * R + nm * groups * (hl * r) ** 2, groups * r * dog
 
 
-def _wgrad_split(T, di, do, r, bk, tile=256, groups=1, hl=2):
+def _wgrad_split(T, di, do, r, bk, tile=256, groups=1, hl=2, nm=1):
     """K pieces of dW in the weight-gradient launch.  r = 0: dW alone
     (_split_partials).  r > 0: dW and the rank products (dW_down, dW_up and
     dM, counted whatever the activation) together, minimising the makespan
@@ -127,8 +129,8 @@ def _wgrad_split(T, di, do, r, bk, tile=256, groups=1, hl=2):
     if r == 0:
         return _split_partials(tiles, nk, di * do), 1
     G, R, dog = groups, groups * r, do // groups
-    rank_tiles = cd(di, tile) * cd(hl * R, tile) + G * (cd(r, tile) * cd(dog, tile) + cd(hl * r, tile) ** 2)
-    folded, unfolded = _rank_parts(di, do, r, groups, hl)
+    rank_tiles = cd(di, tile) * cd(hl * R, tile) + G * (cd(r, tile) * cd(dog, tile) + nm * cd(hl * r, tile) ** 2)
+    folded, unfolded = _rank_parts(di, do, r, groups, hl, nm)
     best, pick = None, (1, 1)
     cands = (1, 2, 3, 4, 6, 8, 12, 16)
     for sw in cands:
@@ -148,21 +150,21 @@ def _wgrad_split(T, di, do, r, bk, tile=256, groups=1, hl=2):
     return pick
 
 
-def _wgrad_bytes(T, di, do, r, bk, tile=256, groups=1, hl=2):
+def _wgrad_bytes(T, di, do, r, bk, tile=256, groups=1, hl=2, nm=1):
     """Split-K partials of the weight gradients: dW's region, then one
     region for the rank products (see _rank_parts).  Output tiles are 256
     square on the bf16 path (hl = 2), 128 on the float32 path (hl = 1)."""
-    sw, sr = _wgrad_split(T, di, do, r, bk, tile, groups, hl)
-    folded, unfolded = _rank_parts(di, do, r, groups, hl)
+    sw, sr = _wgrad_split(T, di, do, r, bk, tile, groups, hl, nm)
+    folded, unfolded = _rank_parts(di, do, r, groups, hl, nm)
     fp = max(sr, 1) if hl == 2 else (sr if sr > 1 else 0)
     rank = fp * folded + (sr * unfolded if sr > 1 else 0)
     return (_align(sw * di * do * 4) if sw > 1 else 0) + (_align(rank * 4) if r > 0 and T > 0 and rank else 0)
 
 
-def _branch_scratch(T, di, do, r, G=1, bf16=True):
+def _branch_scratch(T, di, do, r, G=1, bf16=True, three=False):
     """Rank-side scratch: C2 [T, R], the bf16 projection partials, then C1,
-    dH2, dH [T, hl R] and the bf16 copies of the frequency / phase
-    gradients."""
+    dH2, dH [T, hl R] (and the 3-layer form's middle C2 and dH3) and the
+    bf16 copies of the frequency / phase gradients."""
     R, es, hl = G * r, (2 if bf16 else 4), (2 if bf16 else 1)
     if r == 0:
         return 0
@@ -171,7 +173,8 @@ def _branch_scratch(T, di, do, r, G=1, bf16=True):
         J = G * -(-r // 128)
         S = max(_proj_split(T, di, J), _proj_split(T, do // G, J))
         part = _align(S * T * R * 4)
-    return _align(T * R * es) + part + 3 * _align(hl * T * R * es) + (_copies(R) if bf16 else 0)
+    nreg, nvec = (5, 6) if three else (3, 4)
+    return _align(T * R * es) + part + nreg * _align(hl * T * R * es) + (_copies(R, nvec) if bf16 else 0)
 
 
 def test_workspace_sizes():
@@ -433,15 +436,14 @@ def test_activation_codes_match_header_and_oracle():
     import oracle
     hdr = _header_enum("NOBLE_ACT_")
     assert {k.lower(): v for k, v in hdr.items()} == noble.ACTIVATIONS
-    # the 3-layer CosNet is stated in the oracle ahead of its kernels
-    assert set(noble.ACTIVATIONS) | {"cosnet3"} == set(oracle.ACTIVATIONS)
+    assert set(noble.ACTIVATIONS) == set(oracle.ACTIVATIONS)
     for name, (_, layers) in oracle.ACTIVATIONS.items():
-        if name in noble.ACTIVATIONS:
-            assert noble.two_layers(name) == (layers == 2), name
+        assert noble.layers(name) == layers, name
+        assert noble.two_layers(name) == (layers >= 2), name
     assert _header_enum("NOBLE_ERR_")["BAD_ACTIVATION"] == BADACT
 
 
-@pytest.mark.parametrize("act", [-1, 8, 1 << 20])
+@pytest.mark.parametrize("act", [-1, 9, 1 << 20])
 def test_bad_activation_rejected(act):
     d = noble.make_desc(64, 64, 64, 16, noble.NOBLE_BF16, act)
     a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
@@ -452,10 +454,24 @@ def test_bad_activation_rejected(act):
         noble.activation_code("relu")
 
 
-def test_workspace_does_not_depend_on_activation():
+def test_workspace_depends_only_on_the_three_layer_form():
+    """Every one- and two-application activation shares one size; the
+    3-layer form adds the middle C2 and dH3 regions, two more copies of the
+    gradient vectors (bf16) and its second dM product's partials."""
     for dt in (noble.NOBLE_BF16, noble.NOBLE_F32):
-        sizes = {noble.noble_linear_workspace_size(300, 64, 1024, 40, dt, a) for a in noble.ACTIVATIONS}
+        sizes = {noble.noble_linear_workspace_size(300, 64, 1024, 40, dt, a) for a in noble.ACTIVATIONS
+                 if a != "cosnet3"}
         assert len(sizes) == 1
+        three = noble.noble_linear_workspace_size(300, 64, 1024, 40, dt, "cosnet3")
+        assert three[0] == sizes.pop()[0] and three[1] > 0
+    for (T, di, do, r, G) in ((300, 64, 1024, 40, 1), (8192, 2048, 6144, 128, 3), (8192, 2048, 8192, 128, 1)):
+        bf = _branch_scratch(T, di, do, r, G, True, True) + _wgrad_bytes(T, di, do, r, 64, 256, G, 2, 2)
+        assert _ws(T, di, do, r, noble.NOBLE_BF16, G, 8) == (OK, 4 * T * G * r, bf)
+        f32 = _branch_scratch(T, di, do, r, G, False, True) + _wgrad_bytes(T, di, do, r, 32, 128, G, 1, 2)
+        assert _ws(T, di, do, r, noble.NOBLE_F32, G, 8) == (OK, 4 * T * G * r, f32)
+    # both mixing matrices stay in LDS: r <= 128 on either path
+    assert _ws(16, 64, 64, 128, noble.NOBLE_BF16, 1, 8)[0] == OK
+    assert _ws(16, 64, 64, 136, noble.NOBLE_BF16, 1, 8)[0] == SHAPE
 
 
 ONE = [a for a in noble.ACTIVATIONS if not noble.two_layers(a)]

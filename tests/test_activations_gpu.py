@@ -1,7 +1,8 @@
 """Parity of the bottleneck activation variants through the C ABI against the
 fp64 oracle: single cosine, tanh, LeakyReLU and GELU, each as one application
 and (except cosine, whose two-application form is the CosNet covered by
-test_parity_gpu.py) as two applications with the mixing matrix M.
+test_parity_gpu.py) as two applications with the mixing matrix M, and the
+3-layer CosNet (two mixing matrices; more of it in test_cosnet3_gpu.py).
 
 Same metric and bounds as test_parity_gpu.py, against the plain oracle.  On
 the bf16 path the kernels take the mixing operand (C1 in H2 = C1 M, dH2 in
@@ -53,7 +54,8 @@ def test_activation_parity(act, case):
     # LeakyReLU: the seed is stepped (deterministically) until no
     # pre-activation lies in the kink band, as in test_fuzz_gpu.py
     for attempt in range(50 if act.startswith("leaky") else 1):
-        p = inp.draw_projection(name, T, di, do, r, dt, seed=seed + 1000 * attempt, bias_std=0.5)
+        p = inp.draw_projection(name, T, di, do, r, dt, seed=seed + 1000 * attempt, bias_std=0.5,
+                                layers=max(2, noble.layers(act)))
         if not act.startswith("leaky") or kink_margin(p, act) > 1.0:
             break
     else:

@@ -1,6 +1,7 @@
 """Seeded random shapes through the C ABI against the fp64 oracle: token
 counts from 1 to 700, widths that are any multiple of 8, ranks up to 256
-(bf16) / 128 (f32), 1 to 4 groups, every activation, both storage types.
+(bf16) / 128 (f32 and the 3-layer CosNet), 1 to 4 groups, every activation,
+both storage types.
 
 Every case is compared with the plain oracle.  A LeakyReLU case is redrawn
 (deterministically) until no pre-activation lies in the band where float32
@@ -22,19 +23,20 @@ from _parity import OUTPUTS, TOL, kink_margin, oracle_outputs, parity_report
 pytestmark = pytest.mark.gpu
 
 
-def _cases(n=24, seed=2026):
+def _cases(n=24, seed=2026, acts=None, rmax_bf16=256, tag=""):
     rng = np.random.default_rng(seed)
-    acts = sorted(noble.ACTIVATIONS)
+    acts = sorted(a for a in noble.ACTIVATIONS if a != "cosnet3") if acts is None else acts
     out = []
     for i in range(n):
         dt = "bf16" if i % 4 else "f32"
         G = int(rng.choice([1, 1, 2, 3, 4]))
-        r = 8 * int(rng.integers(1, (32 if dt == "bf16" else 16) + 1))
+        r = 8 * int(rng.integers(1, (rmax_bf16 // 8 if dt == "bf16" else 16) + 1))
         T = int(rng.choice([1, 2, 31, 33, 64, 127, 129, 255, 300, 511, 700]))
         d_in = 8 * int(rng.integers(1, 65))
         d_out = 8 * G * int(rng.integers(1, 65 // G + 1))
         act = acts[i % len(acts)]
-        out.append((f"c{i}_{dt}_T{T}_{d_in}x{d_out}_r{r}_g{G}_{act}", T, d_in, d_out, r, G, dt, act, 500 + i))
+        out.append((f"c{tag}{i}_{dt}_T{T}_{d_in}x{d_out}_r{r}_g{G}_{act}", T, d_in, d_out, r, G, dt, act,
+                    500 + i))
     return out
 
 
@@ -42,7 +44,8 @@ FIXED = [
     ("fixed_bf16_T256_192x160_r8_g4_tanh_m", 256, 192, 160, 8, 4, "bf16", "tanh_m", 749),
     ("fixed_bf16_T256_96x128_r16_g4_tanh_m", 256, 96, 128, 16, 4, "bf16", "tanh_m", 727),
 ]
-CASES = _cases() + FIXED
+# the 3-layer CosNet (r <= 128 on both paths) over shapes of its own
+CASES = _cases() + _cases(8, 2027, ["cosnet3"], 128, "l3_") + FIXED
 # A single float32 token whose dW_up row is the relative error of one tanh
 # value near zero: plain float32 evaluation misses the bound there
 # (tests/test_conditioning.py), so the row metric is expected to fail.
@@ -63,7 +66,8 @@ def test_fuzz_parity(case):
     assert torch.cuda.is_available(), "GPU tests need an MI355X"
     name, T, d_in, d_out, r, G, dt, act, seed = case
     for attempt in range(50):
-        p = inp.draw_projection(name, T, d_in, d_out, r, dt, seed=seed + 1000 * attempt, bias_std=0.5, groups=G)
+        p = inp.draw_projection(name, T, d_in, d_out, r, dt, seed=seed + 1000 * attempt, bias_std=0.5, groups=G,
+                                layers=max(2, noble.layers(act)))
         if not act.startswith("leaky") or kink_margin(p, act) > 1.0:
             break
     else:

@@ -147,3 +147,22 @@ def test_init_params_validation_makes_no_hip_call():
     assert L.noble_init_params(ctypes.byref(d), ctypes.byref(rc), 1, *bad, None) == MISAL
     d = noble.make_desc(0, 64, 64, 20, noble.NOBLE_BF16)
     assert L.noble_init_params(ctypes.byref(d), ctypes.byref(rc), 1, *none, None) == SHAPE
+
+
+def test_init_values_three_layer_form_continues_the_streams():
+    """The 3-layer form's M [2, r, r] and omega2 / phi2 [2, r]: the first
+    halves are the two-layer draws, the second halves continue the same
+    streams (and the same distributions)."""
+    two = rec.init_values(256, 128, 32, seed=9, dtype="bf16")
+    three = rec.init_values(256, 128, 32, seed=9, dtype="bf16", layers=3)
+    assert three["M"].shape == (2, 32, 32) and three["omega2"].shape == (2, 32)
+    np.testing.assert_array_equal(three["M"][0], two["M"])
+    for k in ("omega2", "phi2"):
+        np.testing.assert_array_equal(three[k][0], two[k])
+    for k in ("W", "W_down", "W_up", "omega1", "phi1", "b"):
+        np.testing.assert_array_equal(three[k], two[k])
+    assert not np.array_equal(three["M"][1], three["M"][0])
+    assert np.all(np.abs(three["M"][1]) <= np.sqrt(3 / 32) * (1 + 2.0 ** -8))   # bf16 rounding
+    assert np.all((three["omega2"][1] >= 0.8) & (three["omega2"][1] <= 1.2))
+    g = rec.init_values(64, 96, 8, seed=9, dtype="f32", groups=3, layers=3)
+    assert g["M"].shape == (2, 3, 8, 8) and g["phi2"].shape == (2, 24)
