@@ -279,6 +279,11 @@ int64_t max_gemm_blocks(const noble_linear_desc* d) {
     return (int64_t)UINT32_MAX / (d->dtype == NOBLE_BF16 ? kDmaThreads : kThreads);
 }
 
+// bf16 products (256-square tiles) of at most 128 rows without column sums
+// split each K chunk between the two M halves of the workgroup's waves
+// (gemm_bf16_kernel), which takes about half the MFMA time of a full tile.
+bool kpair_tile(int tile, int64_t M, bool bsum) { return tile == 256 && M <= 128 && !bsum; }
+
 struct Batch {
     GemmBatch b{};
     int blocks = 0;
@@ -306,6 +311,7 @@ struct Batch {
         p.nblocks = p.tiles_m * p.tiles_n * split;
         p.out_f32 = out_f32 ? 1 : 0;
         p.atomic = split > 1 && !partials ? 1 : 0;
+        p.kpair = kpair_tile(tile, M, bsum != nullptr) ? 1 : 0;
         blocks += p.nblocks;
     }
 };
@@ -316,7 +322,7 @@ struct Batch {
 // workgroup per CU).  A workgroup costs kWgFixed plus kWgChunk per 64-token
 // chunk (fit to the measured time of the forward GEMM against K: prologue,
 // epilogue stores and ramp are about 12 us per tile, a chunk 1.45 us).
-double launch_makespan(const std::vector<std::pair<int, int>>& wgs) {
+double launch_makespan(const std::vector<std::pair<int, double>>& wgs) {
     constexpr double kWgFixed = 12.0, kWgChunk = 1.45;
     // CU free times with their multiplicities.  The workgroups of one group
     // are identical, so handing all the CUs that free first to as many of
@@ -418,9 +424,16 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
         constexpr double kPartialBytesPerUs = 5.0e6;
         const int64_t R = rank_total(d), dog = group_dout(d), hl = hilo(d);
         const int G = ngroups(d);
-        const int rank_tiles = cdiv(din, tile) * cdiv(hl * R, tile) +
-                               G * (cdiv(r, tile) * cdiv(dog, tile) +
-                                    (int)n_mix(d) * cdiv(hl * r, tile) * cdiv(hl * r, tile));
+        // the rank products in launch order (dW_down, then per group dW_up
+        // and dM): tiles and whether they run as kpair tiles (half the chunk time)
+        std::vector<std::pair<int, bool>> rank;
+        rank.push_back({cdiv(din, tile) * cdiv(hl * R, tile), kpair_tile(tile, din, false)});
+        for (int g = 0; g < G; ++g) {
+            rank.push_back({cdiv(r, tile) * cdiv(dog, tile), kpair_tile(tile, r, false)});
+            rank.push_back({(int)n_mix(d) * cdiv(hl * r, tile) * cdiv(hl * r, tile), kpair_tile(tile, hl * r, false)});
+        }
+        int rank_tiles = 0;
+        for (const auto& e : rank) rank_tiles += e.first;
         const RankParts rp = rank_parts(d);
         double best = -1.0;
         for (int sw : {1, 2, 3, 4, 6, 8, 12, 16}) {
@@ -432,7 +445,9 @@ WgradPlan plan_wgrad_uncached(const noble_linear_desc* d) {
                 const double fp = (double)rank_folded_pieces(d, sr), up = sr > 1 ? sr : 0;
                 const double rank_traffic = 4.0 * ((fp > 0 ? 2.0 * fp + 1 : 0) * rp.folded +
                                                    (up > 0 ? 2.0 * up + 1 : 0) * rp.unfolded);
-                const double t = launch_makespan({{tiles * sw, cdiv(nkT, sw)}, {rank_tiles * sr, cdiv(nkT, sr)}}) +
+                std::vector<std::pair<int, double>> wgs{{tiles * sw, (double)cdiv(nkT, sw)}};
+                for (const auto& e : rank) wgs.push_back({e.first * sr, cdiv(nkT, sr) / (e.second ? 2.0 : 1.0)});
+                const double t = launch_makespan(wgs) +
                                  (sw > 1 ? (2.0 * sw + 1) * (double)MN * 4 / kPartialBytesPerUs : 0.0) +
                                  rank_traffic / kPartialBytesPerUs;
                 if (best < 0 || t < best) {

@@ -45,7 +45,8 @@ struct GemmProblem {
     int nblocks;        // tiles_m * tiles_n * split
     int out_f32;        // C holds float (1) or the storage type (0)
     int atomic;         // atomicAdd into a zeroed float C
-    int pad_;
+    int kpair;          // bf16 path, M <= 128, no bsum: the two M halves of the
+                        // workgroup's waves split each K chunk instead
     int64_t pstride;    // elements between the partials of consecutive pieces
 };
 

@@ -201,7 +201,14 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
     // w + 4 share a SIMD, and this way they differ in both the M half and the
     // N half: a tile that is only half inside M or N (the rank-r products,
     // r <= 128) leaves every SIMD one live wave instead of idling two SIMDs.
-    const int wm0 = (wave / kDmaWN) * WTM, wn0 = ((wave % kDmaWN) ^ ((wave / kDmaWN) * (kDmaWN / 2))) * WTN;
+    // A problem with M <= 128 (`kpair`: W_up's gradient, r rows) instead gives
+    // both halves the rows 0..127: half w / 4 takes K steps 2 (w / 4) and
+    // 2 (w / 4) + 1 of every chunk, and the second half's sums are added to
+    // the first's through LDS at the end, so the half-empty tile costs about
+    // half the MFMA time.
+    const bool kpair = P.kpair != 0;
+    const int khalf = wave / kDmaWN;
+    const int wm0 = kpair ? 0 : khalf * WTM, wn0 = ((wave % kDmaWN) ^ (khalf * (kDmaWN / 2))) * WTN;
     static_assert(kDmaWM == 2, "the N-quarter swizzle pairs two M halves");
     const int r32 = lane & 31, h = lane >> 5;
 
@@ -227,6 +234,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
                 __syncthreads();
             }
         }
+        if (kpair) __syncthreads();   // the hand-over of the second half's sums
         return;
     }
 
@@ -238,7 +246,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const bool do_bsum = HAS_BSUM && (P.bsum != nullptr) && tm == 0 && wm0 == 0;
+    const bool do_bsum = HAS_BSUM && (P.bsum != nullptr) && tm == 0 && wm0 == 0 && !kpair;
     float bs[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) bs[j] = 0.f;
@@ -254,9 +262,12 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
 
-        // Multiply chunk kc from `cur` while chunk kc + 1 streams into `nxt`.
-        auto chunk = [&](int kc, const char* cur, char* nxt, auto bs_c) __attribute__((always_inline)) {
+        // Multiply chunk kc from `cur` while chunk kc + 1 streams into `nxt`:
+        // all four K steps, or (NS = 2, kpair) the two of this wave's half.
+        auto chunk = [&](int kc, const char* cur, char* nxt, auto bs_c, auto ns_c) __attribute__((always_inline)) {
             constexpr bool BS = decltype(bs_c)::value;
+            constexpr int NS = decltype(ns_c)::value;
+            const int sb = NS == 4 ? 0 : 2 * khalf;
             const char* ldsA = cur;
             const char* ldsB = cur + TILE;
             if (kc + 1 < kc1) {
@@ -269,18 +280,18 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
             constexpr int NMFMA = TM * TN;
             u32x4 a[2][TM], b[2][TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a[0][i] = fa.read(ldsA, i, 0);
+            for (int i = 0; i < TM; ++i) a[0][i] = fa.read(ldsA, i, sb);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b[0][j] = fb.read(ldsB, j, 0);
+            for (int j = 0; j < TN; ++j) b[0][j] = fb.read(ldsB, j, sb);
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
+            for (int s = 0; s < NS; ++s) {
                 const int cb = s & 1, nb = cb ^ 1;
                 __builtin_amdgcn_sched_barrier(0);
-                if (s + 1 < 4) {
+                if (s + 1 < NS) {
 #pragma unroll
-                    for (int i = 0; i < TM; ++i) a[nb][i] = fa.read(ldsA, i, s + 1);
+                    for (int i = 0; i < TM; ++i) a[nb][i] = fa.read(ldsA, i, sb + s + 1);
 #pragma unroll
-                    for (int j = 0; j < TN; ++j) b[nb][j] = fb.read(ldsB, j, s + 1);
+                    for (int j = 0; j < TN; ++j) b[nb][j] = fb.read(ldsB, j, sb + s + 1);
                 }
                 if constexpr (BS) {
 #pragma unroll
@@ -292,7 +303,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j) mma32<uint16_t>(acc[i][j], a[cb][i], b[cb][j]);
-                if (s + 1 < 4) {
+                if (s + 1 < NS) {
 #pragma unroll
                     for (int qq = 0; qq < NMFMA; ++qq) {
                         if (qq < NREAD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
@@ -303,22 +314,61 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             __syncthreads();
         };
-        auto run = [&](auto bs_c) __attribute__((always_inline)) {
+        auto run = [&](auto bs_c, auto ns_c) __attribute__((always_inline)) {
             int kc = kc0;
             for (; kc + 1 < kc1; kc += 2) {
-                chunk(kc, lds0, lds1, bs_c);
-                chunk(kc + 1, lds1, lds0, bs_c);
+                chunk(kc, lds0, lds1, bs_c, ns_c);
+                chunk(kc + 1, lds1, lds0, bs_c, ns_c);
             }
-            if (kc < kc1) chunk(kc, lds0, lds1, bs_c);
+            if (kc < kc1) chunk(kc, lds0, lds1, bs_c, ns_c);
         };
-        if constexpr (HAS_BSUM) {
+        using Four = std::integral_constant<int, 4>;
+        using Two = std::integral_constant<int, 2>;
+        if (kpair)
+            run(std::false_type{}, Two{});
+        else if constexpr (HAS_BSUM) {
             if (do_bsum)
-                run(std::true_type{});
+                run(std::true_type{}, Four{});
             else
-                run(std::false_type{});
+                run(std::false_type{}, Four{});
         } else {
-            run(std::false_type{});
+            run(std::false_type{}, Four{});
         }
+    }
+
+    if (kpair) {
+        // Hand-over: the waves of the second half store their sums in the
+        // (now idle) operand stages, 32 KB per N quarter, lane-interleaved
+        // 16-byte vectors; the first half adds them.  The last chunk's barrier
+        // has retired every fragment read of the stages.
+        const int qn = wn0 / WTN;
+        char* hand = (qn < 2 ? lds0 : lds1) + (qn & 1) * (STAGE / 2);
+        static_assert(TM * TN * 16 * 4 * 64 == STAGE / 2, "one wave's sums fill half a stage");
+        if (khalf == 1) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int v4 = 0; v4 < 4; ++v4) {
+                        f32x4 t;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) t[e] = acc[i][j][4 * v4 + e];
+                        *reinterpret_cast<f32x4*>(hand + (((i * TN + j) * 4 + v4) * 64 + lane) * 16) = t;
+                    }
+        }
+        __syncthreads();
+        if (khalf == 1) return;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int v4 = 0; v4 < 4; ++v4) {
+                    const f32x4 t = *reinterpret_cast<const f32x4*>(hand + (((i * TN + j) * 4 + v4) * 64 + lane) * 16);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[i][j][4 * v4 + e] += t[e];
+                }
     }
 
     if (do_bsum) {

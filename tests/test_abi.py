@@ -97,7 +97,7 @@ def _makespan(groups):
     cu, end = [0.0] * 256, 0.0
     for n, ch in groups:
         for _ in range(n):
-            t = heapq.heappop(cu) + 12.0 + 1.45 * ch
+            t = heapq.heappop(cu) + (12.0 + 1.45 * ch)
             heapq.heappush(cu, t)
             end = max(end, t)
     return end
@@ -129,7 +129,12 @@ def _wgrad_split(T, di, do, r, bk, tile=256, groups=1, hl=2, nm=1):
     if r == 0:
         return _split_partials(tiles, nk, di * do), 1
     G, R, dog = groups, groups * r, do // groups
-    rank_tiles = cd(di, tile) * cd(hl * R, tile) + G * (cd(r, tile) * cd(dog, tile) + nm * cd(hl * r, tile) ** 2)
+    # rank products in launch order; bf16 products of at most 128 rows split
+    # each K chunk between the workgroup's two halves (half the chunk time)
+    kp = lambda m: tile == 256 and m <= 128
+    rank = [(cd(di, tile) * cd(hl * R, tile), kp(di))]
+    for _ in range(G):
+        rank += [(cd(r, tile) * cd(dog, tile), kp(r)), (nm * cd(hl * r, tile) ** 2, kp(hl * r))]
     folded, unfolded = _rank_parts(di, do, r, groups, hl, nm)
     best, pick = None, (1, 1)
     cands = (1, 2, 3, 4, 6, 8, 12, 16)
@@ -142,7 +147,7 @@ def _wgrad_split(T, di, do, r, bk, tile=256, groups=1, hl=2, nm=1):
             fp = (max(sr, 1) if hl == 2 else (sr if sr > 1 else 0))
             up = sr if sr > 1 else 0
             traffic = 4.0 * (((2.0 * fp + 1) * folded if fp else 0.0) + ((2.0 * up + 1) * unfolded if up else 0.0))
-            t = (_makespan([(tiles * sw, cd(nk, sw)), (rank_tiles * sr, cd(nk, sr))])
+            t = (_makespan([(tiles * sw, cd(nk, sw))] + [(n * sr, cd(nk, sr) / (2.0 if h else 1.0)) for n, h in rank])
                  + ((2.0 * sw + 1) * di * do * 4 / 5.0e6 if sw > 1 else 0.0)
                  + traffic / 5.0e6)
             if best is None or t < best:
