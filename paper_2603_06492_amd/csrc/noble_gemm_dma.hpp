@@ -246,7 +246,11 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const bool do_bsum = HAS_BSUM && (P.bsum != nullptr) && tm == 0 && wm0 == 0 && !kpair;
+    // db's column sums ride on the B fragments of the waves of M half 0.  The
+    // tiles of one column block share them out: tile row tm sums its own
+    // contiguous share of the K chunks, so that no tile row carries all of
+    // that work (a launch ends with its slowest tile).
+    const bool do_bsum = HAS_BSUM && (P.bsum != nullptr) && wm0 == 0 && !kpair;
     float bs[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) bs[j] = 0.f;
@@ -322,15 +326,31 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
             }
             if (kc < kc1) chunk(kc, lds0, lds1, bs_c, ns_c);
         };
+        // chunks [b, e) of the piece (chunk kc uses stage (kc - kc0) % 2)
+        auto run_range = [&](int b, int e, auto bs_c) __attribute__((always_inline)) {
+            using Four = std::integral_constant<int, 4>;
+            int kc = b;
+            if (kc < e && ((kc - kc0) & 1)) chunk(kc++, lds1, lds0, bs_c, Four{});
+            for (; kc + 1 < e; kc += 2) {
+                chunk(kc, lds0, lds1, bs_c, Four{});
+                chunk(kc + 1, lds1, lds0, bs_c, Four{});
+            }
+            if (kc < e) chunk(kc, lds0, lds1, bs_c, Four{});
+        };
         using Four = std::integral_constant<int, 4>;
         using Two = std::integral_constant<int, 2>;
         if (kpair)
             run(std::false_type{}, Two{});
         else if constexpr (HAS_BSUM) {
-            if (do_bsum)
-                run(std::true_type{}, Four{});
-            else
+            if (do_bsum) {
+                const int n = kc1 - kc0;
+                const int sb = kc0 + (int)((int64_t)n * tm / P.tiles_m), se = kc0 + (int)((int64_t)n * (tm + 1) / P.tiles_m);
+                run_range(kc0, sb, std::false_type{});
+                run_range(sb, se, std::true_type{});
+                run_range(se, kc1, std::false_type{});
+            } else {
                 run(std::false_type{}, Four{});
+            }
         } else {
             run(std::false_type{}, Four{});
         }
