@@ -284,10 +284,24 @@ int64_t max_gemm_blocks(const noble_linear_desc* d) {
 // (gemm_bf16_kernel), which takes about half the MFMA time of a full tile.
 bool kpair_tile(int tile, int64_t M, bool bsum) { return tile == 256 && M <= 128 && !bsum; }
 
+// A bf16 launch of 256 x 256 tiles that fills its last wave of 256 CUs
+// poorly runs as 256 x 128 `npair` tiles (gemm_bf16_kernel): chosen when
+// their waves, weighted by kHalfTileCost, are fewer.  A half tile does half
+// the MFMA work but loads three quarters of the operand bytes per chunk;
+// measured on the 250M and ViT layers it costs about 0.8 of a full tile
+// (so 2 waves of full tiles beat 3 of half tiles, 1 of half tiles beats 1 of
+// full ones).
+constexpr double kHalfTileCost = 0.8;
+bool npair_pays(int64_t full_blocks, int64_t half_blocks) {
+    const int64_t wf = (full_blocks + 255) / 256, wh = (half_blocks + 255) / 256;
+    return half_blocks < (1 << 22) && (double)wh * kHalfTileCost < 0.95 * (double)wf;
+}
+
 struct Batch {
     GemmBatch b{};
     int blocks = 0;
-    int tile = 256;   // square output tile
+    int tile = 256;      // square output tile
+    bool npair = false;  // bf16: 256 x 128 tiles (set before adding problems)
     // With `partials`, each of the `split` pieces stores its float32 partial
     // [M][ldc] at partials + piece * M * ldc (also for split = 1); without,
     // split > 1 pieces add atomically into C.
@@ -306,12 +320,13 @@ struct Batch {
         p.nk = nk;
         p.split = split;
         p.tiles_m = cdiv(M, tile);
-        p.tiles_n = cdiv(N, tile);
+        p.tiles_n = cdiv(N, npair ? tile / 2 : tile);
         p.tile_begin = blocks;
         p.nblocks = p.tiles_m * p.tiles_n * split;
         p.out_f32 = out_f32 ? 1 : 0;
         p.atomic = split > 1 && !partials ? 1 : 0;
-        p.kpair = kpair_tile(tile, M, bsum != nullptr) ? 1 : 0;
+        p.npair = npair ? 1 : 0;
+        p.kpair = !npair && kpair_tile(tile, M, bsum != nullptr) ? 1 : 0;
         blocks += p.nblocks;
     }
 };
@@ -508,6 +523,8 @@ noble_status check_grids(const noble_linear_desc* d) {
     const int64_t hl = hilo(d);
     const int64_t wgrad =
         tiles(din, dout) + (r > 0 ? tiles(din, hl * R) + G * (tiles(r, dog) + n_mix(d) * tiles(hl * r, hl * r)) : 0);
+    // (an npair launch is chosen only when it has fewer weighted waves: at
+    // most about twice the blocks of a launch of a few waves)
     return std::max({fwd, dx, wgrad}) <= max_gemm_blocks(d) ? NOBLE_OK : NOBLE_ERR_BAD_SHAPE;
 }
 
@@ -726,6 +743,8 @@ noble_status fwd_impl(const noble_linear_desc* d, const void* x, const void* W, 
     const int nk = nk1 + (r > 0 ? cdiv(r, GBK) : 0);
     Batch bt;
     bt.tile = gemm_tile<E>();
+    if (sizeof(E) == 2)
+        bt.npair = npair_pays((int64_t)G * cdiv(T, 256) * cdiv(dog, 256), (int64_t)G * cdiv(T, 256) * cdiv(dog, 128));
     for (int g = 0; g < G; ++g) {
         const E* Wg = static_cast<const E*>(W) + g * dog;
         const char* C2g = C2s + g * r * (int64_t)ES;
@@ -857,6 +876,7 @@ noble_status bwd_impl(const noble_linear_desc* d, const void* dy, const void* x,
         const int nk = nk1 + (r > 0 ? cdiv(R, GBK) : 0);
         Batch bt;
         bt.tile = gemm_tile<E>();
+        if (sizeof(E) == 2) bt.npair = npair_pays((int64_t)cdiv(T, 256) * cdiv(din, 256), (int64_t)cdiv(T, 256) * cdiv(din, 128));
         bt.add(operand2(seg(dy, dout, dout), seg(dHs, hl * R, R), nk1, T), operand2(seg(W, dout, dout), seg(Wd, R, R), nk1, din),
                (int)T, (int)din, nk, dx, din, sizeof(E) == 4, nullptr, nullptr, 1);
         NOBLE_TRY((launch_gemm<E, true, true>(bt, st)));

@@ -47,6 +47,9 @@ struct GemmProblem {
     int atomic;         // atomicAdd into a zeroed float C
     int kpair;          // bf16 path, M <= 128, no bsum: the two M halves of the
                         // workgroup's waves split each K chunk instead
+    int npair;          // bf16 path: 256 x 128 output tiles, the waves of the
+                        // two N halves splitting each K chunk (no bsum)
+    int pad2_;
     int64_t pstride;    // elements between the partials of consecutive pieces
 };
 

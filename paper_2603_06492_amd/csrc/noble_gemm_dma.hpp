@@ -190,7 +190,8 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
     const int first_m = grp * kGroupM;
     const int gsz = min(P.tiles_m - first_m, kGroupM);
     const int tm = first_m + in % gsz, tn = in / gsz;
-    const int m0 = tm * BM, n0 = tn * BN;
+    const bool kpair = P.kpair != 0, npair = P.npair != 0;
+    const int m0 = tm * BM, n0 = tn * (npair ? BN / 2 : BN);
     const int kc0 = (int)((int64_t)P.nk * piece / P.split);
     const int kc1 = (int)((int64_t)P.nk * (piece + 1) / P.split);
 
@@ -205,10 +206,15 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
     // both halves the rows 0..127: half w / 4 takes K steps 2 (w / 4) and
     // 2 (w / 4) + 1 of every chunk, and the second half's sums are added to
     // the first's through LDS at the end, so the half-empty tile costs about
-    // half the MFMA time.
-    const bool kpair = P.kpair != 0;
+    // half the MFMA time.  `npair` tiles are 256 x 128 (twice the tiles of a
+    // launch that would under-fill the CUs): the wave that would take N
+    // quarter q >= 2 takes quarter q - 2 and K steps 2 and 3, its partner
+    // (same M half, quarter q - 2) steps 0 and 1, with the same hand-over.
     const int khalf = wave / kDmaWN;
-    const int wm0 = kpair ? 0 : khalf * WTM, wn0 = ((wave % kDmaWN) ^ (khalf * (kDmaWN / 2))) * WTN;
+    const int qw = (wave % kDmaWN) ^ (khalf * (kDmaWN / 2));
+    const int wm0 = kpair ? 0 : khalf * WTM, wn0 = (npair ? (qw & 1) : qw) * WTN;
+    const bool split2 = kpair || npair;               // a K-split pair of waves per output block
+    const int kh = kpair ? khalf : (npair ? qw >> 1 : 0);   // this wave's K half
     static_assert(kDmaWM == 2, "the N-quarter swizzle pairs two M halves");
     const int r32 = lane & 31, h = lane >> 5;
 
@@ -217,9 +223,15 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
     // same barrier sequence (one after the first chunk's loads, one per chunk)
     // as the loop below, without fragment reads, MFMAs or stores.  Kept apart
     // from that loop: a test inside it slowed the full tiles by 2-4%.
+    // B rows of an npair tile stop at its 128 columns (the rest read nothing).
+    auto b_operand = [&]() {
+        Operand o = P.B;
+        if (npair) o.rows = min(o.rows, n0 + BN / 2);
+        return o;
+    };
     if (m0 + wm0 >= P.M || n0 + wn0 >= P.N) {
         if (kc0 < kc1) {
-            const Operand opA = P.A, opB = P.B;
+            const Operand opA = P.A, opB = b_operand();
             dma_tile<AK, NW>(opA, m0, kc0, lds0, wave, lane);
             dma_tile<BKM, NW>(opB, n0, kc0, lds0 + TILE, wave, lane);
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -234,7 +246,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
                 __syncthreads();
             }
         }
-        if (kpair) __syncthreads();   // the hand-over of the second half's sums
+        if (split2) __syncthreads();   // the hand-over of the second half's sums
         return;
     }
 
@@ -250,7 +262,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
     // tiles of one column block share them out: tile row tm sums its own
     // contiguous share of the K chunks, so that no tile row carries all of
     // that work (a launch ends with its slowest tile).
-    const bool do_bsum = HAS_BSUM && (P.bsum != nullptr) && wm0 == 0 && !kpair;
+    const bool do_bsum = HAS_BSUM && (P.bsum != nullptr) && wm0 == 0 && !split2;
     float bs[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) bs[j] = 0.f;
@@ -260,7 +272,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
         const FragAddr<BKM, TN> fb(wn0, lane);
         // Local copies of the operand descriptions: read once from the kernel
         // arguments instead of once per chunk.
-        const Operand opA = P.A, opB = P.B;
+        const Operand opA = P.A, opB = b_operand();
         dma_tile<AK, NW>(opA, m0, kc0, lds0, wave, lane);
         dma_tile<BKM, NW>(opB, n0, kc0, lds0 + TILE, wave, lane);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -271,7 +283,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
         auto chunk = [&](int kc, const char* cur, char* nxt, auto bs_c, auto ns_c) __attribute__((always_inline)) {
             constexpr bool BS = decltype(bs_c)::value;
             constexpr int NS = decltype(ns_c)::value;
-            const int sb = NS == 4 ? 0 : 2 * khalf;
+            const int sb = NS == 4 ? 0 : 2 * kh;
             const char* ldsA = cur;
             const char* ldsB = cur + TILE;
             if (kc + 1 < kc1) {
@@ -339,7 +351,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
         };
         using Four = std::integral_constant<int, 4>;
         using Two = std::integral_constant<int, 2>;
-        if (kpair)
+        if (split2)
             run(std::false_type{}, Two{});
         else if constexpr (HAS_BSUM) {
             if (do_bsum) {
@@ -356,15 +368,16 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
         }
     }
 
-    if (kpair) {
-        // Hand-over: the waves of the second half store their sums in the
-        // (now idle) operand stages, 32 KB per N quarter, lane-interleaved
-        // 16-byte vectors; the first half adds them.  The last chunk's barrier
-        // has retired every fragment read of the stages.
-        const int qn = wn0 / WTN;
-        char* hand = (qn < 2 ? lds0 : lds1) + (qn & 1) * (STAGE / 2);
+    if (split2) {
+        // Hand-over: the waves of the second K half store their sums in the
+        // (now idle) operand stages, 32 KB per output block (kpair: per N
+        // quarter; npair: per M half and N quarter), lane-interleaved 16-byte
+        // vectors; the first K half adds them.  The last chunk's barrier has
+        // retired every fragment read of the stages.
+        const int reg = kpair ? wn0 / WTN : 2 * khalf + (qw & 1);
+        char* hand = (reg < 2 ? lds0 : lds1) + (reg & 1) * (STAGE / 2);
         static_assert(TM * TN * 16 * 4 * 64 == STAGE / 2, "one wave's sums fill half a stage");
-        if (khalf == 1) {
+        if (kh == 1) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -378,7 +391,7 @@ __global__ __launch_bounds__(kDmaThreads, 1) void gemm_bf16_kernel(GemmBatch bat
                     }
         }
         __syncthreads();
-        if (khalf == 1) return;
+        if (kh == 1) return;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
